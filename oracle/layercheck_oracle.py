@@ -1,0 +1,332 @@
+"""CPU oracle for the LayerCheck decision step -- TEST INFRASTRUCTURE ONLY.
+
+Only the tests, the package's smoke check and the benchmark's CPU-baseline leg
+may import this module.  It is a plain, slow, obviously-correct restatement
+of the paper's method (Section 3.2 "Layer-wise Monitoring and Checkpointing",
+Section 3.3 "Bounding Mixed-Timestamp Staleness", Section 3.5 "Recovery from
+LayerCheck Checkpoints", Equations 1-5 and 8) on host numpy arrays, in fp64.
+It shares no code with the HIP library and imports nothing from it.
+
+What it computes, in the paper's notation:
+
+* Eq. 1: for layer l, u_l(t) = mean|W_l(t) - W_l(t-1)| / (mean|W_l(t-1)| + eps_w),
+  the means taken jointly over every element of every tensor of the layer.
+  W_l(t-1) is the caller-held shadow copy S of the weights.
+* Eq. 2: Delta_l <- Delta_l + u_l(t)   (ACCUM mode, the paper's rule).
+  SNAPSHOT mode instead keeps S equal to the last *persisted* weights and sets
+  Delta_l <- u_l(t) (distance to the last persisted version).
+* Eq. 3 and the LR adaptation: persist l if Delta_l >= K(t), K(t) = K0_l * s(lr(t));
+  the caller passes s(lr(t)) as ``lr_scale``.
+* Section 3.3 staleness guard: persist l also when t - t_l >= S_max.
+* Eq. 4: a persisted layer gets Delta_l <- 0 and t_l <- t.
+* Section 3.3 reporting metric: size-weighted staleness sum_l n_l (t - t_l) / sum_l n_l.
+* Section 3.1 / Eq. 8 recovery: each layer takes its newest persisted record
+  with step <= t_fail; the base full checkpoint is simply a version holding
+  every layer.
+
+Readings where the paper is silent (each is listed with its reason in the
+design notes): eps_w is added to the *mean* exactly as Eq. 1 is typeset; the
+comparison operators are ">=" for both rules; the payload format (records of
+selected layers in ascending layer id, each record [W | master | m | v],
+every (array, tensor) block zero-padded to a multiple of 256 bytes) is this
+implementation's own, since the paper only says a DeepSpeed-compatible
+checkpoint is assembled; after recovery Delta_l = 0, t_l = the restored step
+and S = W.
+
+Parity status: every function here is pinned by the ``-m "not gpu"`` tests
+(closed forms, exact-rational brute force, invariants, the paper's Table 1
+record-size and layer-count figures); no function is "parity unpinned".
+"""
+from __future__ import annotations
+
+from dataclasses import dataclass
+from typing import List, Optional, Sequence
+
+import numpy as np
+
+# Status codes (same numbering as the C interface, so tests can compare).
+LC_OK = 0
+LC_ERR_INVALID_ARG = 1
+LC_ERR_BAD_STATE = 2
+LC_ERR_CAPACITY = 3
+LC_ERR_NO_VERSION = 4
+
+DT_BF16 = 1
+DT_F32 = 2
+MODE_ACCUM = 0
+MODE_SNAPSHOT = 1
+
+PAD = 256  # block alignment inside a packed record (this implementation's format)
+
+
+class OracleError(Exception):
+    def __init__(self, code: int, msg: str):
+        super().__init__(msg)
+        self.code = code
+
+
+@dataclass
+class OSegment:
+    """One tensor of one layer, as host arrays (bf16 weights are raw uint16)."""
+    layer: int
+    weight: np.ndarray
+    shadow: np.ndarray
+    master: Optional[np.ndarray]
+    exp_avg: np.ndarray
+    exp_avg_sq: np.ndarray
+
+    @property
+    def numel(self) -> int:
+        return int(self.weight.size)
+
+
+def widen(values: np.ndarray, dtype: int) -> np.ndarray:
+    """Exact fp64 value of each stored weight (bf16 is the top half of an fp32)."""
+    if dtype == DT_BF16:
+        return (values.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return values.astype(np.float64)
+
+
+def layer_update_score(weights: Sequence[np.ndarray], previous: Sequence[np.ndarray],
+                       dtype: int, eps_w: float):
+    """Eq. 1 for one layer.  Returns (sum|W-S|, sum|S|, n, u)."""
+    A = 0.0
+    B = 0.0
+    n = 0
+    for w, s in zip(weights, previous):
+        x = widen(w, dtype)
+        y = widen(s, dtype)
+        A += float(np.sum(np.abs(x - y)))
+        B += float(np.sum(np.abs(y)))
+        n += int(w.size)
+    with np.errstate(divide="ignore", invalid="ignore"):
+        u = float(np.float64(A / n) / np.float64(B / n + eps_w))
+    return A, B, n, u
+
+
+def padded(nbytes: int) -> int:
+    return (nbytes + PAD - 1) // PAD * PAD
+
+
+def _arrays_in_record(has_master: bool) -> List[str]:
+    return ["weight"] + (["master"] if has_master else []) + ["exp_avg", "exp_avg_sq"]
+
+
+def record_bytes(seg_numels: Sequence[int], weight_itemsize: int, has_master: bool) -> int:
+    """Size of one layer's packed record: every (array, tensor) block padded."""
+    total = 0
+    for arr in _arrays_in_record(has_master):
+        item = weight_itemsize if arr == "weight" else 4
+        for n in seg_numels:
+            total += padded(n * item)
+    return total
+
+
+class LayerCheckOracle:
+    """Stateful mirror of the decision step on host arrays."""
+
+    def __init__(self, segments: Sequence[OSegment], n_layers: int, weight_dtype: int,
+                 has_master: bool, mode: int, k0: Sequence[float], s_max: int,
+                 eps_w: float = 1e-8, t_base: int = 0):
+        if n_layers <= 0 or len(segments) == 0:
+            raise OracleError(LC_ERR_INVALID_ARG, "empty layout")
+        if weight_dtype not in (DT_BF16, DT_F32) or mode not in (MODE_ACCUM, MODE_SNAPSHOT):
+            raise OracleError(LC_ERR_INVALID_ARG, "bad dtype or mode")
+        if len(k0) != n_layers or s_max < 1 or not (eps_w >= 0.0):
+            raise OracleError(LC_ERR_INVALID_ARG, "bad thresholds")
+        self.by_layer: List[List[OSegment]] = [[] for _ in range(n_layers)]
+        last = -1
+        for s in segments:
+            if not (0 <= s.layer < n_layers) or s.layer < last or s.numel == 0:
+                raise OracleError(LC_ERR_INVALID_ARG, "segments must be grouped by ascending layer")
+            if (s.master is None) == has_master:
+                raise OracleError(LC_ERR_INVALID_ARG, "master presence mismatch")
+            last = s.layer
+            self.by_layer[s.layer].append(s)
+        if any(len(g) == 0 for g in self.by_layer):
+            raise OracleError(LC_ERR_INVALID_ARG, "layer without tensors")
+        self.N = n_layers
+        self.dtype = weight_dtype
+        self.itemsize = 2 if weight_dtype == DT_BF16 else 4
+        self.has_master = has_master
+        self.mode = mode
+        self.k0 = [float(k) for k in k0]
+        self.s_max = int(s_max)
+        self.eps_w = float(eps_w)
+        self.t_base = int(t_base)
+        self.n = [sum(s.numel for s in g) for g in self.by_layer]
+        self.R = [record_bytes([s.numel for s in g], self.itemsize, has_master) for g in self.by_layer]
+        # Section 3.2: accumulators start at 0; every layer counts as persisted
+        # by the base full checkpoint at t_base; the shadow starts equal to W.
+        self.delta = [0.0] * n_layers
+        self.u = [0.0] * n_layers
+        self.t_last = [self.t_base] * n_layers
+        for g in self.by_layer:
+            for s in g:
+                s.shadow[...] = s.weight
+        self.last_step = self.t_base
+        self.scored_step: Optional[int] = None
+        # the base version is pending: every layer selected at t_base
+        self.mask = np.ones(n_layers, dtype=np.uint8)
+        self.mask_step = self.t_base
+        self.unpacked = set(range(n_layers))
+
+    # -- Eq. 1-2 -------------------------------------------------------------
+    def score(self, step: int) -> None:
+        if step <= self.last_step:
+            raise OracleError(LC_ERR_BAD_STATE, "decision steps must strictly increase")
+        if self.mode == MODE_SNAPSHOT and self.unpacked:
+            raise OracleError(LC_ERR_BAD_STATE, "previous selection not fully packed")
+        for l, g in enumerate(self.by_layer):
+            _, _, _, u = layer_update_score([s.weight for s in g], [s.shadow for s in g],
+                                            self.dtype, self.eps_w)
+            self.u[l] = u
+            if self.mode == MODE_ACCUM:
+                self.delta[l] = self.delta[l] + u
+            else:
+                self.delta[l] = u
+        if self.mode == MODE_ACCUM:
+            # the next step's W(t-1) is this step's W(t)
+            for g in self.by_layer:
+                for s in g:
+                    s.shadow[...] = s.weight
+        self.last_step = step
+        self.scored_step = step
+        self.unpacked = set()
+        self.mask = None
+
+    # -- Eq. 3-5 -------------------------------------------------------------
+    def select(self, step: int, lr_scale: float):
+        if self.scored_step is None or self.scored_step != step:
+            raise OracleError(LC_ERR_BAD_STATE, "select must follow score at the same step")
+        if not (lr_scale > 0.0) or lr_scale == float("inf"):
+            raise OracleError(LC_ERR_INVALID_ARG, "lr_scale must be positive and finite")
+        mask = np.zeros(self.N, dtype=np.uint8)
+        n_forced = 0
+        for l in range(self.N):
+            K = self.k0[l] * lr_scale
+            age = step - self.t_last[l]
+            by_drift = self.delta[l] >= K
+            by_age = age >= self.s_max
+            if by_drift or by_age:
+                mask[l] = 1
+                if not by_drift:
+                    n_forced += 1
+                self.delta[l] = 0.0
+                self.t_last[l] = step
+        self.scored_step = None
+        self.mask = mask
+        self.mask_step = step
+        self.unpacked = {l for l in range(self.N) if mask[l]}
+        return mask.copy(), self.stats(step, mask, n_forced)
+
+    def stats(self, step: int, mask: np.ndarray, n_forced: int) -> dict:
+        ages = [step - self.t_last[l] for l in range(self.N)]
+        num = sum(self.n[l] * ages[l] for l in range(self.N))
+        den = sum(self.n)
+        return {
+            "n_selected": int(mask.sum()),
+            "n_forced": n_forced,
+            "payload_bytes": sum(self.R[l] for l in range(self.N) if mask[l]),
+            "max_age": max(ages),
+            "weighted_age": float(num) / float(den),
+        }
+
+    def resync(self, layer: int, selected: bool) -> None:
+        """Parity-protocol helper: adopt another implementation's decision for
+        a layer whose accumulator lies within the tolerance band of K."""
+        if self.mask is None:
+            raise OracleError(LC_ERR_BAD_STATE, "no selection to resync")
+        if selected and not self.mask[layer]:
+            self.mask[layer] = 1
+            self.delta[layer] = 0.0
+            self.t_last[layer] = self.mask_step
+            self.unpacked.add(layer)
+        elif not selected and self.mask[layer]:
+            raise OracleError(LC_ERR_INVALID_ARG, "cannot un-persist a layer after reset")
+
+    # -- Section 3.2 "writes the full layer state" ----------------------------
+    def layer_record(self, l: int) -> bytes:
+        out = bytearray()
+        g = self.by_layer[l]
+        for arr in _arrays_in_record(self.has_master):
+            for s in g:
+                raw = getattr(s, arr).tobytes()
+                out += raw
+                out += bytes(padded(len(raw)) - len(raw))
+        assert len(out) == self.R[l]
+        return bytes(out)
+
+    def pack(self, first_rank: int, capacity: int):
+        if self.mask is None:
+            raise OracleError(LC_ERR_BAD_STATE, "nothing selected")
+        sel = [l for l in range(self.N) if self.mask[l]]
+        if first_rank < 0 or first_rank > len(sel):
+            raise OracleError(LC_ERR_INVALID_ARG, "first_rank out of range")
+        last, total = first_rank, 0
+        while last < len(sel) and total + self.R[sel[last]] <= capacity:
+            total += self.R[sel[last]]
+            last += 1
+        if last == first_rank and first_rank < len(sel):
+            raise OracleError(LC_ERR_CAPACITY, "record does not fit")
+        payload = b"".join(self.layer_record(l) for l in sel[first_rank:last])
+        if self.mode == MODE_SNAPSHOT:
+            for l in sel[first_rank:last]:
+                for s in self.by_layer[l]:
+                    s.shadow[...] = s.weight
+        for l in sel[first_rank:last]:
+            self.unpacked.discard(l)
+        return np.frombuffer(payload, dtype=np.uint8).copy(), {
+            "bytes_written": total, "n_packed": last - first_rank,
+            "next_rank": last, "done": int(last == len(sel))}
+
+    # -- Section 3.5 / Eq. 8 -------------------------------------------------
+    def plan(self, versions: Sequence[dict], t_fail: int) -> List[int]:
+        """Index of the version each layer is restored from."""
+        for v in versions:
+            m = np.asarray(v["mask"])
+            if m.shape != (self.N,):
+                raise OracleError(LC_ERR_INVALID_ARG, "mask length")
+            need = sum(self.R[l] for l in range(self.N) if m[l])
+            if len(v["payload"]) != need:
+                raise OracleError(LC_ERR_INVALID_ARG, "payload size does not match mask")
+        choice = []
+        for l in range(self.N):
+            best, best_step, dup = None, None, False
+            for i, v in enumerate(versions):
+                if v["step"] <= t_fail and v["mask"][l]:
+                    if best is None or v["step"] > best_step:
+                        best, best_step, dup = i, v["step"], False
+                    elif v["step"] == best_step:
+                        dup = True
+            if best is None:
+                raise OracleError(LC_ERR_NO_VERSION, f"layer {l}: no persisted version <= {t_fail}")
+            if dup:
+                raise OracleError(LC_ERR_INVALID_ARG, f"layer {l}: two versions at step {best_step}")
+            choice.append(best)
+        return choice
+
+    def restore(self, versions: Sequence[dict], t_fail: int) -> np.ndarray:
+        choice = self.plan(versions, t_fail)
+        chosen = np.zeros(self.N, dtype=np.int64)
+        for l in range(self.N):
+            v = versions[choice[l]]
+            off = sum(self.R[j] for j in range(l) if v["mask"][j])
+            rec = bytes(np.asarray(v["payload"], dtype=np.uint8)[off:off + self.R[l]])
+            pos = 0
+            for arr in _arrays_in_record(self.has_master):
+                for s in self.by_layer[l]:
+                    dst = getattr(s, arr)
+                    nb = dst.nbytes
+                    dst[...] = np.frombuffer(rec[pos:pos + nb], dtype=dst.dtype)
+                    pos += padded(nb)
+            for s in self.by_layer[l]:
+                s.shadow[...] = s.weight
+            self.delta[l] = 0.0
+            self.t_last[l] = int(v["step"])
+            chosen[l] = int(v["step"])
+        self.last_step = t_fail
+        self.scored_step = None
+        self.mask = None
+        self.unpacked = set()
+        return chosen

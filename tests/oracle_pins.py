@@ -1,0 +1,394 @@
+"""Pins for the CPU oracle, written as reusable checks.
+
+Each ``check_*`` takes the oracle class under test (and, for the score pins,
+its Eq. 1 function) so that the same checks run against the real oracle and
+against deliberately broken copies (see test_oracle_mutations.py): a check
+that never fails on a planted mistake is not pinning anything.
+
+What pins what (the paper prints no worked example of u, Delta or a
+selection trace, so the pins are closed forms, exact-rational brute force,
+invariants and the paper's Table 1 figures):
+
+* Eq. 1 closed forms: constant shadow a and constant change c give
+  |c| / (|a| + eps_w); the denominator is the *previous* weights; the mean is
+  joint over all tensors of a layer; zero change gives exactly 0.
+* Eq. 3 uses ">=": an accumulator exactly equal to K persists.
+* Section 3.3 guard: with zero drift a layer persists exactly every S_max steps.
+* Eq. 4: reset to 0 after persisting (brute force checks Delta as the sum of
+  exact per-step scores since the layer's last persist).
+* Stats: size-weighted staleness <= max staleness <= S_max - 1 after a decision.
+* Records: 14 bytes per parameter for bf16 + fp32 master + m + v (Section 4.1
+  with Table 1); padded blocks hold the raw bytes in order.
+* Recovery: newest version <= t_fail per layer; round trip is bit-exact.
+"""
+from __future__ import annotations
+
+from fractions import Fraction
+
+import numpy as np
+
+from oracle import layercheck_oracle as O
+from tests._helpers import HostLayout, f32_to_bf16_bits
+
+
+def expect_error(fn, code):
+    """Run fn; it must raise an error carrying status ``code`` (any oracle copy)."""
+    try:
+        fn()
+    except AssertionError:
+        raise
+    except Exception as e:  # noqa: BLE001 - mutant copies define their own error class
+        assert getattr(e, "code", None) == code, (getattr(e, "code", None), code, e)
+        return
+    raise AssertionError(f"expected error code {code}")
+
+
+def _seg(layer, w, s, dtype, master=True):
+    n = w.size
+    return O.OSegment(layer, w, s, np.zeros(n, np.float32) if master else None,
+                      np.zeros(n, np.float32), np.zeros(n, np.float32))
+
+
+# ---------------------------------------------------------------- Eq. 1 -----
+
+def check_closed_form(score_fn):
+    # S = 0.5 everywhere, W = 0.5 + 2^-8 everywhere (both exact in bf16).
+    for dtype in (O.DT_BF16, O.DT_F32):
+        n = 37
+        if dtype == O.DT_BF16:
+            s = f32_to_bf16_bits(np.full(n, 0.5, np.float32))
+            w = f32_to_bf16_bits(np.full(n, 0.5 + 2.0 ** -8, np.float32))
+        else:
+            s = np.full(n, 0.5, np.float32)
+            w = np.full(n, 0.5 + 2.0 ** -8, np.float32)
+        A, B, cnt, u = score_fn([w], [s], dtype, 0.0)
+        assert cnt == n
+        assert A == n * 2.0 ** -8 and B == n * 0.5
+        assert u == 2.0 ** -7, u
+        # negative change of the same size gives the same score (absolute values)
+        if dtype == O.DT_F32:
+            w2 = np.full(n, 0.5 - 2.0 ** -8, np.float32)
+            assert score_fn([w2], [s], dtype, 0.0)[3] == 2.0 ** -7
+
+
+def check_denominator_is_previous(score_fn):
+    # S = 0.5, W = 1.0: mean|W-S| / mean|S| = 1 (dividing by mean|W| would give 0.5)
+    s = np.full(8, 0.5, np.float32)
+    w = np.full(8, 1.0, np.float32)
+    assert score_fn([w], [s], O.DT_F32, 0.0)[3] == 1.0
+
+
+def check_joint_mean(score_fn):
+    # Layer of two tensors (3 and 1 elements); only the first changes by 2^-8.
+    s1, s2 = np.full(3, 0.5, np.float32), np.full(1, 0.5, np.float32)
+    w1, w2 = np.full(3, 0.5 + 2.0 ** -8, np.float32), s2.copy()
+    u = score_fn([w1, w2], [s1, s2], O.DT_F32, 0.0)[3]
+    assert u == 3.0 * 2.0 ** -9, u  # joint mean; a mean of per-tensor means gives 2^-8
+
+
+def check_zero_change(score_fn):
+    rng = np.random.default_rng(1)
+    for dtype in (O.DT_BF16, O.DT_F32):
+        x = (rng.standard_normal(1000) * 0.02).astype(np.float32)
+        w = f32_to_bf16_bits(x) if dtype == O.DT_BF16 else x
+        u = score_fn([w], [w.copy()], dtype, 1e-8)[3]
+        assert u == 0.0 and not np.signbit(u)
+
+
+def check_eps_in_denominator(score_fn):
+    # all-zero previous weights: u = mean|W| / eps_w exactly when eps_w = 2^-10
+    s = np.zeros(4, np.float32)
+    w = np.full(4, 2.0 ** -12, np.float32)
+    assert score_fn([w], [s], O.DT_F32, 2.0 ** -10)[3] == 0.25
+
+
+def check_scale_invariance(score_fn):
+    rng = np.random.default_rng(2)
+    s = (rng.standard_normal(257) * 0.02).astype(np.float32)
+    w = (s + rng.standard_normal(257).astype(np.float32) * 1e-4).astype(np.float32)
+    u0 = score_fn([w], [s], O.DT_F32, 0.0)[3]
+    for k in (-3, 5):
+        u1 = score_fn([w * np.float32(2.0 ** k)], [s * np.float32(2.0 ** k)], O.DT_F32, 0.0)[3]
+        assert u1 == u0
+
+
+def check_exact_rational(score_fn):
+    """u within 1e-12 of the exact rational value on random tiny tensors."""
+    rng = np.random.default_rng(3)
+    for trial in range(20):
+        n1, n2 = rng.integers(1, 40, 2)
+        dt = O.DT_BF16 if trial % 2 else O.DT_F32
+        xs = [(rng.standard_normal(n) * 0.02).astype(np.float32) for n in (n1, n2)]
+        ys = [(x + rng.standard_normal(x.size).astype(np.float32) * 1e-3).astype(np.float32) for x in xs]
+        if dt == O.DT_BF16:
+            xs = [f32_to_bf16_bits(x) for x in xs]
+            ys = [f32_to_bf16_bits(y) for y in ys]
+        eps = 1e-8
+        u = score_fn(ys, xs, dt, eps)[3]
+        exact = exact_u(ys, xs, dt, eps)
+        assert abs(Fraction(u) - exact) <= Fraction(1, 10 ** 12) * abs(exact)
+
+
+def exact_value(v, dtype):
+    if dtype == O.DT_BF16:
+        return Fraction(float(np.array([int(v) << 16], dtype=np.uint32).view(np.float32)[0]))
+    return Fraction(float(v))
+
+
+def exact_u(ws, ss, dtype, eps):
+    A = Fraction(0)
+    B = Fraction(0)
+    n = 0
+    for w, s in zip(ws, ss):
+        for a, b in zip(w.tolist(), s.tolist()):
+            x, y = exact_value(a, dtype), exact_value(b, dtype)
+            A += abs(x - y)
+            B += abs(y)
+            n += 1
+    return (A / n) / (B / n + Fraction(eps))
+
+
+# ---------------------------------------------------------------- Eq. 3-5 ---
+
+def _const_layout(n_layers, per_layer=4):
+    segs = []
+    for l in range(n_layers):
+        s = np.full(per_layer, 0.5, np.float32)
+        segs.append(_seg(l, s.copy(), np.zeros(per_layer, np.float32), O.DT_F32))
+    return segs
+
+
+def check_ge_threshold(cls):
+    # u = 2^-7 exactly; K0 = 2^-7: Delta == K must persist under Eq. 3's ">=".
+    segs = _const_layout(2)
+    orc = cls(segs, 2, O.DT_F32, True, O.MODE_ACCUM, [2.0 ** -7, 2.0 ** -6], s_max=100, eps_w=0.0)
+    orc.pack(0, 1 << 30)  # base version
+    for s in segs:
+        s.weight[...] = 0.5 + 2.0 ** -8
+    orc.score(1)
+    mask, st = orc.select(1, 1.0)
+    assert list(mask) == [1, 0], mask
+    assert st["n_forced"] == 0
+    # lr_scale = 0.5 halves K: layer 1 holds 2^-7 + u(2) ~= 0.01556, which is
+    # below K0 = 2^-6 but above K0 * 0.5 (ignoring or inverting s(lr) fails here)
+    orc.pack(0, 1 << 30)
+    for s in segs:
+        s.weight[...] = 0.5 + 2.0 ** -7
+    orc.score(2)
+    mask, _ = orc.select(2, 0.5)
+    assert list(mask) == [1, 1], mask
+
+
+def check_staleness_period(cls, mode=O.MODE_ACCUM):
+    # zero drift: each layer persists exactly at t_base + k*S_max
+    for s_max in (1, 3, 4):
+        for t_base in (0, 7):
+            segs = _const_layout(3)
+            orc = cls(segs, 3, O.DT_F32, True, mode, [1e-3] * 3, s_max=s_max, t_base=t_base)
+            orc.pack(0, 1 << 30)
+            for t in range(t_base + 1, t_base + 4 * s_max + 2):
+                orc.score(t)
+                mask, st = orc.select(t, 1.0)
+                expect = int((t - t_base) % s_max == 0)
+                assert list(mask) == [expect] * 3, (s_max, t, mask)
+                assert st["n_forced"] == 3 * expect
+                assert st["max_age"] == (t - t_base) % s_max
+                orc.pack(0, 1 << 30)
+
+
+def check_k0_extremes(cls):
+    lay = HostLayout([[5, 3], [4], [7]], seed=4)
+    # K0 = 0: every layer persists by drift every step.  With S_max = 1 every
+    # layer is also due by age, and n_forced counts only age-only selections.
+    orc = cls(lay.segs, 3, O.DT_BF16, True, O.MODE_ACCUM, [0.0] * 3, s_max=1)
+    orc.pack(0, 1 << 40)
+    for t in range(1, 5):
+        lay.step([1.0, 0.0, 0.5], zero_layers=(1,))
+        orc.score(t)
+        mask, st = orc.select(t, 1.0)
+        assert mask.tolist() == [1, 1, 1] and st["n_forced"] == 0
+        orc.pack(0, 1 << 40)
+    lay = HostLayout([[5, 3], [4], [7]], seed=4)
+    orc = cls(lay.segs, 3, O.DT_BF16, True, O.MODE_ACCUM, [1e300] * 3, s_max=2)
+    orc.pack(0, 1 << 40)
+    for t in range(1, 7):
+        lay.step([1.0, 1.0, 1.0])
+        orc.score(t)
+        mask, st = orc.select(t, 1.0)
+        assert mask.tolist() == [t % 2 == 0] * 3
+        assert st["n_forced"] == (3 if t % 2 == 0 else 0)
+        orc.pack(0, 1 << 40)
+
+
+def check_stats_invariants(cls, mode=O.MODE_ACCUM):
+    rng = np.random.default_rng(5)
+    for trial in range(6):
+        sizes = [[int(x) for x in rng.integers(1, 30, rng.integers(1, 4))] for _ in range(rng.integers(2, 7))]
+        lay = HostLayout(sizes, seed=trial)
+        N = len(sizes)
+        s_max = int(rng.integers(1, 6))
+        k0 = list(10.0 ** rng.uniform(-3, -1, N))
+        orc = cls(lay.segs, N, O.DT_BF16, True, mode, k0, s_max=s_max)
+        orc.pack(0, 1 << 40)
+        scales = list(10.0 ** rng.uniform(-1.5, 1.0, N))
+        for t in range(1, 15):
+            lay.step(scales)
+            orc.score(t)
+            mask, st = orc.select(t, 1.0)
+            assert st["weighted_age"] <= st["max_age"] <= s_max - 1
+            n = [sum(s.numel for s in lay.segs if s.layer == l) for l in range(N)]
+            ages = [t - orc.t_last[l] for l in range(N)]
+            assert st["max_age"] == max(ages)
+            # weighted staleness: an explicit sum over layers
+            assert abs(st["weighted_age"] - sum(a * b for a, b in zip(n, ages)) / sum(n)) <= 1e-12 * max(1, st["max_age"])
+            assert st["n_selected"] == int(mask.sum())
+            orc.pack(0, 1 << 40)
+
+
+# ---------------------------------------------------------------- records ---
+
+def check_record_format(cls):
+    lay = HostLayout([[3, 200], [128]], dtype=O.DT_BF16, has_master=True, seed=6)
+    orc = cls(lay.segs, 2, O.DT_BF16, True, O.MODE_ACCUM, [1e-3, 1e-3], s_max=4)
+    payload, res = orc.pack(0, 1 << 30)
+    # layer 0 record: W blocks (6 B -> 256, 400 B -> 512), master (12 -> 256, 800 -> 1024),
+    # m and v like master: 768 + 1280 * 3 = 4608; layer 1: 256 + 512 * 3 = 1792
+    assert res["bytes_written"] == len(payload) == 4608 + 1792
+    s0, s1, s2 = lay.segs
+    assert bytes(payload[0:6]) == s0.weight.tobytes()
+    assert not payload[6:256].any()
+    assert bytes(payload[256:656]) == s1.weight.tobytes()
+    assert not payload[656:768].any()
+    assert bytes(payload[768:780]) == s0.master.tobytes()
+    off = 768 + 256 + 1024
+    assert bytes(payload[off:off + 12]) == s0.exp_avg.tobytes()
+    off = 768 + 2 * 1280
+    assert bytes(payload[off + 256:off + 256 + 800]) == s1.exp_avg_sq.tobytes()
+    off = 4608
+    assert bytes(payload[off:off + 256]) == s2.weight.tobytes()
+    assert bytes(payload[off + 256:off + 768]) == s2.master.tobytes()
+    assert bytes(payload[off + 1280:off + 1792]) == s2.exp_avg_sq.tobytes()
+
+
+def check_fourteen_bytes_per_param():
+    # pad-free blocks (every tensor a multiple of 128 elements): 2 + 4 + 4 + 4 bytes
+    assert O.record_bytes([128 * 7, 4096], 2, True) == 14 * (128 * 7 + 4096)
+    assert O.record_bytes([128 * 7, 4096], 2, False) == 10 * (128 * 7 + 4096)
+    assert O.record_bytes([64 * 3], 4, False) == 12 * 64 * 3
+    assert O.record_bytes([1], 2, True) == 4 * 256
+
+
+def check_capacity(cls):
+    lay = HostLayout([[100], [300], [50]], seed=7)
+    orc = cls(lay.segs, 3, O.DT_BF16, True, O.MODE_ACCUM, [1e-3] * 3, s_max=4)
+    R = orc.R
+    p0, r0 = orc.pack(0, R[0] + R[1] - 1)
+    assert r0 == {"bytes_written": R[0], "n_packed": 1, "next_rank": 1, "done": 0}
+    expect_error(lambda: orc.pack(1, R[1] - 1), O.LC_ERR_CAPACITY)
+    p1, r1 = orc.pack(1, R[1] + R[2])
+    assert r1["done"] == 1 and r1["n_packed"] == 2
+    full = O.LayerCheckOracle(HostLayout([[100], [300], [50]], seed=7).segs, 3, O.DT_BF16, True,
+                              O.MODE_ACCUM, [1e-3] * 3, s_max=4).pack(0, 1 << 30)[0]
+    assert bytes(np.concatenate([p0, p1])) == bytes(full)
+
+
+# ---------------------------------------------------------------- recovery --
+
+def check_restore_roundtrip(cls, mode=O.MODE_ACCUM):
+    sizes = [[17, 5], [64], [9, 9, 9], [1]]
+    lay = HostLayout(sizes, seed=8)
+    N = len(sizes)
+    orc = cls(lay.segs, N, O.DT_BF16, True, mode, [2e-2] * N, s_max=3)
+    versions = []
+    payload, _ = orc.pack(0, 1 << 40)
+    versions.append({"step": 0, "mask": np.ones(N, np.uint8), "payload": payload})
+    truth = {}  # (layer, step) -> arrays as persisted
+    for s in lay.segs:
+        truth.setdefault((s.layer, 0), []).append((s.weight.copy(), s.master.copy(), s.exp_avg.copy(), s.exp_avg_sq.copy()))
+    for t in range(1, 8):
+        lay.step([3.0, 0.2, 1.0, 0.05])
+        orc.score(t)
+        mask, _ = orc.select(t, 1.0)
+        payload, _ = orc.pack(0, 1 << 40)
+        versions.append({"step": t, "mask": mask, "payload": payload})
+        for s in lay.segs:
+            if mask[s.layer]:
+                truth.setdefault((s.layer, t), []).append((s.weight.copy(), s.master.copy(), s.exp_avg.copy(), s.exp_avg_sq.copy()))
+    t_fail = 5
+    # brute-force plan: newest persisted step <= t_fail per layer
+    expect = [max(v["step"] for v in versions if v["step"] <= t_fail and v["mask"][l]) for l in range(N)]
+    for s in lay.segs:  # lose the live state
+        for a in (s.weight, s.shadow, s.master, s.exp_avg, s.exp_avg_sq):
+            a[...] = 0
+    chosen = orc.restore(versions, t_fail)
+    assert chosen.tolist() == expect
+    per_layer = {}
+    for s in lay.segs:
+        k = per_layer.get(s.layer, 0)
+        w, m0, m, v = truth[(s.layer, expect[s.layer])][k]
+        per_layer[s.layer] = k + 1
+        assert np.array_equal(s.weight, w) and np.array_equal(s.master, m0)
+        assert np.array_equal(s.exp_avg, m) and np.array_equal(s.exp_avg_sq, v)
+        assert np.array_equal(s.shadow, s.weight)
+    assert orc.t_last == expect and orc.delta == [0.0] * N
+    # restore -> re-pack of every layer reproduces each layer's chosen record
+    orc2 = cls(lay.segs, N, O.DT_BF16, True, mode, [2e-2] * N, s_max=3)
+    allrec, _ = orc2.pack(0, 1 << 40)
+    pos = 0
+    for l in range(N):
+        v = versions[[i for i, vv in enumerate(versions) if vv["step"] == expect[l]][0]]
+        off = sum(orc.R[j] for j in range(l) if v["mask"][j])
+        assert bytes(allrec[pos:pos + orc.R[l]]) == bytes(v["payload"][off:off + orc.R[l]])
+        pos += orc.R[l]
+    # dropping the newest version of a layer moves it to the next-newest
+    newest = max(range(len(versions)), key=lambda i: versions[i]["step"] if versions[i]["step"] <= t_fail else -1)
+    rest = [v for i, v in enumerate(versions) if i != newest]
+    plan = orc.plan(rest, t_fail)
+    for l in range(N):
+        exp2 = max(v["step"] for v in rest if v["step"] <= t_fail and v["mask"][l])
+        assert rest[plan[l]]["step"] == exp2
+
+
+def check_restore_errors(cls):
+    lay = HostLayout([[4], [4]], seed=9)
+    orc = cls(lay.segs, 2, O.DT_BF16, True, O.MODE_ACCUM, [1e-3] * 2, s_max=3)
+    payload, _ = orc.pack(0, 1 << 30)
+    base = {"step": 0, "mask": np.ones(2, np.uint8), "payload": payload}
+    part = {"step": 3, "mask": np.array([1, 0], np.uint8), "payload": payload[:orc.R[0]]}
+    for versions, t_fail, code in (
+            ([part], 3, O.LC_ERR_NO_VERSION),
+            ([base, part], -1, O.LC_ERR_NO_VERSION),
+            ([base, dict(base)], 2, O.LC_ERR_INVALID_ARG),
+            ([base, {"step": 3, "mask": np.array([1, 0], np.uint8), "payload": payload}], 5, O.LC_ERR_INVALID_ARG)):
+        expect_error(lambda: orc.restore(versions, t_fail), code)
+    # a version newer than t_fail is ignored
+    assert orc.restore([base, part], 2).tolist() == [0, 0]
+    assert orc.restore([base, part], 3).tolist() == [3, 0]
+
+
+def check_accum_equals_snapshot_first_step(cls):
+    la = HostLayout([[30, 2], [50]], seed=10)
+    lb = HostLayout([[30, 2], [50]], seed=10)
+    oa = cls(la.segs, 2, O.DT_BF16, True, O.MODE_ACCUM, [1e9, 1e9], s_max=100)
+    ob = cls(lb.segs, 2, O.DT_BF16, True, O.MODE_SNAPSHOT, [1e9, 1e9], s_max=100)
+    oa.pack(0, 1 << 30)
+    ob.pack(0, 1 << 30)
+    acc = [0.0, 0.0]  # summed per-step drift numerators sum|W(t) - W(t-1)|
+    for t in range(1, 6):
+        la.step([1.0, 0.3])
+        lb.step([1.0, 0.3])
+        for l in range(2):
+            g = [s for s in la.segs if s.layer == l]
+            acc[l] += O.layer_update_score([s.weight for s in g], [s.shadow for s in g], O.DT_BF16, 0.0)[0]
+        oa.score(t)
+        ob.score(t)
+        if t == 1:  # first step after a persist: both modes see the same drift
+            assert oa.delta == ob.delta and oa.delta[0] > 0
+        oa.select(t, 1.0)
+        ob.select(t, 1.0)
+    # triangle inequality: distance to the last persisted weights (SNAPSHOT's
+    # numerator) is bounded by the summed per-step distances
+    for l in range(2):
+        g = [s for s in lb.segs if s.layer == l]
+        a_snap = O.layer_update_score([s.weight for s in g], [s.shadow for s in g], O.DT_BF16, 0.0)[0]
+        assert 0 < a_snap <= acc[l] * (1 + 1e-12)

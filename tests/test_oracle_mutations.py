@@ -1,0 +1,90 @@
+"""Plant plausible mistakes in copies of the oracle (CPU only) and require that
+the pins catch every one of them: a dropped term, a wrong comparison, a wrong
+operand or index must fail at least one check."""
+import sys
+import types
+
+import pytest
+
+from oracle import layercheck_oracle as O
+from tests import oracle_pins as P
+from tests.test_bruteforce_tiny import run_bruteforce
+
+SRC = open(O.__file__).read()
+
+MUTANTS = {
+    "denominator_uses_current": ("B += float(np.sum(np.abs(y)))", "B += float(np.sum(np.abs(x)))"),
+    "signed_difference": ("A += float(np.sum(np.abs(x - y)))", "A += float(np.sum(x - y))"),
+    "eps_dropped": ("np.float64(B / n + eps_w)", "np.float64(B / n)"),
+    "eps_outside_mean": ("np.float64(B / n + eps_w)", "np.float64((B + eps_w) / n)"),
+    "per_tensor_count": ("n += int(w.size)", "n = int(w.size)"),
+    "strict_threshold": ("by_drift = self.delta[l] >= K", "by_drift = self.delta[l] > K"),
+    "strict_staleness": ("by_age = age >= self.s_max", "by_age = age > self.s_max"),
+    "lr_scale_ignored": ("K = self.k0[l] * lr_scale", "K = self.k0[l]"),
+    "lr_scale_inverted": ("K = self.k0[l] * lr_scale", "K = self.k0[l] / lr_scale"),
+    "no_reset": ("                self.delta[l] = 0.0\n                self.t_last[l] = step",
+                 "                self.t_last[l] = step"),
+    "no_timestamp": ("                self.delta[l] = 0.0\n                self.t_last[l] = step",
+                     "                self.delta[l] = 0.0"),
+    "accum_overwrites": ("self.delta[l] = self.delta[l] + u", "self.delta[l] = u"),
+    "accum_shadow_stale": ("        if self.mode == MODE_ACCUM:\n            # the next step's",
+                           "        if False:\n            # the next step's"),
+    "forced_count_wrong": ("if not by_drift:\n                    n_forced += 1", "if by_age:\n                    n_forced += 1"),
+    "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
+    "moments_swapped": ('+ ["exp_avg", "exp_avg_sq"]', '+ ["exp_avg_sq", "exp_avg"]'),
+    "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),
+    "restore_ignores_t_fail": ('if v["step"] <= t_fail and v["mask"][l]:', 'if v["mask"][l]:'),
+    "restore_offset_counts_all": ('off = sum(self.R[j] for j in range(l) if v["mask"][j])',
+                                  'off = sum(self.R[j] for j in range(l))'),
+    "restore_keeps_old_shadow": ("            for s in self.by_layer[l]:\n                s.shadow[...] = s.weight\n            self.delta[l] = 0.0",
+                                 "            self.delta[l] = 0.0"),
+    "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
+                                   "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
+    "capacity_off_by_record": ("total + self.R[sel[last]] <= capacity", "total + self.R[sel[last]] < capacity"),
+}
+
+
+def mutant(name):
+    old, new = MUTANTS[name]
+    assert SRC.count(old) == 1, f"mutation anchor for {name} not unique"
+    mod = types.ModuleType(f"oracle_mutant_{name}")
+    sys.modules[mod.__name__] = mod
+    exec(compile(SRC.replace(old, new), f"<mutant {name}>", "exec"), mod.__dict__)
+    return mod
+
+
+def all_checks(M):
+    yield lambda: [c(M.layer_update_score) for c in (
+        P.check_closed_form, P.check_denominator_is_previous, P.check_joint_mean,
+        P.check_zero_change, P.check_eps_in_denominator, P.check_scale_invariance,
+        P.check_exact_rational)]
+    cls = M.LayerCheckOracle
+    for c in (P.check_ge_threshold, P.check_k0_extremes, P.check_record_format, P.check_capacity,
+              P.check_restore_errors, P.check_accum_equals_snapshot_first_step):
+        yield lambda c=c: c(cls)
+    for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
+        yield lambda mode=mode: P.check_staleness_period(cls, mode)
+        yield lambda mode=mode: P.check_stats_invariants(cls, mode)
+        yield lambda mode=mode: P.check_restore_roundtrip(cls, mode)
+    yield lambda: M.record_bytes([128], 2, True) == 14 * 128 or (_ for _ in ()).throw(AssertionError())
+    for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
+        yield lambda mode=mode: run_bruteforce(M, mode, O.DT_BF16, 0, steps=12)
+
+
+def test_unmutated_passes_everything():
+    mod = types.ModuleType("oracle_copy")
+    sys.modules[mod.__name__] = mod
+    exec(compile(SRC, "<copy>", "exec"), mod.__dict__)
+    for chk in all_checks(mod):
+        chk()
+
+
+@pytest.mark.parametrize("name", sorted(MUTANTS))
+def test_mutant_is_caught(name):
+    M = mutant(name)
+    for chk in all_checks(M):
+        try:
+            chk()
+        except Exception:
+            return
+    pytest.fail(f"planted mistake {name!r} passed every pin")
