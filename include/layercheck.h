@@ -1,0 +1,197 @@
+/*
+ * layercheck.h - C interface of the MI355X (gfx950) LayerCheck decision step.
+ *
+ * LayerCheck (adaptive layer-wise checkpointing for LLM post-training) keeps,
+ * for every layer group of a model, a drift accumulator and the step at which
+ * the layer was last persisted.  At each checkpoint opportunity it scores
+ * every layer, selects the layers whose accumulated drift reached the
+ * threshold or whose staleness reached the bound, and persists the full state
+ * of exactly those layers (weights together with their optimizer tensors).
+ * After a failure it assembles a mixed-timestamp composite state from the
+ * newest persisted record of each layer.
+ *
+ * Every entry point returns an lc_status; nothing throws across this
+ * interface.  All pointers to model arrays are DEVICE pointers owned by the
+ * caller; the library never frees or reallocates them.  The library owns only
+ * the opaque context and its small device tables.  Work is enqueued on the
+ * HIP stream given at init; a context is single-stream and not thread-safe,
+ * separate contexts are independent.  On any HIP failure the call returns
+ * LC_ERR_HIP and the context is poisoned: later calls return
+ * LC_ERR_BAD_STATE (lc_destroy still works).  Validation failures return
+ * before anything is enqueued, leaving the context unchanged.  A message for
+ * the last failure on the calling thread is available from lc_last_error().
+ *
+ * Layer groups (Section 2.2): embed_tokens, each transformer block, the final
+ * norm and lm_head.  A layer may consist of any number of tensors
+ * ("segments"); a segment is one contiguous range of one tensor, so a ZeRO-3
+ * shard of a layer is simply one segment (Section 4.1: each rank decides on
+ * its own shard).
+ */
+#ifndef LAYERCHECK_H
+#define LAYERCHECK_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  LC_OK = 0,
+  LC_ERR_INVALID_ARG = 1, /* bad pointer, size, id, order, value          */
+  LC_ERR_BAD_STATE = 2,   /* call out of sequence, or poisoned context    */
+  LC_ERR_CAPACITY = 3,    /* next record does not fit the staging buffer  */
+  LC_ERR_NO_VERSION = 4,  /* a layer has no persisted record <= t_fail    */
+  LC_ERR_HIP = 5,         /* a HIP runtime call failed                    */
+  LC_ERR_OOM = 6          /* host or device allocation of library tables  */
+} lc_status;
+
+typedef enum { LC_DT_BF16 = 1, LC_DT_F32 = 2 } lc_dtype;
+
+typedef enum {
+  /* Eq. 1-2: the shadow holds W(t-1); each score adds u_l(t) to Delta_l and
+   * the same pass refreshes the shadow of every layer to W(t). */
+  LC_MODE_ACCUM = 0,
+  /* Distance to the last persisted version: the shadow holds the weights as
+   * last persisted; each score sets Delta_l = u_l(t); the pack of a selected
+   * layer refreshes its shadow. */
+  LC_MODE_SNAPSHOT = 1
+} lc_mode;
+
+typedef struct lc_ctx lc_ctx; /* opaque, library-owned */
+
+/* One contiguous piece of one tensor of one layer.  All arrays hold `numel`
+ * elements; weight and shadow have the layout's weight dtype, the others are
+ * fp32.  Pointers must be naturally aligned (2 B for bf16, 4 B for fp32);
+ * 16-byte alignment selects the vectorised fast path. */
+typedef struct {
+  uint32_t layer;     /* layer group id in [0, n_layers)                      */
+  uint32_t reserved;  /* must be 0                                            */
+  uint64_t numel;     /* > 0                                                  */
+  void *weight;       /* device, live weights W (bf16 or fp32)                */
+  void *shadow;       /* device, shadow copy S, same dtype; written by the lib */
+  float *master;      /* device fp32 master copy; NULL iff !has_master        */
+  float *exp_avg;     /* device fp32 Adam first moment m                      */
+  float *exp_avg_sq;  /* device fp32 Adam second moment v                     */
+} lc_segment;
+
+typedef struct {
+  uint32_t n_layers;          /* N >= 1                                        */
+  uint32_t n_segments;        /* >= n_layers                                   */
+  const lc_segment *segments; /* host array; grouped by ascending layer id; the
+                                 order inside a layer is the record order      */
+  int32_t weight_dtype;       /* lc_dtype                                      */
+  int32_t has_master;         /* 0 or 1                                        */
+  int32_t mode;               /* lc_mode                                       */
+  int32_t reserved;           /* must be 0                                     */
+  const double *k0;           /* host [n_layers]: base thresholds K0_l >= 0
+                                 (Section 3.4 uses 1e-3, 1e-2 for embeddings) */
+  int64_t s_max;              /* staleness bound S_max >= 1 (Eq. 5)            */
+  double eps_w;               /* Eq. 1 stabiliser, >= 0 (e.g. 1e-8)            */
+  int64_t t_base;             /* step of the base full checkpoint (Sec. 3.4)   */
+  void *stream;               /* hipStream_t, borrowed; NULL = null stream     */
+} lc_layout_desc;
+
+typedef struct {
+  uint32_t n_selected;    /* layers persisted at this step                    */
+  uint32_t n_forced;      /* selected by the staleness guard alone            */
+  uint64_t payload_bytes; /* sum of record sizes of the selected layers       */
+  int64_t max_age;        /* max_l (t - t_l) after the decision               */
+  double weighted_age;    /* sum_l n_l (t - t_l) / sum_l n_l after the decision
+                             (Section 3.3 size-weighted staleness), computed as
+                             double(integer numerator) / double(integer denominator) */
+} lc_select_stats;
+
+typedef struct {
+  uint64_t bytes_written; /* bytes of staging written by this call            */
+  uint32_t n_packed;      /* records written by this call                     */
+  uint32_t next_rank;     /* rank to pass as first_rank of the next call      */
+  int32_t done;           /* 1 when every selected layer has been packed      */
+  int32_t reserved;
+} lc_pack_result;
+
+typedef struct {
+  int64_t step;           /* step the records were persisted at               */
+  const uint8_t *mask;    /* host [n_layers]: 1 for each layer in the payload */
+  const void *payload;    /* device memory, pinned host memory, or pageable
+                             host memory: records of the masked layers in
+                             ascending layer id (the lc_pack_selected format) */
+  uint64_t payload_bytes; /* must equal the sum of their record sizes         */
+} lc_version;
+
+/* Layout query without any GPU work: validates `d` as lc_init_layout does and
+ * reports per-layer element counts and record sizes (host arrays of n_layers
+ * entries, either may be NULL). */
+lc_status lc_query_layout(const lc_layout_desc *d, uint64_t *numel_out,
+                          uint64_t *record_bytes_out);
+
+/* Layer-aligned layout (Section 3.4 "Layer-aligned optimizer state layout"):
+ * builds the per-layer chunk and copy tables, allocates the small device
+ * state, sets S <- W for every segment, Delta_l = 0 and t_l = t_base for every
+ * layer (Section 3.2; the base full checkpoint of Section 3.4 counts as the
+ * last persist).  The base selection (every layer, at t_base) is left
+ * pending so the caller can pack the base version with lc_pack_selected.
+ * Enqueued on d->stream; returns after the enqueue. */
+lc_status lc_init_layout(const lc_layout_desc *d, lc_ctx **out);
+
+/* Eq. 1-2 for every layer at decision step `step` (> every earlier step and
+ * > t_base):  u_l = mean|W_l - S_l| / (mean|S_l| + eps_w), means taken jointly
+ * over all elements of all segments of layer l, accumulated in fp64.
+ * ACCUM: Delta_l += u_l and S <- W for all layers in the same pass.
+ * SNAPSHOT: Delta_l = u_l; requires the previous selection fully packed.
+ * In ACCUM mode an unpacked selection is discarded.  Asynchronous. */
+lc_status lc_score_layers(lc_ctx *c, int64_t step);
+
+/* Eq. 3-5 for every layer: K_l = K0_l * lr_scale (lr_scale = s(lr(t)) > 0,
+ * finite); select l when Delta_l >= K_l or step - t_l >= S_max; a selected
+ * layer gets Delta_l = 0 and t_l = step (Eq. 4).  Must follow
+ * lc_score_layers(step).  Writes the 0/1 mask (host [n_layers]) and stats
+ * when the pointers are non-NULL, which synchronises the stream; with both
+ * NULL the call is asynchronous. */
+lc_status lc_select(lc_ctx *c, int64_t step, double lr_scale, uint8_t *mask_out,
+                    lc_select_stats *stats_out);
+
+/* Selective persistence (Section 3.2): writes the records of the selected
+ * layers of rank >= first_rank (ranks count selected layers in ascending id)
+ * into `staging` (device, 256-byte aligned), as many whole records as fit in
+ * `capacity` bytes.  Record of layer l: its W blocks, then master (if
+ * present), exp_avg and exp_avg_sq blocks; one block per segment in layout
+ * order holding the raw little-endian bytes, zero-padded to a multiple of 256
+ * bytes.  Records are concatenated without gaps.  SNAPSHOT mode also sets
+ * S <- W for the packed layers in the same pass.  Returns LC_ERR_CAPACITY if
+ * the record at first_rank alone exceeds `capacity`.  Synchronises the stream
+ * only when the selection mask is not yet on the host; the copy itself is
+ * asynchronous. */
+lc_status lc_pack_selected(lc_ctx *c, void *staging, uint64_t capacity, uint32_t first_rank,
+                           lc_pack_result *out);
+
+/* Composite recovery (Section 3.5, Eq. 8): for each layer the version with the
+ * greatest step <= t_fail whose mask holds the layer is restored into W,
+ * master, exp_avg, exp_avg_sq and S (<- W); Delta_l = 0, t_l = that step; the
+ * next step must exceed t_fail.  A version newer than t_fail is ignored.  No
+ * candidate for a layer: LC_ERR_NO_VERSION; two candidates at the same
+ * greatest step: LC_ERR_INVALID_ARG.  `chosen_step_out` (host [n_layers] or
+ * NULL) receives the step each layer was restored from.  Returns after the
+ * restore has completed on the device. */
+lc_status lc_restore_composite(lc_ctx *c, const lc_version *versions, uint32_t n_versions,
+                               int64_t t_fail, int64_t *chosen_step_out);
+
+/* Synchronises the stream and copies the per-layer state to host arrays of
+ * n_layers entries (any may be NULL): the last scores u_l, accumulators
+ * Delta_l and last-persist steps t_l. */
+lc_status lc_read_state(lc_ctx *c, double *u_out, double *delta_out, int64_t *t_last_out);
+
+/* Record size of one layer in bytes (0 for a bad id or NULL context). */
+uint64_t lc_record_bytes(const lc_ctx *c, uint32_t layer);
+
+/* Synchronises the stream and frees the context (NULL is a no-op). */
+lc_status lc_destroy(lc_ctx *c);
+
+/* Message for the last failing call on this thread ("" if none). */
+const char *lc_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LAYERCHECK_H */

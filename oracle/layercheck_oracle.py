@@ -122,6 +122,23 @@ def record_bytes(seg_numels: Sequence[int], weight_itemsize: int, has_master: bo
     return total
 
 
+def decide(delta, t_last, k0, lr_scale: float, s_max: int, step: int):
+    """Eq. 3 with K(t) = K0 * s(lr(t)), and the Section 3.3 staleness guard.
+    Returns (selected, selected-by-the-guard-alone) as uint8 arrays."""
+    n = len(delta)
+    mask = np.zeros(n, dtype=np.uint8)
+    forced = np.zeros(n, dtype=np.uint8)
+    for l in range(n):
+        K = k0[l] * lr_scale
+        age = step - t_last[l]
+        by_drift = delta[l] >= K
+        by_age = age >= s_max
+        if by_drift or by_age:
+            mask[l] = 1
+            forced[l] = 0 if by_drift else 1
+    return mask, forced
+
+
 class LayerCheckOracle:
     """Stateful mirror of the decision step on host arrays."""
 
@@ -201,17 +218,12 @@ class LayerCheckOracle:
             raise OracleError(LC_ERR_BAD_STATE, "select must follow score at the same step")
         if not (lr_scale > 0.0) or lr_scale == float("inf"):
             raise OracleError(LC_ERR_INVALID_ARG, "lr_scale must be positive and finite")
-        mask = np.zeros(self.N, dtype=np.uint8)
-        n_forced = 0
+        self._pre_delta = list(self.delta)
+        self._pre_t_last = list(self.t_last)
+        mask, forced = decide(self.delta, self.t_last, self.k0, lr_scale, self.s_max, step)
+        n_forced = int(forced.sum())
         for l in range(self.N):
-            K = self.k0[l] * lr_scale
-            age = step - self.t_last[l]
-            by_drift = self.delta[l] >= K
-            by_age = age >= self.s_max
-            if by_drift or by_age:
-                mask[l] = 1
-                if not by_drift:
-                    n_forced += 1
+            if mask[l]:  # Eq. 4: reset on persist
                 self.delta[l] = 0.0
                 self.t_last[l] = step
         self.scored_step = None
@@ -243,7 +255,10 @@ class LayerCheckOracle:
             self.t_last[layer] = self.mask_step
             self.unpacked.add(layer)
         elif not selected and self.mask[layer]:
-            raise OracleError(LC_ERR_INVALID_ARG, "cannot un-persist a layer after reset")
+            self.mask[layer] = 0
+            self.delta[layer] = self._pre_delta[layer]
+            self.t_last[layer] = self._pre_t_last[layer]
+            self.unpacked.discard(layer)
 
     # -- Section 3.2 "writes the full layer state" ----------------------------
     def layer_record(self, l: int) -> bytes:

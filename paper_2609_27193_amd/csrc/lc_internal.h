@@ -1,0 +1,103 @@
+// Internal tables and kernel launchers of the LayerCheck HIP library.
+// Shared by the host runtime (lc_runtime.cpp) and the kernels (lc_kernels.hip).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lc {
+
+// ---- tiling ------------------------------------------------------------------
+// Score: a chunk is a run of consecutive elements of one segment holding
+// kChunkBytes of weights (and the same of shadow).  Chunks never cross a
+// segment, so every layer owns a contiguous range of chunks and one fp64
+// (sum|W-S|, sum|S|) pair per chunk is reduced in a fixed order per layer.
+constexpr uint32_t kScoreThreads = 256;
+constexpr uint32_t kChunkBytes = 64u * 1024u;
+// Pack/restore: a piece is kPieceBytes of one copy unit (one array of one
+// segment); records are laid out so that every unit starts 256-B aligned.
+constexpr uint32_t kCopyThreads = 256;
+constexpr uint32_t kPieceBytes = 64u * 1024u;
+constexpr uint32_t kRecordAlign = 256u;
+constexpr uint32_t kFinalizeThreads = 256;
+constexpr uint32_t kSelectThreads = 256;
+
+// One segment as the score kernel sees it.
+struct ScoreSeg {
+  uint64_t w;            // device address of the weights
+  uint64_t s;            // device address of the shadow
+  uint64_t numel;
+  uint32_t chunk_begin;  // global index of the segment's first chunk
+  uint32_t vec_ok;       // w and s both 16-B aligned
+};
+
+// One block of a layer record: one array (W, master, m or v) of one segment.
+struct CopyUnit {
+  uint64_t arr;      // device address of the array range
+  uint64_t shadow;   // shadow range for W units, 0 otherwise
+  uint64_t rec_off;  // byte offset of the block inside the record (256-B aligned)
+  uint64_t bytes;    // payload bytes (the block is padded to kRecordAlign)
+  uint32_t piece0;   // first layer-local piece index of this unit
+  uint32_t vec_ok;   // arr (and shadow) 16-B aligned
+  uint32_t elem;     // element size in bytes (2 or 4)
+  uint32_t pad;
+};
+
+// Written by the select kernel, copied to pinned host memory, followed by the
+// 0/1 mask of n_layers bytes.
+struct SelectHeader {
+  uint32_t n_selected;
+  uint32_t n_forced;
+  uint64_t payload_bytes;
+  int64_t max_age;
+  double weighted_age;
+  uint64_t total_pieces;
+  uint64_t age_numerator;
+  uint64_t reserved[2];
+};
+static_assert(sizeof(SelectHeader) == 64, "header layout");
+
+// Device-resident state of one context.
+struct DeviceTables {
+  uint32_t n_layers;
+  uint32_t n_chunks;
+  int dtype;  // 1 bf16, 2 f32
+  int mode;   // 0 accum, 1 snapshot
+  double eps_w;
+  int64_t s_max;
+
+  const ScoreSeg* segs;
+  const uint32_t* chunk_seg;          // [n_chunks]
+  const uint32_t* layer_chunk_begin;  // [N+1]
+  double2* partials;                  // [n_chunks] (sum|W-S|, sum|S|)
+  double* u;                          // [N]
+  double* delta;                      // [N]
+  int64_t* t_last;                    // [N]
+  const double* k0;                   // [N]
+  const uint64_t* numel;              // [N]
+  const uint64_t* rec_bytes;          // [N]
+  const uint64_t* layer_pieces;       // [N] pieces of one record
+  const CopyUnit* units;              // all units, layer-major, record order
+  const uint32_t* piece_unit;         // layout-wide piece -> unit index
+  const uint64_t* layer_piece_begin;  // [N+1] offset of each layer in piece_unit
+  uint32_t* sel_layer;                // [N] layer of each selected rank
+  uint64_t* sel_rec_prefix;           // [N+1] record byte offsets by rank
+  uint64_t* sel_piece_prefix;         // [N+1] piece offsets by rank
+  SelectHeader* result;               // header + mask[N]
+  // restore scratch
+  uint32_t* rank_layer;               // [N]
+  uint64_t* rank_src;                 // [N]
+  uint64_t* rank_piece_prefix;        // [N+1]
+};
+
+// Launchers: return hipGetLastError() of the launches.
+hipError_t launch_score(const DeviceTables& t, hipStream_t st);
+hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode,
+                         hipStream_t st);
+hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last_rank,
+                       uint64_t piece_base, uint64_t n_pieces, uint64_t rec_base,
+                       void* staging, int refresh_shadow, hipStream_t st);
+hipError_t launch_unpack(const DeviceTables& t, uint32_t n_ranks, uint64_t n_pieces,
+                         hipStream_t st);
+
+}  // namespace lc

@@ -1,0 +1,643 @@
+// Host runtime of the LayerCheck HIP library: validation, layer-aligned
+// tables, the call-order state machine and kernel launches behind the C
+// interface declared in include/layercheck.h.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <limits>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/layercheck.h"
+#include "lc_internal.h"
+
+using namespace lc;
+
+namespace {
+
+thread_local std::string g_error;
+
+lc_status fail(lc_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return st;
+}
+
+uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// Host-side layout derived from a descriptor (no GPU work).
+struct HostLayout {
+  uint32_t N = 0;
+  int dtype = 0;
+  uint32_t esz = 0;
+  bool has_master = false;
+  std::vector<lc_segment> segs;
+  std::vector<uint32_t> layer_seg_begin;  // [N+1]
+  std::vector<uint64_t> numel;            // [N]
+  std::vector<uint64_t> rec_bytes;        // [N]
+  std::vector<uint64_t> layer_pieces;     // [N]
+  std::vector<ScoreSeg> score_segs;
+  std::vector<uint32_t> chunk_seg;
+  std::vector<uint32_t> layer_chunk_begin;  // [N+1]
+  std::vector<CopyUnit> units;
+  std::vector<uint32_t> piece_unit;
+  std::vector<uint64_t> layer_piece_begin;  // [N+1]
+  uint64_t total_numel = 0;
+};
+
+lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
+  if (!d) return fail(LC_ERR_INVALID_ARG, "descriptor is NULL");
+  if (d->n_layers == 0) return fail(LC_ERR_INVALID_ARG, "n_layers must be >= 1");
+  if (d->n_segments < d->n_layers) return fail(LC_ERR_INVALID_ARG, "n_segments < n_layers");
+  if (!d->segments) return fail(LC_ERR_INVALID_ARG, "segments is NULL");
+  if (d->weight_dtype != LC_DT_BF16 && d->weight_dtype != LC_DT_F32)
+    return fail(LC_ERR_INVALID_ARG, "unknown weight dtype %d", d->weight_dtype);
+  if (d->has_master != 0 && d->has_master != 1) return fail(LC_ERR_INVALID_ARG, "has_master must be 0 or 1");
+  if (d->mode != LC_MODE_ACCUM && d->mode != LC_MODE_SNAPSHOT)
+    return fail(LC_ERR_INVALID_ARG, "unknown mode %d", d->mode);
+  if (d->reserved != 0) return fail(LC_ERR_INVALID_ARG, "reserved field must be 0");
+  if (!d->k0) return fail(LC_ERR_INVALID_ARG, "k0 is NULL");
+  for (uint32_t l = 0; l < d->n_layers; ++l)
+    if (!(d->k0[l] >= 0.0)) return fail(LC_ERR_INVALID_ARG, "k0[%u] must be >= 0", l);
+  if (d->s_max < 1) return fail(LC_ERR_INVALID_ARG, "s_max must be >= 1");
+  if (!(d->eps_w >= 0.0) || !std::isfinite(d->eps_w)) return fail(LC_ERR_INVALID_ARG, "eps_w must be finite and >= 0");
+
+  const uint32_t N = d->n_layers;
+  L.N = N;
+  L.dtype = d->weight_dtype;
+  L.esz = d->weight_dtype == LC_DT_BF16 ? 2 : 4;
+  L.has_master = d->has_master != 0;
+  L.segs.assign(d->segments, d->segments + d->n_segments);
+  L.layer_seg_begin.assign(N + 1, 0);
+  L.numel.assign(N, 0);
+  int64_t prev = -1;
+  for (uint32_t i = 0; i < d->n_segments; ++i) {
+    const lc_segment& s = L.segs[i];
+    if (s.layer >= N) return fail(LC_ERR_INVALID_ARG, "segment %u: layer %u out of range", i, s.layer);
+    if (static_cast<int64_t>(s.layer) < prev)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: segments must be grouped by ascending layer", i);
+    if (static_cast<int64_t>(s.layer) > prev + 1)
+      return fail(LC_ERR_INVALID_ARG, "layer %lld has no segment", static_cast<long long>(prev + 1));
+    if (s.reserved != 0) return fail(LC_ERR_INVALID_ARG, "segment %u: reserved field must be 0", i);
+    if (s.numel == 0) return fail(LC_ERR_INVALID_ARG, "segment %u: numel is 0", i);
+    if (s.numel > (1ull << 46)) return fail(LC_ERR_INVALID_ARG, "segment %u: numel too large", i);
+    if (!s.weight || !s.shadow || !s.exp_avg || !s.exp_avg_sq)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: NULL array pointer", i);
+    if ((s.master != nullptr) != L.has_master)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: master must be %s", i, L.has_master ? "non-NULL" : "NULL");
+    const uintptr_t wa = reinterpret_cast<uintptr_t>(s.weight), sa = reinterpret_cast<uintptr_t>(s.shadow);
+    if (wa % L.esz || sa % L.esz || reinterpret_cast<uintptr_t>(s.exp_avg) % 4 ||
+        reinterpret_cast<uintptr_t>(s.exp_avg_sq) % 4 || reinterpret_cast<uintptr_t>(s.master) % 4)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: misaligned pointer", i);
+    if (s.weight == s.shadow) return fail(LC_ERR_INVALID_ARG, "segment %u: weight and shadow alias", i);
+    if (static_cast<int64_t>(s.layer) != prev) L.layer_seg_begin[s.layer] = i;
+    prev = s.layer;
+    L.numel[s.layer] += s.numel;
+  }
+  if (prev != static_cast<int64_t>(N) - 1)
+    return fail(LC_ERR_INVALID_ARG, "layer %lld has no segment", static_cast<long long>(prev + 1));
+  L.layer_seg_begin[N] = d->n_segments;
+  L.total_numel = 0;
+  for (uint32_t l = 0; l < N; ++l) L.total_numel += L.numel[l];
+  // the staleness numerator sum_l n_l * age_l (age <= S_max - 1) must fit in 64 bits
+  if (L.total_numel > static_cast<uint64_t>(std::numeric_limits<int64_t>::max()) / static_cast<uint64_t>(d->s_max))
+    return fail(LC_ERR_INVALID_ARG, "total elements times s_max overflows 63 bits");
+
+  // score chunks
+  const uint64_t ce = kChunkBytes / L.esz;
+  L.layer_chunk_begin.assign(N + 1, 0);
+  uint64_t nchunks = 0;
+  for (uint32_t i = 0; i < d->n_segments; ++i) {
+    const lc_segment& s = L.segs[i];
+    ScoreSeg ss;
+    ss.w = reinterpret_cast<uint64_t>(s.weight);
+    ss.s = reinterpret_cast<uint64_t>(s.shadow);
+    ss.numel = s.numel;
+    ss.chunk_begin = static_cast<uint32_t>(nchunks);
+    ss.vec_ok = (ss.w % 16 == 0 && ss.s % 16 == 0) ? 1u : 0u;
+    const uint64_t k = (s.numel + ce - 1) / ce;
+    if (nchunks + k > 0xFFFFFFF0ull) return fail(LC_ERR_INVALID_ARG, "too many chunks");
+    for (uint64_t j = 0; j < k; ++j) L.chunk_seg.push_back(i);
+    nchunks += k;
+    L.score_segs.push_back(ss);
+    L.layer_chunk_begin[s.layer + 1] = static_cast<uint32_t>(nchunks);
+  }
+
+  // copy units in record order: W blocks, master blocks, m blocks, v blocks
+  L.rec_bytes.assign(N, 0);
+  L.layer_pieces.assign(N, 0);
+  L.layer_piece_begin.assign(N + 1, 0);
+  for (uint32_t l = 0; l < N; ++l) {
+    uint64_t rec = 0, pieces = 0;
+    for (int arr = 0; arr < 4; ++arr) {
+      if (arr == 1 && !L.has_master) continue;
+      for (uint32_t i = L.layer_seg_begin[l]; i < L.layer_seg_begin[l + 1]; ++i) {
+        const lc_segment& s = L.segs[i];
+        CopyUnit u{};
+        const void* base = arr == 0 ? s.weight : arr == 1 ? static_cast<void*>(s.master)
+                          : arr == 2 ? static_cast<void*>(s.exp_avg) : static_cast<void*>(s.exp_avg_sq);
+        u.arr = reinterpret_cast<uint64_t>(base);
+        u.shadow = arr == 0 ? reinterpret_cast<uint64_t>(s.shadow) : 0;
+        u.elem = arr == 0 ? L.esz : 4;
+        u.bytes = s.numel * u.elem;
+        u.rec_off = rec;
+        u.piece0 = static_cast<uint32_t>(pieces);
+        u.vec_ok = (u.arr % 16 == 0 && u.shadow % 16 == 0) ? 1u : 0u;
+        const uint64_t k = (u.bytes + kPieceBytes - 1) / kPieceBytes;
+        const uint32_t uid = static_cast<uint32_t>(L.units.size());
+        for (uint64_t j = 0; j < k; ++j) L.piece_unit.push_back(uid);
+        pieces += k;
+        rec += round_up(u.bytes, kRecordAlign);
+        L.units.push_back(u);
+      }
+    }
+    if (pieces > 0xFFFFFFF0ull) return fail(LC_ERR_INVALID_ARG, "layer %u record too large", l);
+    L.rec_bytes[l] = rec;
+    L.layer_pieces[l] = pieces;
+    L.layer_piece_begin[l + 1] = L.layer_piece_begin[l] + pieces;
+  }
+  return LC_OK;
+}
+
+}  // namespace
+
+struct lc_ctx {
+  HostLayout L;
+  int mode = 0;
+  int64_t s_max = 1;
+  double eps_w = 0;
+  int64_t t_base = 0;
+  hipStream_t stream = nullptr;
+  DeviceTables dt{};
+  std::vector<void*> allocations;
+  SelectHeader* h_result = nullptr;  // pinned: header + mask[N]
+
+  // state machine
+  bool poisoned = false;
+  int64_t last_step = 0;
+  bool scored = false;
+  int64_t scored_step = 0;
+  bool have_selection = false; // a selection (or the base) exists to pack
+  bool pending = false;        // a selection whose records are not all packed
+  bool result_on_host = false; // h_result reflects the pending selection
+  std::vector<uint32_t> sel;            // selected layers, ascending
+  std::vector<uint64_t> sel_rec_prefix, sel_piece_prefix;
+  std::vector<uint8_t> rank_packed;
+  uint32_t n_unpacked = 0;
+};
+
+namespace {
+
+#define LC_HIP(ctx, call)                                                                  \
+  do {                                                                                    \
+    hipError_t e_ = (call);                                                               \
+    if (e_ != hipSuccess) {                                                               \
+      if (ctx) (ctx)->poisoned = true;                                                    \
+      return fail(LC_ERR_HIP, "%s failed: %s (%s:%d)", #call, hipGetErrorString(e_), __FILE__, __LINE__); \
+    }                                                                                     \
+  } while (0)
+
+template <typename T>
+lc_status dev_alloc(lc_ctx* c, T** p, size_t count) {
+  void* q = nullptr;
+  const size_t bytes = count * sizeof(T) > 0 ? count * sizeof(T) : 16;
+  hipError_t e = hipMalloc(&q, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return fail(LC_ERR_OOM, "hipMalloc(%zu) failed: %s", bytes, hipGetErrorString(e));
+  }
+  c->allocations.push_back(q);
+  *p = static_cast<T*>(q);
+  return LC_OK;
+}
+
+template <typename T>
+lc_status upload(lc_ctx* c, T* dst, const std::vector<T>& src) {
+  if (src.empty()) return LC_OK;
+  LC_HIP(c, hipMemcpyAsync(dst, src.data(), src.size() * sizeof(T), hipMemcpyHostToDevice, c->stream));
+  return LC_OK;
+}
+
+void free_all(lc_ctx* c) {
+  for (void* p : c->allocations) (void)hipFree(p);
+  c->allocations.clear();
+  if (c->h_result) (void)hipHostFree(c->h_result);
+  c->h_result = nullptr;
+}
+
+lc_status check_ctx(lc_ctx* c) {
+  if (!c) return fail(LC_ERR_INVALID_ARG, "context is NULL");
+  if (c->poisoned) return fail(LC_ERR_BAD_STATE, "context is poisoned by an earlier HIP error");
+  return LC_OK;
+}
+
+// Make the pending selection's mask available on the host.
+lc_status fetch_result(lc_ctx* c) {
+  if (c->result_on_host) return LC_OK;
+  LC_HIP(c, hipStreamSynchronize(c->stream));
+  const uint32_t N = c->L.N;
+  const uint8_t* mask = reinterpret_cast<const uint8_t*>(c->h_result + 1);
+  c->sel.clear();
+  c->sel_rec_prefix.assign(1, 0);
+  c->sel_piece_prefix.assign(1, 0);
+  for (uint32_t l = 0; l < N; ++l) {
+    if (mask[l] > 1) return fail(LC_ERR_HIP, "corrupt selection mask");
+    if (mask[l]) {
+      c->sel.push_back(l);
+      c->sel_rec_prefix.push_back(c->sel_rec_prefix.back() + c->L.rec_bytes[l]);
+      c->sel_piece_prefix.push_back(c->sel_piece_prefix.back() + c->L.layer_pieces[l]);
+    }
+  }
+  if (c->sel.size() != c->h_result->n_selected || c->sel_rec_prefix.back() != c->h_result->payload_bytes) {
+    c->poisoned = true;
+    return fail(LC_ERR_HIP, "device selection plan disagrees with the host");
+  }
+  c->rank_packed.assign(c->sel.size(), 0);
+  c->n_unpacked = static_cast<uint32_t>(c->sel.size());
+  c->result_on_host = true;
+  if (c->n_unpacked == 0) c->pending = false;
+  return LC_OK;
+}
+
+lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode) {
+  LC_HIP(c, launch_select(c->dt, step, lr, base_mode, c->stream));
+  LC_HIP(c, hipMemcpyAsync(c->h_result, c->dt.result, sizeof(SelectHeader) + c->L.N,
+                           hipMemcpyDeviceToHost, c->stream));
+  c->have_selection = true;
+  c->pending = true;
+  c->result_on_host = false;
+  return LC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* lc_last_error(void) { return g_error.c_str(); }
+
+lc_status lc_query_layout(const lc_layout_desc* d, uint64_t* numel_out, uint64_t* record_bytes_out) {
+  HostLayout L;
+  lc_status st = build_layout(d, L);
+  if (st != LC_OK) return st;
+  for (uint32_t l = 0; l < L.N; ++l) {
+    if (numel_out) numel_out[l] = L.numel[l];
+    if (record_bytes_out) record_bytes_out[l] = L.rec_bytes[l];
+  }
+  return LC_OK;
+}
+
+lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
+  if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  lc_ctx* c = new (std::nothrow) lc_ctx();
+  if (!c) return fail(LC_ERR_OOM, "host allocation failed");
+  lc_status st = build_layout(d, c->L);
+  if (st != LC_OK) {
+    delete c;
+    return st;
+  }
+  c->mode = d->mode;
+  c->s_max = d->s_max;
+  c->eps_w = d->eps_w;
+  c->t_base = d->t_base;
+  c->stream = static_cast<hipStream_t>(d->stream);
+  c->last_step = d->t_base;
+  const HostLayout& L = c->L;
+  const uint32_t N = L.N;
+
+  auto bail = [&](lc_status s) {
+    (void)hipStreamSynchronize(c->stream);
+    free_all(c);
+    delete c;
+    return s;
+  };
+#define LC_TRY(expr)                   \
+  do {                                 \
+    lc_status s_ = (expr);             \
+    if (s_ != LC_OK) return bail(s_);  \
+  } while (0)
+
+  DeviceTables& t = c->dt;
+  t.n_layers = N;
+  t.n_chunks = static_cast<uint32_t>(L.chunk_seg.size());
+  t.dtype = L.dtype;
+  t.mode = d->mode;
+  t.eps_w = d->eps_w;
+  t.s_max = d->s_max;
+  ScoreSeg* segs; uint32_t* chunk_seg; uint32_t* lcb; double2* partials; double* u; double* delta;
+  int64_t* t_last; double* k0; uint64_t* numel; uint64_t* rec; uint64_t* lpieces; CopyUnit* units;
+  uint32_t* piece_unit; uint64_t* lpb; uint32_t* sel_layer; uint64_t* srp; uint64_t* spp;
+  SelectHeader* result; uint32_t* rank_layer; uint64_t* rank_src; uint64_t* rpp;
+  LC_TRY(dev_alloc(c, &segs, L.score_segs.size()));
+  LC_TRY(dev_alloc(c, &chunk_seg, L.chunk_seg.size()));
+  LC_TRY(dev_alloc(c, &lcb, N + 1));
+  LC_TRY(dev_alloc(c, &partials, L.chunk_seg.size()));
+  LC_TRY(dev_alloc(c, &u, N));
+  LC_TRY(dev_alloc(c, &delta, N));
+  LC_TRY(dev_alloc(c, &t_last, N));
+  LC_TRY(dev_alloc(c, &k0, N));
+  LC_TRY(dev_alloc(c, &numel, N));
+  LC_TRY(dev_alloc(c, &rec, N));
+  LC_TRY(dev_alloc(c, &lpieces, N));
+  LC_TRY(dev_alloc(c, &units, L.units.size()));
+  LC_TRY(dev_alloc(c, &piece_unit, L.piece_unit.size()));
+  LC_TRY(dev_alloc(c, &lpb, N + 1));
+  LC_TRY(dev_alloc(c, &sel_layer, N));
+  LC_TRY(dev_alloc(c, &srp, N + 1));
+  LC_TRY(dev_alloc(c, &spp, N + 1));
+  {
+    uint8_t* r8;
+    LC_TRY(dev_alloc(c, &r8, sizeof(SelectHeader) + N));
+    result = reinterpret_cast<SelectHeader*>(r8);
+  }
+  LC_TRY(dev_alloc(c, &rank_layer, N));
+  LC_TRY(dev_alloc(c, &rank_src, N));
+  LC_TRY(dev_alloc(c, &rpp, N + 1));
+  {
+    void* h = nullptr;
+    hipError_t e = hipHostMalloc(&h, sizeof(SelectHeader) + N, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return bail(fail(LC_ERR_OOM, "hipHostMalloc failed: %s", hipGetErrorString(e)));
+    }
+    c->h_result = static_cast<SelectHeader*>(h);
+  }
+  t.segs = segs; t.chunk_seg = chunk_seg; t.layer_chunk_begin = lcb; t.partials = partials;
+  t.u = u; t.delta = delta; t.t_last = t_last; t.k0 = k0; t.numel = numel; t.rec_bytes = rec;
+  t.layer_pieces = lpieces; t.units = units; t.piece_unit = piece_unit; t.layer_piece_begin = lpb;
+  t.sel_layer = sel_layer; t.sel_rec_prefix = srp; t.sel_piece_prefix = spp; t.result = result;
+  t.rank_layer = rank_layer; t.rank_src = rank_src; t.rank_piece_prefix = rpp;
+
+  std::vector<double> zeros(N, 0.0), k0v(d->k0, d->k0 + N);
+  std::vector<int64_t> tl(N, d->t_base);
+  LC_TRY(upload(c, segs, L.score_segs));
+  LC_TRY(upload(c, chunk_seg, L.chunk_seg));
+  LC_TRY(upload(c, lcb, L.layer_chunk_begin));
+  LC_TRY(upload(c, u, zeros));
+  LC_TRY(upload(c, delta, zeros));
+  LC_TRY(upload(c, t_last, tl));
+  LC_TRY(upload(c, k0, k0v));
+  LC_TRY(upload(c, numel, L.numel));
+  LC_TRY(upload(c, rec, L.rec_bytes));
+  LC_TRY(upload(c, lpieces, L.layer_pieces));
+  LC_TRY(upload(c, units, L.units));
+  LC_TRY(upload(c, piece_unit, L.piece_unit));
+  LC_TRY(upload(c, lpb, L.layer_piece_begin));
+  // S <- W for every segment (Section 3.2: drift is measured from the base)
+  for (const lc_segment& s : L.segs) {
+    hipError_t e = hipMemcpyAsync(s.shadow, s.weight, s.numel * L.esz, hipMemcpyDeviceToDevice, c->stream);
+    if (e != hipSuccess) return bail(fail(LC_ERR_HIP, "shadow init copy failed: %s", hipGetErrorString(e)));
+  }
+  // base selection: every layer, at t_base
+  LC_TRY(enqueue_select(c, d->t_base, 1.0, 1));
+  {
+    hipError_t e = hipStreamSynchronize(c->stream);
+    if (e != hipSuccess) return bail(fail(LC_ERR_HIP, "init failed: %s", hipGetErrorString(e)));
+  }
+#undef LC_TRY
+  *out = c;
+  return LC_OK;
+}
+
+lc_status lc_score_layers(lc_ctx* c, int64_t step) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (step <= c->last_step)
+    return fail(LC_ERR_BAD_STATE, "step %lld must exceed the previous step %lld", static_cast<long long>(step),
+                static_cast<long long>(c->last_step));
+  if (c->mode == LC_MODE_SNAPSHOT && c->pending) {
+    if (!c->result_on_host) {
+      st = fetch_result(c);
+      if (st != LC_OK) return st;
+    }
+    if (c->pending)
+      return fail(LC_ERR_BAD_STATE, "SNAPSHOT mode: the previous selection is not fully packed");
+  }
+  LC_HIP(c, launch_score(c->dt, c->stream));
+  c->last_step = step;
+  c->scored = true;
+  c->scored_step = step;
+  c->have_selection = false;
+  c->pending = false;
+  c->result_on_host = false;
+  return LC_OK;
+}
+
+lc_status lc_select(lc_ctx* c, int64_t step, double lr_scale, uint8_t* mask_out, lc_select_stats* stats_out) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (!c->scored || c->scored_step != step)
+    return fail(LC_ERR_BAD_STATE, "lc_select(%lld) must follow lc_score_layers at the same step",
+                static_cast<long long>(step));
+  if (!(lr_scale > 0.0) || !std::isfinite(lr_scale))
+    return fail(LC_ERR_INVALID_ARG, "lr_scale must be positive and finite");
+  st = enqueue_select(c, step, lr_scale, 0);
+  if (st != LC_OK) return st;
+  c->scored = false;
+  if (mask_out || stats_out) {
+    st = fetch_result(c);
+    if (st != LC_OK) return st;
+    if (mask_out) std::memcpy(mask_out, c->h_result + 1, c->L.N);
+    if (stats_out) {
+      const SelectHeader& h = *c->h_result;
+      stats_out->n_selected = h.n_selected;
+      stats_out->n_forced = h.n_forced;
+      stats_out->payload_bytes = h.payload_bytes;
+      stats_out->max_age = h.max_age;
+      stats_out->weighted_age = h.weighted_age;
+    }
+  }
+  return LC_OK;
+}
+
+lc_status lc_pack_selected(lc_ctx* c, void* staging, uint64_t capacity, uint32_t first_rank,
+                           lc_pack_result* out) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
+  if (!c->have_selection) return fail(LC_ERR_BAD_STATE, "no selection to pack");
+  st = fetch_result(c);
+  if (st != LC_OK) return st;
+  const uint32_t ns = static_cast<uint32_t>(c->sel.size());
+  if (first_rank > ns) return fail(LC_ERR_INVALID_ARG, "first_rank %u > %u selected", first_rank, ns);
+  uint32_t last = first_rank;
+  while (last < ns && c->sel_rec_prefix[last + 1] - c->sel_rec_prefix[first_rank] <= capacity) ++last;
+  if (last == first_rank && first_rank < ns)
+    return fail(LC_ERR_CAPACITY, "record of layer %u (%llu B) exceeds capacity %llu", c->sel[first_rank],
+                static_cast<unsigned long long>(c->L.rec_bytes[c->sel[first_rank]]),
+                static_cast<unsigned long long>(capacity));
+  const uint64_t bytes = c->sel_rec_prefix[last] - c->sel_rec_prefix[first_rank];
+  if (last > first_rank) {
+    if (!staging) return fail(LC_ERR_INVALID_ARG, "staging is NULL");
+    if (reinterpret_cast<uintptr_t>(staging) % kRecordAlign)
+      return fail(LC_ERR_INVALID_ARG, "staging must be %u-byte aligned", kRecordAlign);
+    const uint64_t pieces = c->sel_piece_prefix[last] - c->sel_piece_prefix[first_rank];
+    if (pieces >= (1ull << 32) / kCopyThreads) return fail(LC_ERR_INVALID_ARG, "pack range too large for one launch");
+    LC_HIP(c, launch_pack(c->dt, first_rank, last, c->sel_piece_prefix[first_rank], pieces,
+                          c->sel_rec_prefix[first_rank], staging, c->mode == LC_MODE_SNAPSHOT, c->stream));
+    for (uint32_t r = first_rank; r < last; ++r)
+      if (!c->rank_packed[r]) {
+        c->rank_packed[r] = 1;
+        --c->n_unpacked;
+      }
+  }
+  if (c->n_unpacked == 0) c->pending = false;
+  out->bytes_written = bytes;
+  out->n_packed = last - first_rank;
+  out->next_rank = last;
+  out->done = last == ns ? 1 : 0;
+  out->reserved = 0;
+  return LC_OK;
+}
+
+lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versions, int64_t t_fail,
+                               int64_t* chosen_step_out) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (!v || n_versions == 0) return fail(LC_ERR_INVALID_ARG, "no versions");
+  const HostLayout& L = c->L;
+  const uint32_t N = L.N;
+  for (uint32_t i = 0; i < n_versions; ++i) {
+    if (!v[i].mask) return fail(LC_ERR_INVALID_ARG, "version %u: mask is NULL", i);
+    uint64_t need = 0;
+    for (uint32_t l = 0; l < N; ++l) {
+      if (v[i].mask[l] > 1) return fail(LC_ERR_INVALID_ARG, "version %u: mask must be 0/1", i);
+      if (v[i].mask[l]) need += L.rec_bytes[l];
+    }
+    if (need != v[i].payload_bytes)
+      return fail(LC_ERR_INVALID_ARG, "version %u: payload_bytes %llu != %llu for its mask", i,
+                  static_cast<unsigned long long>(v[i].payload_bytes), static_cast<unsigned long long>(need));
+    if (need && !v[i].payload) return fail(LC_ERR_INVALID_ARG, "version %u: payload is NULL", i);
+  }
+  // plan (Section 3.5): newest version <= t_fail holding the layer
+  std::vector<int64_t> choice(N, -1);
+  for (uint32_t l = 0; l < N; ++l) {
+    int64_t best = -1;
+    bool dup = false;
+    for (uint32_t i = 0; i < n_versions; ++i) {
+      if (v[i].step > t_fail || !v[i].mask[l]) continue;
+      if (best < 0 || v[i].step > v[best].step) {
+        best = i;
+        dup = false;
+      } else if (v[i].step == v[best].step) {
+        dup = true;
+      }
+    }
+    if (best < 0)
+      return fail(LC_ERR_NO_VERSION, "layer %u: no persisted version at step <= %lld", l,
+                  static_cast<long long>(t_fail));
+    if (dup)
+      return fail(LC_ERR_INVALID_ARG, "layer %u: two versions at step %lld", l,
+                  static_cast<long long>(v[best].step));
+    choice[l] = best;
+  }
+  // record address of each layer, and where each version's payload lives
+  std::vector<int> kind(n_versions, -1);  // 0 device, 1 host
+  std::vector<const uint8_t*> dev_base(n_versions, nullptr);
+  std::vector<uint32_t> rank_layer;
+  std::vector<uint64_t> rank_src, rank_pp(1, 0);
+  std::vector<std::pair<uint32_t, const uint8_t*>> host_layers;
+  for (uint32_t l = 0; l < N; ++l) {
+    const uint32_t i = static_cast<uint32_t>(choice[l]);
+    if (kind[i] < 0) {
+      hipPointerAttribute_t attr;
+      hipError_t e = hipPointerGetAttributes(&attr, v[i].payload);
+      if (e == hipSuccess && attr.type == hipMemoryTypeDevice) {
+        kind[i] = 0;
+        dev_base[i] = static_cast<const uint8_t*>(v[i].payload);
+      } else {
+        (void)hipGetLastError();
+        kind[i] = 1;
+      }
+    }
+    uint64_t off = 0;
+    for (uint32_t j = 0; j < l; ++j)
+      if (v[i].mask[j]) off += L.rec_bytes[j];
+    if (kind[i] == 0) {
+      rank_layer.push_back(l);
+      rank_src.push_back(reinterpret_cast<uint64_t>(dev_base[i] + off));
+      rank_pp.push_back(rank_pp.back() + L.layer_pieces[l]);
+    } else {
+      host_layers.emplace_back(l, static_cast<const uint8_t*>(v[i].payload) + off);
+    }
+  }
+  if (!rank_layer.empty()) {
+    st = upload(c, c->dt.rank_layer, rank_layer);
+    if (st != LC_OK) return st;
+    st = upload(c, c->dt.rank_src, rank_src);
+    if (st != LC_OK) return st;
+    st = upload(c, c->dt.rank_piece_prefix, rank_pp);
+    if (st != LC_OK) return st;
+    const uint64_t pieces = rank_pp.back();
+    if (pieces >= (1ull << 32) / kCopyThreads) return fail(LC_ERR_INVALID_ARG, "restore too large for one launch");
+    LC_HIP(c, launch_unpack(c->dt, static_cast<uint32_t>(rank_layer.size()), pieces, c->stream));
+  }
+  // host-resident records: one copy per block, then S <- W
+  for (const auto& hl : host_layers) {
+    const uint32_t l = hl.first;
+    uint32_t ub = 0;
+    for (uint32_t j = 0; j < l; ++j) {
+      const uint32_t nseg = L.layer_seg_begin[j + 1] - L.layer_seg_begin[j];
+      ub += nseg * (L.has_master ? 4 : 3);
+    }
+    const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * (L.has_master ? 4 : 3);
+    for (uint32_t k = 0; k < nu; ++k) {
+      const CopyUnit& u = L.units[ub + k];
+      LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.arr), hl.second + u.rec_off, u.bytes,
+                               hipMemcpyHostToDevice, c->stream));
+      if (u.shadow)
+        LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.shadow), reinterpret_cast<void*>(u.arr), u.bytes,
+                                 hipMemcpyDeviceToDevice, c->stream));
+    }
+  }
+  std::vector<double> zeros(N, 0.0);
+  std::vector<int64_t> steps(N);
+  for (uint32_t l = 0; l < N; ++l) steps[l] = v[choice[l]].step;
+  st = upload(c, c->dt.delta, zeros);
+  if (st != LC_OK) return st;
+  st = upload(c, c->dt.t_last, steps);
+  if (st != LC_OK) return st;
+  LC_HIP(c, hipStreamSynchronize(c->stream));
+  if (chosen_step_out) std::memcpy(chosen_step_out, steps.data(), N * sizeof(int64_t));
+  c->last_step = t_fail;
+  c->scored = false;
+  c->have_selection = false;
+  c->pending = false;
+  c->result_on_host = false;
+  return LC_OK;
+}
+
+lc_status lc_read_state(lc_ctx* c, double* u_out, double* delta_out, int64_t* t_last_out) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  const size_t N = c->L.N;
+  LC_HIP(c, hipStreamSynchronize(c->stream));
+  if (u_out) LC_HIP(c, hipMemcpy(u_out, c->dt.u, N * sizeof(double), hipMemcpyDeviceToHost));
+  if (delta_out) LC_HIP(c, hipMemcpy(delta_out, c->dt.delta, N * sizeof(double), hipMemcpyDeviceToHost));
+  if (t_last_out) LC_HIP(c, hipMemcpy(t_last_out, c->dt.t_last, N * sizeof(int64_t), hipMemcpyDeviceToHost));
+  return LC_OK;
+}
+
+uint64_t lc_record_bytes(const lc_ctx* c, uint32_t layer) {
+  if (!c || layer >= c->L.N) return 0;
+  return c->L.rec_bytes[layer];
+}
+
+lc_status lc_destroy(lc_ctx* c) {
+  if (!c) return LC_OK;
+  hipError_t e = hipStreamSynchronize(c->stream);
+  free_all(c);
+  delete c;
+  if (e != hipSuccess) return fail(LC_ERR_HIP, "stream synchronize failed: %s", hipGetErrorString(e));
+  return LC_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,130 @@
+"""The C interface on the CPU: the library loads, exports every declared
+entry point, and its host-side validation and record layout behave as
+specified (no device work is issued by these calls)."""
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import layercheck_oracle as O
+from paper_2609_27193_amd import layercheck as LC
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LC.LIB_PATH):
+        from paper_2609_27193_amd.build_lib import build
+        build()
+    return LC.load_library()
+
+
+def declared_functions():
+    text = open(os.path.join(ROOT, "include", "layercheck.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(lc_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert set(names) == set(LC.EXPORTED), names
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+FAKE = 0x7F0000000000  # never dereferenced by lc_query_layout
+
+
+def fake_segments(sizes, esz=2, master=True, offset=0):
+    segs, addr = [], FAKE + offset
+    for l, layer in enumerate(sizes):
+        for n in layer:
+            step = (n * 4 + 255) // 256 * 256
+            segs.append(LC.Segment(l, n, addr, addr + step, addr + 2 * step if master else None,
+                                   addr + 3 * step, addr + 4 * step))
+            addr += 5 * step
+    return segs
+
+
+def desc(segs, n_layers, **kw):
+    args = dict(weight_dtype=LC.LC_DT_BF16, has_master=True, mode=LC.LC_MODE_ACCUM,
+                k0=[1e-3] * n_layers, s_max=8, eps_w=1e-8, t_base=0)
+    args.update(kw)
+    return LC.LayoutDesc(segs, n_layers, **args)
+
+
+@pytest.mark.parametrize("sizes,dtype,master", [
+    ([[1], [3, 7], [8, 1023, 4097]], LC.LC_DT_BF16, True),
+    ([[65536 * 3 + 5], [128]], LC.LC_DT_BF16, False),
+    ([[17, 33], [100000]], LC.LC_DT_F32, False),
+])
+def test_record_bytes_match_oracle(lib, sizes, dtype, master):
+    segs = fake_segments(sizes, esz=2 if dtype == LC.LC_DT_BF16 else 4, master=master)
+    numel, rec = LC.lc_query_layout(desc(segs, len(sizes), weight_dtype=dtype, has_master=master))
+    assert numel == [sum(l) for l in sizes]
+    esz = 2 if dtype == LC.LC_DT_BF16 else 4
+    assert rec == [O.record_bytes(l, esz, master) for l in sizes]
+
+
+def _expect(code, fn):
+    with pytest.raises(LC.LCError) as e:
+        fn()
+    assert e.value.code == code, str(e.value)
+    assert LC.load_library().lc_last_error().decode()
+
+
+def test_validation_errors(lib):
+    good = fake_segments([[4], [4]])
+    q = lambda **kw: LC.lc_query_layout(desc(kw.pop("segs", good), kw.pop("n", 2), **kw))
+    q()  # valid
+    I = LC.LC_ERR_INVALID_ARG
+    _expect(I, lambda: q(weight_dtype=3))
+    _expect(I, lambda: q(mode=2))
+    _expect(I, lambda: q(s_max=0))
+    _expect(I, lambda: q(eps_w=-1.0))
+    _expect(I, lambda: q(eps_w=float("inf")))
+    _expect(I, lambda: q(k0=[1e-3, -1.0]))
+    _expect(I, lambda: q(k0=[1e-3, float("nan")]))
+    _expect(I, lambda: q(has_master=False))         # master pointers present
+    _expect(I, lambda: q(segs=good[::-1]))            # not grouped by ascending layer
+    _expect(I, lambda: q(n=3, k0=[1e-3] * 3))         # layer 2 has no segment
+    bad = fake_segments([[4], [4]])
+    bad[0].numel = 0
+    _expect(I, lambda: q(segs=bad))
+    bad = fake_segments([[4], [4]])
+    bad[1].weight += 1                                  # odd address for bf16
+    _expect(I, lambda: q(segs=bad))
+    bad = fake_segments([[4], [4]])
+    bad[1].shadow = bad[1].weight
+    _expect(I, lambda: q(segs=bad))
+    bad = fake_segments([[4], [4]])
+    bad[0].exp_avg = 0
+    _expect(I, lambda: q(segs=bad))
+    bad = fake_segments([[4], [4]])
+    bad[1].layer = 5
+    _expect(I, lambda: q(segs=bad))
+    big = fake_segments([[1 << 40]])
+    _expect(I, lambda: q(segs=big, n=1, k0=[1e-3], s_max=1 << 30))  # staleness numerator overflow
+    with pytest.raises(ValueError):
+        desc(good, 2, k0=[1e-3])
+
+
+def test_null_handling(lib):
+    assert lib.lc_destroy(None) == LC.LC_OK
+    assert lib.lc_record_bytes(None, 0) == 0
+    assert lib.lc_query_layout(None, None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_init_layout(None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_score_layers(None, 1) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_select(None, 1, 1.0, None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_pack_selected(None, None, 0, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_read_state(None, None, None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_restore_composite(None, None, 0, 0, None) == LC.LC_ERR_INVALID_ARG
+
+
+def test_invalid_init_enqueues_nothing(lib):
+    # validation happens before any HIP call, so this runs without a GPU
+    bad = fake_segments([[4], [4]])
+    bad[0].numel = 0
+    _expect(LC.LC_ERR_INVALID_ARG, lambda: LC.lc_init_layout(desc(bad, 2)))

@@ -18,18 +18,18 @@ MUTANTS = {
     "eps_dropped": ("np.float64(B / n + eps_w)", "np.float64(B / n)"),
     "eps_outside_mean": ("np.float64(B / n + eps_w)", "np.float64((B + eps_w) / n)"),
     "per_tensor_count": ("n += int(w.size)", "n = int(w.size)"),
-    "strict_threshold": ("by_drift = self.delta[l] >= K", "by_drift = self.delta[l] > K"),
-    "strict_staleness": ("by_age = age >= self.s_max", "by_age = age > self.s_max"),
-    "lr_scale_ignored": ("K = self.k0[l] * lr_scale", "K = self.k0[l]"),
-    "lr_scale_inverted": ("K = self.k0[l] * lr_scale", "K = self.k0[l] / lr_scale"),
-    "no_reset": ("                self.delta[l] = 0.0\n                self.t_last[l] = step",
-                 "                self.t_last[l] = step"),
-    "no_timestamp": ("                self.delta[l] = 0.0\n                self.t_last[l] = step",
-                     "                self.delta[l] = 0.0"),
+    "strict_threshold": ("by_drift = delta[l] >= K", "by_drift = delta[l] > K"),
+    "strict_staleness": ("by_age = age >= s_max", "by_age = age > s_max"),
+    "lr_scale_ignored": ("K = k0[l] * lr_scale", "K = k0[l]"),
+    "lr_scale_inverted": ("K = k0[l] * lr_scale", "K = k0[l] / lr_scale"),
+    "no_reset": ("            if mask[l]:  # Eq. 4: reset on persist\n                self.delta[l] = 0.0\n",
+                 "            if mask[l]:  # Eq. 4: reset on persist\n"),
+    "no_timestamp": ("                self.delta[l] = 0.0\n                self.t_last[l] = step\n        self.scored_step = None",
+                     "                self.delta[l] = 0.0\n        self.scored_step = None"),
     "accum_overwrites": ("self.delta[l] = self.delta[l] + u", "self.delta[l] = u"),
     "accum_shadow_stale": ("        if self.mode == MODE_ACCUM:\n            # the next step's",
                            "        if False:\n            # the next step's"),
-    "forced_count_wrong": ("if not by_drift:\n                    n_forced += 1", "if by_age:\n                    n_forced += 1"),
+    "forced_count_wrong": ("forced[l] = 0 if by_drift else 1", "forced[l] = 1 if by_age else 0"),
     "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
     "moments_swapped": ('+ ["exp_avg", "exp_avg_sq"]', '+ ["exp_avg_sq", "exp_avg"]'),
     "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),

@@ -1,0 +1,228 @@
+"""GPU parity: the HIP library through its C interface against the CPU oracle.
+
+Sizes are chosen so the oracle finishes in seconds while the layouts still
+span many score chunks (32768 bf16 / 16384 fp32 elements) and pack pieces
+(64 KiB) with ragged tails.
+"""
+import numpy as np
+import pytest
+
+from oracle import layercheck_oracle as O
+from paper_2609_27193_amd import layercheck as LC
+from paper_2609_27193_amd import inputs as I
+from tests.conftest import gpu_available
+from tests.gpu_harness import Pair, log, torch_bytes
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not gpu_available():
+        pytest.skip("needs an MI355X")
+    LC.load_library()  # a missing build fails here, loudly
+
+
+def k0_for(spec, base):
+    return [base * (10.0 if l.name == "embed_tokens" else 1.0) for l in spec.layers]
+
+
+def reduced_8b():
+    return I.scaled_spec(I.llama3_8b_spec(), hidden=256, ffn=896, n_blocks=4, vocab=1000, n_q=8, n_kv=2)
+
+
+def reduced_qwen():
+    return I.scaled_spec(I.qwen25_14b_spec(), hidden=320, ffn=864, n_blocks=3, vocab=777, n_q=5, n_kv=1,
+                         qkv_bias=True)
+
+
+def reduced_13b():
+    return I.scaled_spec(I.llama2_13b_spec(), hidden=320, ffn=864, n_blocks=4, vocab=640, n_q=5, n_kv=5)
+
+
+def run_steps(p, steps, lr=lambda t: 1.0, capacity=None):
+    fracs = []
+    for t in steps:
+        mask, st = p.step(t, lr(t), capacity(t) if capacity else None)
+        fracs.append(mask.mean())
+        log(f"  step {t}: selected {st['n_selected']}/{p.N} forced {st['n_forced']} "
+            f"payload {st['payload_bytes']} max_age {st['max_age']} w_age {st['weighted_age']:.3f}")
+    return fracs
+
+
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_toy_ten_steps(mode):
+    """The toy decoder (fp32 weights, 3.67M params, S_max = 4) for 10 steps."""
+    spec = I.toy_spec()
+    log(f"toy mode={mode}")
+    p = Pair(spec, mode, k0_for(spec, 0.08))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))  # base version
+        fracs = run_steps(p, range(1, 11))
+        log(f"  mean selected fraction {np.mean(fracs):.3f}; near-threshold excluded {p.near_excluded}, "
+            f"resyncs {p.resyncs}")
+        p.check_arrays()
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("maker,mode", [(reduced_8b, LC.LC_MODE_ACCUM), (reduced_8b, LC.LC_MODE_SNAPSHOT),
+                                        (reduced_qwen, LC.LC_MODE_ACCUM), (reduced_13b, LC.LC_MODE_SNAPSHOT)],
+                         ids=["8b-accum", "8b-snapshot", "qwen-accum", "13b-snapshot"])
+def test_reduced_bf16(maker, mode):
+    """bf16 weights (with and without master), learning-rate scaling and
+    capacity-limited packing in several calls."""
+    spec = maker()
+    log(f"{spec.name} mode={mode} P={spec.numel}")
+    p = Pair(spec, mode, k0_for(spec, 0.01))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        cap = lambda t: (max(p.R) + 4096) if t % 3 == 0 else None  # several pack calls on some steps
+        run_steps(p, range(1, 13), lr=lambda t: 1.0 if t < 6 else 0.5, capacity=cap)
+        p.check_arrays()
+    finally:
+        p.close()
+
+
+def _restore_and_compare(p, t_fail, where):
+    import torch
+    versions_c, versions_o = [], []
+    keep = []
+    for (step, mask, dev), (_, _, host) in zip(p.versions_dev, p.versions_host):
+        if where == "device":
+            ptr = dev.data_ptr() if dev is not None else 0
+        elif where == "pinned":
+            t = torch.from_numpy(host).pin_memory() if len(host) else None
+            keep.append(t)
+            ptr = t.data_ptr() if t is not None else 0
+        else:
+            arr = np.ascontiguousarray(host)
+            keep.append(arr)
+            ptr = arr.ctypes.data if len(arr) else 0
+        versions_c.append({"step": step, "mask": mask, "payload": ptr, "payload_bytes": len(host)})
+        versions_o.append({"step": step, "mask": mask, "payload": host})
+    # fail-stop: the live state is lost on both sides
+    for t in (p.dW, p.dS, p.dm, p.dv) + ((p.dM,) if p.dM is not None else ()):
+        t.fill_(0)
+    for a in (p.hW, p.hS, p.hm, p.hv) + ((p.hM,) if p.hM is not None else ()):
+        a[...] = 0
+    torch.cuda.synchronize()
+    chosen = LC.lc_restore_composite(p.ctx, versions_c, t_fail, p.N)
+    chosen_o = p.orc.restore(versions_o, t_fail)
+    assert chosen.tolist() == chosen_o.tolist()
+    p.check_arrays()
+    u, d, tl = LC.lc_read_state(p.ctx, p.N)
+    assert tl.tolist() == chosen.tolist() and not d.any()
+    return chosen
+
+
+@pytest.mark.parametrize("where", ["device", "pinned", "pageable"])
+def test_restore_composite_then_continue(where):
+    """Mixed-timestamp recovery (Section 3.5) from versions held in device,
+    pinned-host and pageable-host memory; training then resumes after t_fail
+    and both sides keep agreeing."""
+    spec = reduced_8b()
+    p = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 0.01))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        run_steps(p, range(1, 9))
+        t_fail = 6
+        chosen = _restore_and_compare(p, t_fail, where)
+        log(f"  restored from steps {sorted(set(chosen.tolist()))}")
+        assert len(set(chosen.tolist())) >= 2
+        p.adopt_restored()  # resume from the composite state
+        run_steps(p, range(t_fail + 1, t_fail + 4))
+    finally:
+        p.close()
+
+
+def test_restore_roundtrip_repack():
+    """Restore, then re-pack every layer: each record equals the record it was
+    restored from, bit for bit."""
+    import torch
+    spec = reduced_qwen()
+    p = Pair(spec, LC.LC_MODE_SNAPSHOT, k0_for(spec, 0.01))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        run_steps(p, range(1, 7))
+        chosen = _restore_and_compare(p, 5, "device")
+        lay2 = LC.LayoutDesc(p.lsegs, p.N, p.dtype, spec.has_master, LC.LC_MODE_SNAPSHOT, p.k0,
+                             spec.s_max, stream=p.stream)
+        ctx2 = LC.lc_init_layout(lay2)
+        try:
+            total = sum(p.R)
+            st = torch.empty(total, dtype=torch.uint8, device="cuda")
+            res = LC.lc_pack_selected(ctx2, st.data_ptr(), total, 0)
+            assert res["done"] == 1 and res["bytes_written"] == total
+            allrec = torch_bytes(st)
+            pos = 0
+            for l in range(p.N):
+                v = [vv for vv in p.versions_host if vv[0] == chosen[l]][0]
+                off = sum(p.R[j] for j in range(l) if v[1][j])
+                assert np.array_equal(allrec[pos:pos + p.R[l]], v[2][off:off + p.R[l]]), l
+                pos += p.R[l]
+        finally:
+            LC.lc_destroy(ctx2)
+    finally:
+        p.close()
+
+
+def test_state_machine_errors():
+    import torch
+    spec = reduced_8b()
+    p = Pair(spec, LC.LC_MODE_SNAPSHOT, k0_for(spec, 0.01))
+    try:
+        def expect(code, fn):
+            with pytest.raises(LC.LCError) as e:
+                fn()
+            assert e.value.code == code, str(e.value)
+        B, I_, C_, NV = LC.LC_ERR_BAD_STATE, LC.LC_ERR_INVALID_ARG, LC.LC_ERR_CAPACITY, LC.LC_ERR_NO_VERSION
+        expect(B, lambda: LC.lc_score_layers(p.ctx, 1))        # base not packed (SNAPSHOT)
+        expect(B, lambda: LC.lc_select(p.ctx, 1, 1.0, p.N))    # select before score
+        st = torch.empty(max(p.R), dtype=torch.uint8, device="cuda")
+        expect(C_, lambda: LC.lc_pack_selected(p.ctx, st.data_ptr(), min(p.R) - 1, 0))
+        expect(I_, lambda: LC.lc_pack_selected(p.ctx, st.data_ptr() + 16, max(p.R), 0))  # misaligned staging
+        expect(I_, lambda: LC.lc_pack_selected(p.ctx, st.data_ptr(), max(p.R), p.N + 1))
+        p.pack(0, np.ones(p.N, np.uint8))
+        p.advance(1)
+        p.score(1)
+        expect(I_, lambda: LC.lc_select(p.ctx, 1, 0.0, p.N))
+        expect(I_, lambda: LC.lc_select(p.ctx, 1, float("inf"), p.N))
+        expect(B, lambda: LC.lc_select(p.ctx, 2, 1.0, p.N))
+        expect(B, lambda: LC.lc_score_layers(p.ctx, 1))        # not increasing
+        d, tl = LC.lc_read_state(p.ctx, p.N)[1:]
+        mask, _ = p.select(1, 1.0, d, tl)
+        p.pack(1, mask)
+        # restore errors
+        full = np.ones(p.N, np.uint8)
+        dev = p.versions_dev[0][2]
+        v0 = {"step": 0, "mask": full, "payload": dev.data_ptr(), "payload_bytes": sum(p.R)}
+        expect(NV, lambda: LC.lc_restore_composite(p.ctx, [v0], -1, p.N))
+        expect(I_, lambda: LC.lc_restore_composite(p.ctx, [v0, dict(v0)], 3, p.N))
+        expect(I_, lambda: LC.lc_restore_composite(p.ctx, [dict(v0, payload_bytes=sum(p.R) - 256)], 3, p.N))
+        expect(I_, lambda: LC.lc_restore_composite(p.ctx, [], 3, p.N))
+        p.check_arrays()  # failed calls changed nothing
+    finally:
+        p.close()
+
+
+def test_scores_bitwise_reproducible_and_zero_change():
+    """No floating-point atomics: two contexts over identical inputs give
+    bit-identical scores; an unchanged state scores exactly zero."""
+    spec = reduced_8b()
+    pa = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 1e9))
+    pb = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 1e9))
+    try:
+        for p in (pa, pb):
+            p.pack(0, np.ones(p.N, np.uint8))
+            p.score(1)  # no update since init: u == 0 exactly on both sides
+            assert not LC.lc_read_state(p.ctx, p.N)[0].any()
+            p.select(1, 1.0)
+            p.advance(2)
+            p.score(2)
+        ua = LC.lc_read_state(pa.ctx, pa.N)[0]
+        ub = LC.lc_read_state(pb.ctx, pb.N)[0]
+        assert ua.any() and np.array_equal(ua.view(np.uint64), ub.view(np.uint64))
+    finally:
+        pa.close()
+        pb.close()
