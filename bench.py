@@ -31,6 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+CHUNK_BYTES = int(os.environ.get("LC_CHUNK_BYTES", 16 * 1024))  # score chunk (bytes of W per partial)
 METRIC = "GB/s of model state scored+packed per decision step (% of HBM peak); ms/step"
 
 
@@ -48,6 +49,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also run one plain 4 GiB device copy (counter calibration)")
+    ap.add_argument("--k0", type=float, default=None,
+                    help="base threshold (skips the calibration window)")
     ap.add_argument("--json-out", default=None)
     return ap.parse_args()
 
@@ -102,15 +105,15 @@ def calibrate_k0(u_hist: np.ndarray, embed_mask: np.ndarray, s_max: int, target:
     return 10.0 ** hi
 
 
-def cpu_baseline(state, spec, mode_name):
-    """Time the oracle on one transformer block of the same state (host copy,
-    D2H excluded): score + select (forced) + pack of that block."""
+def cpu_baseline(state, spec, mode_name, n_layers=3):
+    """Time the oracle on the first ``n_layers`` transformer blocks of the same
+    state (host copy, D2H excluded): score + select (all forced) + pack."""
     import torch
     from oracle import layercheck_oracle as O
     from paper_2609_27193_amd.inputs import to_numpy_weight
 
-    li = next(i for i, l in enumerate(spec.layers) if l.name.startswith("block_"))
-    segs = [s for s in state.segments if s.layer == li]
+    blocks = [i for i, l in enumerate(spec.layers) if l.name.startswith("block_")][:n_layers]
+    segs = [s for s in state.segments if s.layer in blocks]
     a, b = segs[0].offset, segs[-1].offset + segs[-1].numel
     t0 = time.perf_counter()
     hW = to_numpy_weight(state.weight[a:b])
@@ -122,11 +125,11 @@ def cpu_baseline(state, spec, mode_name):
     osegs = []
     for s in segs:
         x, y = s.offset - a, s.offset - a + s.numel
-        osegs.append(O.OSegment(0, hW[x:y], hS[x:y].copy(), None if hM is None else hM[x:y],
-                                hm[x:y], hv[x:y]))
+        osegs.append(O.OSegment(blocks.index(s.layer), hW[x:y], hS[x:y].copy(),
+                                None if hM is None else hM[x:y], hm[x:y], hv[x:y]))
     dt = O.DT_BF16 if spec.weight_dtype == "bf16" else O.DT_F32
     mode = O.MODE_ACCUM if mode_name == "accum" else O.MODE_SNAPSHOT
-    orc = O.LayerCheckOracle(osegs, 1, dt, spec.has_master, mode, [0.0], spec.s_max)
+    orc = O.LayerCheckOracle(osegs, len(blocks), dt, spec.has_master, mode, [0.0] * len(blocks), spec.s_max)
     # the oracle's init set S <- W; restore the device shadow so the score sees real drift
     for s, seg in zip(osegs, segs):
         x = seg.offset - a
@@ -145,7 +148,7 @@ def cpu_baseline(state, spec, mode_name):
     pack_bytes = rec_unpadded + len(payload) + (w * n if mode == O.MODE_SNAPSHOT else 0)
     gbs = (score_bytes + pack_bytes) / elapsed / 1e9
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"one transformer block ({spec.layers[li].name}, {n} params) of the same state: "
+            "sample": f"{len(blocks)} transformer blocks ({n} params) of the same state: "
                       f"score + select + pack in {elapsed:.2f} s, host copy {copy_s:.2f} s excluded; "
                       f"numpy fp64, single thread"}
 
@@ -180,21 +183,24 @@ def main():
     embed = np.array([l.name == "embed_tokens" for l in spec.layers])
 
     # -- calibration: record the per-step scores over one staleness period ----
-    probe = LC.LayoutDesc(segs, spec.n_layers, dtype, spec.has_master, LC.LC_MODE_ACCUM,
-                          [float("inf")] * spec.n_layers, s_max, stream=stream.cuda_stream)
-    ctx = LC.lc_init_layout(probe)
-    u_hist = []
     t = 0
-    for _ in range(s_max):
-        t += 1
-        state.step(t)
-        LC.lc_score_layers(ctx, t)
-        LC.lc_select(ctx, t, 1.0)
-        u_hist.append(LC.lc_read_state(ctx, spec.n_layers)[0])
-    LC.lc_destroy(ctx)
-    k0_base = calibrate_k0(np.array(u_hist), embed, s_max, spec.target_fraction)
+    if args.k0 is None:
+        probe = LC.LayoutDesc(segs, spec.n_layers, dtype, spec.has_master, LC.LC_MODE_ACCUM,
+                              [float("inf")] * spec.n_layers, s_max, stream=stream.cuda_stream)
+        ctx = LC.lc_init_layout(probe)
+        u_hist = []
+        for _ in range(s_max):
+            t += 1
+            state.step(t)
+            LC.lc_score_layers(ctx, t)
+            LC.lc_select(ctx, t, 1.0)
+            u_hist.append(LC.lc_read_state(ctx, spec.n_layers)[0])
+        LC.lc_destroy(ctx)
+        k0_base = calibrate_k0(np.array(u_hist), embed, s_max, spec.target_fraction)
+        log(f"[bench] calibrated K0 = {k0_base:.4g} (embeddings x10) for ~{spec.target_fraction:.0%} of layers")
+    else:
+        k0_base = args.k0
     k0 = [k0_base * (10.0 if e else 1.0) for e in embed]
-    log(f"[bench] calibrated K0 = {k0_base:.4g} (embeddings x10) for ~{spec.target_fraction:.0%} of layers")
 
     layout = LC.LayoutDesc(segs, spec.n_layers, dtype, spec.has_master, mode, k0, s_max,
                            t_base=t, stream=stream.cuda_stream)
@@ -207,7 +213,7 @@ def main():
     ctx = LC.lc_init_layout(layout)
     LC.lc_pack_selected(ctx, staging.data_ptr(), cap, 0)  # part of the base version (untimed)
 
-    n_chunks = sum(math.ceil(s.numel * spec.weight_bytes / 65536) for s in state.segments)
+    n_chunks = sum(math.ceil(s.numel * spec.weight_bytes / CHUNK_BYTES) for s in state.segments)
     w = spec.weight_bytes
     P = spec.numel
     score_bytes = (3 if mode == LC.LC_MODE_ACCUM else 2) * w * P + 32 * n_chunks

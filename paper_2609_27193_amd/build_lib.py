@@ -28,9 +28,12 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose: bool = False) -> str:
-    tmp = LIB + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, "-o", tmp, *[os.path.join(CSRC, s) for s in SOURCES]]
+def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+    """Compile the library to ``out``; ``defines`` are extra -D macros
+    (tile sizes LC_CHUNK_BYTES / LC_PIECE_BYTES for tuning builds)."""
+    tmp = out + ".tmp"
+    cmd = [hipcc(), *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-o", tmp,
+           *[os.path.join(CSRC, s) for s in SOURCES]]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -40,8 +43,8 @@ def build(verbose: bool = False) -> str:
     errs = [l for l in res.stderr.splitlines() if "packed-fp32-ops" not in l and l.strip()]
     if verbose and errs:
         sys.stderr.write("\n".join(errs) + "\n")
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":

@@ -12,12 +12,20 @@ namespace lc {
 // kChunkBytes of weights (and the same of shadow).  Chunks never cross a
 // segment, so every layer owns a contiguous range of chunks and one fp64
 // (sum|W-S|, sum|S|) pair per chunk is reduced in a fixed order per layer.
+#ifndef LC_CHUNK_BYTES
+#define LC_CHUNK_BYTES (16u * 1024u)
+#endif
+#ifndef LC_PIECE_BYTES
+#define LC_PIECE_BYTES (16u * 1024u)
+#endif
 constexpr uint32_t kScoreThreads = 256;
-constexpr uint32_t kChunkBytes = 64u * 1024u;
+constexpr uint32_t kChunkBytes = LC_CHUNK_BYTES;
 // Pack/restore: a piece is kPieceBytes of one copy unit (one array of one
 // segment); records are laid out so that every unit starts 256-B aligned.
 constexpr uint32_t kCopyThreads = 256;
-constexpr uint32_t kPieceBytes = 64u * 1024u;
+constexpr uint32_t kPieceBytes = LC_PIECE_BYTES;
+static_assert(kChunkBytes % (16u * kScoreThreads * 4u) == 0, "score tiling: 4 vectors per thread per round");
+static_assert(kPieceBytes % (16u * kCopyThreads) == 0, "pack tiling");
 constexpr uint32_t kRecordAlign = 256u;
 constexpr uint32_t kFinalizeThreads = 256;
 constexpr uint32_t kSelectThreads = 256;
