@@ -139,6 +139,27 @@ def decide(delta, t_last, k0, lr_scale: float, s_max: int, step: int):
     return mask, forced
 
 
+def plan_versions(versions: Sequence[dict], n_layers: int, t_fail: int) -> List[int]:
+    """Section 3.5 step 1: for each layer, the index of the version with the
+    greatest step <= t_fail whose mask holds the layer (the base full
+    checkpoint is one such version).  Only ``step`` and ``mask`` are read."""
+    choice = []
+    for l in range(n_layers):
+        best, best_step, dup = None, None, False
+        for i, v in enumerate(versions):
+            if v["step"] <= t_fail and v["mask"][l]:
+                if best is None or v["step"] > best_step:
+                    best, best_step, dup = i, v["step"], False
+                elif v["step"] == best_step:
+                    dup = True
+        if best is None:
+            raise OracleError(LC_ERR_NO_VERSION, f"layer {l}: no persisted version <= {t_fail}")
+        if dup:
+            raise OracleError(LC_ERR_INVALID_ARG, f"layer {l}: two versions at step {best_step}")
+        choice.append(best)
+    return choice
+
+
 class LayerCheckOracle:
     """Stateful mirror of the decision step on host arrays."""
 
@@ -305,21 +326,7 @@ class LayerCheckOracle:
             need = sum(self.R[l] for l in range(self.N) if m[l])
             if len(v["payload"]) != need:
                 raise OracleError(LC_ERR_INVALID_ARG, "payload size does not match mask")
-        choice = []
-        for l in range(self.N):
-            best, best_step, dup = None, None, False
-            for i, v in enumerate(versions):
-                if v["step"] <= t_fail and v["mask"][l]:
-                    if best is None or v["step"] > best_step:
-                        best, best_step, dup = i, v["step"], False
-                    elif v["step"] == best_step:
-                        dup = True
-            if best is None:
-                raise OracleError(LC_ERR_NO_VERSION, f"layer {l}: no persisted version <= {t_fail}")
-            if dup:
-                raise OracleError(LC_ERR_INVALID_ARG, f"layer {l}: two versions at step {best_step}")
-            choice.append(best)
-        return choice
+        return plan_versions(versions, self.N, t_fail)
 
     def restore(self, versions: Sequence[dict], t_fail: int) -> np.ndarray:
         choice = self.plan(versions, t_fail)

@@ -27,7 +27,7 @@ constexpr uint32_t kPieceBytes = LC_PIECE_BYTES;
 static_assert(kChunkBytes % (16u * kScoreThreads * 4u) == 0, "score tiling: 4 vectors per thread per round");
 static_assert(kPieceBytes % (16u * kCopyThreads) == 0, "pack tiling");
 constexpr uint32_t kRecordAlign = 256u;
-constexpr uint32_t kFinalizeThreads = 256;
+constexpr uint32_t kFinalizeThreads = 1024;
 constexpr uint32_t kSelectThreads = 256;
 
 // One segment as the score kernel sees it.

@@ -190,19 +190,40 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const DeviceTables
 }
 
 // ---- finalize: Eq. 1 and Eq. 2 per layer, one block per layer -----------------
+// Thread j sums partials j, j + NT, j + 2 NT, ... of its layer into four
+// interleaved accumulators (independent loads in flight), combined in a fixed
+// order, then a fixed-order block reduction: deterministic for a given layout.
 __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(const DeviceTables t) {
   const uint32_t l = blockIdx.x;
   const uint32_t c0 = t.layer_chunk_begin[l], c1 = t.layer_chunk_begin[l + 1];
-  double a = 0.0, b = 0.0;
-  for (uint32_t c = c0 + threadIdx.x; c < c1; c += kFinalizeThreads) {
-    const double2 p = t.partials[c];
-    a += p.x;
-    b += p.y;
+  double a[4] = {0.0, 0.0, 0.0, 0.0}, b[4] = {0.0, 0.0, 0.0, 0.0};
+  uint32_t c = c0 + threadIdx.x;
+  for (; c + 3 * kFinalizeThreads < c1; c += 4 * kFinalizeThreads) {
+    double2 p[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) p[k] = t.partials[c + k * kFinalizeThreads];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      a[k] += p[k].x;
+      b[k] += p[k].y;
+    }
   }
-  block_sum2<kFinalizeThreads>(a, b);
+  // at most three partials remain for this thread
+#pragma unroll
+  for (int k = 0; k < 3; ++k) {
+    if (c < c1) {
+      const double2 p = t.partials[c];
+      a[k] += p.x;
+      b[k] += p.y;
+      c += kFinalizeThreads;
+    }
+  }
+  double x = (a[0] + a[1]) + (a[2] + a[3]);
+  double y = (b[0] + b[1]) + (b[2] + b[3]);
+  block_sum2<kFinalizeThreads>(x, y);
   if (threadIdx.x == 0) {
     const double n = static_cast<double>(t.numel[l]);
-    const double u = (a / n) / (b / n + t.eps_w);
+    const double u = (x / n) / (y / n + t.eps_w);
     t.u[l] = u;
     t.delta[l] = (t.mode == 0) ? t.delta[l] + u : u;
   }

@@ -1,0 +1,135 @@
+"""GPU edge cases: odd tensor sizes (every later segment lands on a
+misaligned address, so the element-wise paths of the score and copy kernels
+run), tiny layouts, degenerate thresholds and a single segment larger than
+4 GiB (64-bit offsets), checked against the oracle or against closed forms."""
+import numpy as np
+import pytest
+
+from oracle import layercheck_oracle as O
+from paper_2609_27193_amd import inputs as I
+from paper_2609_27193_amd import layercheck as LC
+from tests.conftest import gpu_available
+from tests.gpu_harness import Pair, log
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not gpu_available():
+        pytest.skip("needs an MI355X")
+    LC.load_library()
+
+
+def odd_spec(weight_dtype, has_master, s_max=3):
+    T = I.TensorSpec
+    layers = (
+        I.LayerSpec("embed_tokens", (T("e", 4097, "embed"),)),
+        I.LayerSpec("block_0", tuple(T(f"t{i}", n, "matrix") for i, n in enumerate((1, 3, 7, 8, 1023, 8193)))),
+        I.LayerSpec("block_1", (T("a", 8191, "matrix"), T("b", 8192, "matrix"), T("n", 5, "norm"))),
+        I.LayerSpec("norm", (T("n", 1, "norm"),)),
+        I.LayerSpec("lm_head", (T("h", 3 * 8192 + 3, "embed"),)),
+    )
+    return I.ModelSpec(name=f"odd-{weight_dtype}-{int(has_master)}", layers=layers, weight_dtype=weight_dtype,
+                       has_master=has_master, scale_rule="loguniform_0.01_1", target_fraction=0.3, s_max=s_max)
+
+
+@pytest.mark.parametrize("dtype,master,mode", [("bf16", True, LC.LC_MODE_ACCUM), ("bf16", False, LC.LC_MODE_SNAPSHOT),
+                                               ("f32", False, LC.LC_MODE_ACCUM), ("f32", True, LC.LC_MODE_SNAPSHOT)])
+def test_odd_sizes_misaligned(dtype, master, mode):
+    spec = odd_spec(dtype, master)
+    p = Pair(spec, mode, [0.05] * spec.n_layers)
+    try:
+        aligned = [seg.weight % 16 == 0 for seg in p.lsegs]
+        assert not all(aligned), "layout should contain misaligned segments"
+        p.pack(0, np.ones(p.N, np.uint8), capacity=max(p.R))
+        for t in range(1, 8):
+            p.step(t, capacity=max(p.R) if t % 2 else None)
+        p.check_arrays()
+    finally:
+        p.close()
+
+
+def test_single_layer_smax_one():
+    T = I.TensorSpec
+    spec = I.ModelSpec(name="one", layers=(I.LayerSpec("block_0", (T("w", 777, "matrix"),)),), weight_dtype="bf16",
+                       has_master=True, scale_rule="constant_1", target_fraction=1.0, s_max=1)
+    p = Pair(spec, LC.LC_MODE_ACCUM, [1e300])
+    try:
+        p.pack(0, np.ones(1, np.uint8))
+        for t in range(1, 5):
+            mask, st = p.step(t)
+            assert mask.tolist() == [1] and st["n_forced"] == 1 and st["max_age"] == 0
+    finally:
+        p.close()
+
+
+def test_threshold_zero_selects_everything_and_no_change_scores_zero():
+    spec = odd_spec("bf16", True, s_max=1000)
+    p = Pair(spec, LC.LC_MODE_ACCUM, [0.0] * spec.n_layers)
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        d, tl = p.score(1)  # no update since init: every score exactly zero
+        assert not any(d)
+        mask, st = p.select(1, 1.0, d, tl)
+        assert mask.all() and st["n_forced"] == 0  # Delta = 0 >= K = 0
+        p.pack(1, mask)
+    finally:
+        p.close()
+
+
+def test_segment_larger_than_4gib_closed_form():
+    """One layer, one segment of 2^31 + 4099 bf16 elements (its fp32 arrays
+    are 8.6 GB each).  S = 0.5 and W = 0.5 + 2^-8 everywhere give
+    u = 2^-7 exactly (Eq. 1 with eps_w = 0: every partial sum is exact); the
+    record must hold the arrays' bytes at the offsets of the format, and a
+    restore from it must reproduce them."""
+    import torch
+    n = (1 << 31) + 4099
+    dev = torch.device("cuda")
+    log(f"large segment: {n} elements")
+    W = torch.full((n,), 0.5, dtype=torch.bfloat16, device=dev)
+    S = torch.empty_like(W)
+    idx = torch.arange(n, dtype=torch.int64, device=dev)  # distinct bit patterns per element
+    M = (idx & 0x7FFFFFFF).to(torch.int32).view(torch.float32)
+    m = ((n - idx) & 0x7FFFFFFF).to(torch.int32).view(torch.float32)
+    v = ((idx * 2654435761) & 0x7FFFFFFF).to(torch.int32).view(torch.float32)
+    del idx
+    seg = LC.Segment(0, n, W.data_ptr(), S.data_ptr(), M.data_ptr(), m.data_ptr(), v.data_ptr())
+    lay = LC.LayoutDesc([seg], 1, LC.LC_DT_BF16, True, LC.LC_MODE_ACCUM, [2.0 ** -7], s_max=100, eps_w=0.0,
+                        stream=torch.cuda.current_stream().cuda_stream)
+    ctx = LC.lc_init_layout(lay)
+    try:
+        R = LC.lc_record_bytes(ctx, 0)
+        assert R == O.record_bytes([n], 2, True)
+        W.fill_(0.5 + 2.0 ** -8)
+        LC.lc_score_layers(ctx, 1)
+        u, d, _ = LC.lc_read_state(ctx, 1)
+        assert u[0] == 2.0 ** -7 and d[0] == 2.0 ** -7
+        assert torch.equal(S, W)  # ACCUM refreshed the shadow in the same pass
+        mask, st = LC.lc_select(ctx, 1, 1.0, 1)
+        assert mask.tolist() == [1] and st["n_forced"] == 0 and st["payload_bytes"] == R  # Delta == K persists
+        staging = torch.empty(R, dtype=torch.uint8, device=dev)
+        res = LC.lc_pack_selected(ctx, staging.data_ptr(), R, 0)
+        assert res == {"bytes_written": R, "n_packed": 1, "next_rank": 1, "done": 1}
+        torch.cuda.synchronize()
+        offs = [0]
+        for nb in (2 * n, 4 * n, 4 * n, 4 * n):
+            offs.append(offs[-1] + O.padded(nb))
+        assert offs[-1] == R
+        blocks = [(W, 2 * n), (M, 4 * n), (m, 4 * n), (v, 4 * n)]
+        for (arr, nb), off in zip(blocks, offs):
+            assert torch.equal(staging[off:off + nb], arr.view(torch.uint8)), off
+            assert not staging[off + nb:O.padded(nb) + off].any()
+        # fail-stop, then restore from the device-resident record
+        saved = [a.clone() for a in (W, M, m, v)]
+        for a in (W, S, M, m, v):
+            a.zero_()
+        chosen = LC.lc_restore_composite(ctx, [{"step": 1, "mask": np.ones(1, np.uint8),
+                                                "payload": staging.data_ptr(), "payload_bytes": R}], 1, 1)
+        assert chosen.tolist() == [1]
+        for a, b in zip((W, M, m, v), saved):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+        assert torch.equal(S, W)
+    finally:
+        LC.lc_destroy(ctx)

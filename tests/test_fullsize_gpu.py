@@ -1,0 +1,300 @@
+"""Full-size parity in the launch configuration the benchmark times.
+
+The whole workload state lives on the GPU (8.0 - 14.8 B parameters).  The
+oracle cannot process it every step, so it checks sampled outputs one by one,
+and properties that hold at any size cover the rest:
+
+* u of sampled layers (a rotating transformer block, the final norm, and the
+  embedding / lm_head on the first step and on the staleness burst) against
+  the oracle's Eq. 1 on host copies, within 1e-5;
+* for every layer, the accumulator arithmetic of Eq. 2 (Delta(t) equals
+  Delta(t-1) + u(t) bit for bit), and in ACCUM mode S == W after the pass;
+* the oracle's decision rule fed the GPU accumulators reproduces the mask
+  and the forced count exactly; stats against their definitions;
+* the records of sampled selected layers against the oracle's records,
+  through capacity-limited multi-call packs where the state leaves no room
+  for worst-case staging;
+* Qwen2.5-14B: composite recovery from six versions at steps 0..5 (base in
+  pageable host memory, partial versions on the device) with t_fail = 4, the
+  plan against the oracle's, sampled layers against their persisted truth,
+  and a restore -> re-pack round trip of every layer.
+"""
+import numpy as np
+import pytest
+
+from oracle import layercheck_oracle as O
+from paper_2609_27193_amd import inputs as I
+from paper_2609_27193_amd import layercheck as LC
+from paper_2609_27193_amd.inputs import to_numpy_weight
+from tests.conftest import gpu_available
+from tests.gpu_harness import REL, log
+
+pytestmark = pytest.mark.gpu
+GiB = 1 << 30
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not gpu_available():
+        pytest.skip("needs an MI355X")
+    LC.load_library()
+
+
+@pytest.fixture(autouse=True)
+def _release():
+    yield
+    import gc
+    import torch
+    gc.collect()
+    torch.cuda.empty_cache()
+
+
+class FullRun:
+    def __init__(self, spec, mode, k0, staging_cap=None, reserve=24 * GiB):
+        import torch
+        self.torch = torch
+        self.spec = spec
+        self.mode = mode
+        self.N = spec.n_layers
+        self.k0 = list(k0)
+        self.dtype = LC.LC_DT_BF16 if spec.weight_dtype == "bf16" else LC.LC_DT_F32
+        self.odt = O.DT_BF16 if spec.weight_dtype == "bf16" else O.DT_F32
+        self.state = I.SyntheticState(spec, device="cuda")
+        self.segs = LC.segments_from_state(self.state)
+        self.stream = torch.cuda.current_stream().cuda_stream
+        self.layout = LC.LayoutDesc(self.segs, self.N, self.dtype, spec.has_master, mode, self.k0, spec.s_max,
+                                    stream=self.stream)
+        self.numel, self.R = LC.lc_query_layout(self.layout)
+        w = spec.weight_bytes
+        assert self.R == [O.record_bytes([t.numel for t in l.tensors], w, spec.has_master) for l in spec.layers]
+        self.ctx = LC.lc_init_layout(self.layout)
+        free = torch.cuda.mem_get_info()[0]
+        cap = min(sum(self.R), free - reserve) if staging_cap is None else staging_cap
+        self.cap = cap // 256 * 256
+        self.staging = torch.empty(self.cap, dtype=torch.uint8, device="cuda")
+        self.delta_post = [0.0] * self.N
+        log(f"{spec.name}: {spec.numel} params, state {self.state.nbytes() / 1e9:.1f} GB, "
+            f"staging {self.cap / 1e9:.1f} GB of {sum(self.R) / 1e9:.1f} GB worst case")
+
+    def close(self):
+        if self.ctx is not None:
+            LC.lc_destroy(self.ctx)
+            self.ctx = None
+
+    def layer_segments(self, l):
+        return [s for s in self.state.segments if s.layer == l]
+
+    def host_layer(self, l, arrays=("weight", "shadow")):
+        out = []
+        for s in self.layer_segments(l):
+            sl = slice(s.offset, s.offset + s.numel)
+            d = {}
+            for a in arrays:
+                t = getattr(self.state, a)
+                if t is None:
+                    d[a] = None
+                elif a in ("weight", "shadow"):
+                    d[a] = to_numpy_weight(t[sl])
+                else:
+                    d[a] = t[sl].cpu().numpy()
+            out.append(d)
+        return out
+
+    def oracle_record(self, l):
+        h = self.host_layer(l, ("weight", "master", "exp_avg", "exp_avg_sq"))
+        segs = [O.OSegment(0, d["weight"], d["weight"].copy(), d["master"], d["exp_avg"], d["exp_avg_sq"])
+                for d in h]
+        orc = O.LayerCheckOracle(segs, 1, self.odt, self.spec.has_master, O.MODE_ACCUM, [0.0], 1)
+        return np.frombuffer(orc.layer_record(0), dtype=np.uint8)
+
+    def step(self, t, sampled, lr=1.0):
+        torch = self.torch
+        self.state.step(t)
+        torch.cuda.synchronize()
+        host = {l: self.host_layer(l) for l in sampled}
+        _, d_prev, tl_prev = LC.lc_read_state(self.ctx, self.N)
+        LC.lc_score_layers(self.ctx, t)
+        u, d, tl = LC.lc_read_state(self.ctx, self.N)
+        for l in sampled:
+            uo = O.layer_update_score([x["weight"] for x in host[l]], [x["shadow"] for x in host[l]],
+                                      self.odt, 1e-8)[3]
+            assert (u[l] == 0) == (uo == 0) and abs(u[l] - uo) <= REL * abs(uo), (t, l, u[l], uo)
+        for l in range(self.N):  # Eq. 2 arithmetic on every layer
+            expect = d_prev[l] + u[l] if self.mode == LC.LC_MODE_ACCUM else u[l]
+            assert d[l] == expect, (t, l)
+        if self.mode == LC.LC_MODE_ACCUM:
+            assert torch.equal(self.state.shadow, self.state.weight)
+        mask, st = LC.lc_select(self.ctx, t, lr, self.N)
+        m_fed, f_fed = O.decide(list(d), list(tl), self.k0, lr, self.spec.s_max, t)
+        assert np.array_equal(m_fed, mask) and int(f_fed.sum()) == st["n_forced"]
+        _, d_post, tl_post = LC.lc_read_state(self.ctx, self.N)
+        ages = [t - x for x in tl_post]
+        assert st["max_age"] == max(ages) <= self.spec.s_max - 1
+        assert st["weighted_age"] == float(sum(n * a for n, a in zip(self.numel, ages))) / float(sum(self.numel))
+        assert st["payload_bytes"] == sum(self.R[l] for l in range(self.N) if mask[l])
+        assert all(d_post[l] == (0.0 if mask[l] else d[l]) for l in range(self.N))
+        self.pack_and_check(mask, [l for l in sampled if mask[l]])
+        log(f"  t={t}: selected {st['n_selected']}/{self.N} (forced {st['n_forced']}), "
+            f"payload {st['payload_bytes'] / 1e9:.2f} GB, sampled {sampled}")
+        return mask, st
+
+    def pack_and_check(self, mask, check_layers, dest=None):
+        """Ranged packs into staging (or into ``dest``); records of
+        ``check_layers`` compared with the oracle's."""
+        torch = self.torch
+        sel = [l for l in range(self.N) if mask[l]]
+        rank, calls = 0, 0
+        while True:
+            if dest is None:
+                buf, cap = self.staging, self.cap
+            else:
+                buf, cap = dest, dest.numel()
+            res = LC.lc_pack_selected(self.ctx, buf.data_ptr(), cap, rank)
+            calls += 1
+            torch.cuda.synchronize()
+            off = 0
+            for r in range(rank, res["next_rank"]):
+                l = sel[r]
+                if l in check_layers:
+                    got = buf[off:off + self.R[l]].cpu().numpy()
+                    assert np.array_equal(got, self.oracle_record(l)), f"record of layer {l}"
+                off += self.R[l]
+            assert off == res["bytes_written"]
+            if res["done"]:
+                return calls
+            rank = res["next_rank"]
+
+
+def sample_for(t, N, s_max):
+    blocks = list(range(1, N - 2))
+    pick = [blocks[(7 * t) % len(blocks)], N - 2]  # one block and the final norm
+    if t == 1 or t % s_max == 0:
+        pick += [0, N - 1]  # embed_tokens and lm_head
+    return sorted(set(pick))
+
+
+WORKLOADS = [
+    ("llama3-8b", LC.LC_MODE_ACCUM, 0.0391),
+    ("llama2-13b", LC.LC_MODE_ACCUM, 0.03),
+    ("llama3-70b-shard0", LC.LC_MODE_SNAPSHOT, 0.03),
+]
+
+
+@pytest.mark.timeout(900)
+@pytest.mark.parametrize("name,mode,k0", WORKLOADS, ids=[w[0] for w in WORKLOADS])
+def test_fullsize_decision_steps(name, mode, k0):
+    spec = I.WORKLOADS[name]()
+    k0s = [k0 * (10.0 if l.name == "embed_tokens" else 1.0) for l in spec.layers]
+    run = FullRun(spec, mode, k0s)
+    try:
+        # base version: every layer; check the small and the largest records
+        base = np.ones(run.N, np.uint8)
+        calls = run.pack_and_check(base, [run.N - 2, run.N - 1])
+        log(f"  base packed in {calls} call(s)")
+        for t in range(1, spec.s_max + 1):
+            run.step(t, sample_for(t, run.N, spec.s_max))
+    finally:
+        run.close()
+
+
+@pytest.mark.timeout(900)
+def test_fullsize_qwen14b_composite_restore_six_versions():
+    """Qwen2.5-14B-shaped state (bf16 W, fp32 m/v, no master, S_max = 6).
+    Per-layer thresholds make layers cross at different steps so the
+    composite mixes several timestamps."""
+    import torch
+    spec = I.qwen25_14b_spec()
+    N = spec.n_layers
+    # measure one step of scores to place the thresholds, then regenerate step 0
+    probe = FullRun(spec, LC.LC_MODE_ACCUM, [float("inf")] * N, staging_cap=1 << 30)
+    probe.state.step(1)
+    LC.lc_score_layers(probe.ctx, 1)
+    u1 = LC.lc_read_state(probe.ctx, N)[0]
+    probe.close()
+    del probe
+    torch.cuda.empty_cache()
+    fast = [l for l in range(N) if u1[l] > 0.5 * max(u1)]
+    k0 = [1e9] * N  # slow layers only by the guard (at t = 6, after t_fail)
+    for i, l in enumerate(fast):
+        k0[l] = u1[l] * (2 + i % 4) * 0.97  # crosses after about 2..5 steps
+    run = FullRun(spec, LC.LC_MODE_ACCUM, k0, staging_cap=1 << 30)
+    try:
+        total = sum(run.R)
+        # 148 GB cannot be page-locked on this host; the base lives in pageable
+        # memory, which the library restores through staged host copies
+        log(f"  base version {total / 1e9:.1f} GB -> pageable host memory")
+        base_host = torch.empty(total, dtype=torch.uint8)
+        chunk = torch.empty(48 * GiB // 256 * 256, dtype=torch.uint8, device="cuda")
+        rank, off = 0, 0
+        while True:  # the base, packed in capacity-limited calls and drained to the host
+            res = LC.lc_pack_selected(run.ctx, chunk.data_ptr(), chunk.numel(), rank)
+            base_host[off:off + res["bytes_written"]].copy_(chunk[:res["bytes_written"]])
+            off += res["bytes_written"]
+            if res["done"]:
+                break
+            rank = res["next_rank"]
+        del chunk
+        torch.cuda.empty_cache()
+        versions = [{"step": 0, "mask": np.ones(N, np.uint8), "buf": base_host}]
+        sampled = sorted(set([0, N - 1, N - 2] + fast[:3] + [l for l in range(1, N - 2) if l not in fast][:2]))
+        truth = {(l, 0): run.host_layer(l, ("weight", "exp_avg", "exp_avg_sq")) for l in sampled}
+        for t in range(1, 6):
+            run.state.step(t)
+            LC.lc_score_layers(run.ctx, t)
+            mask, st = LC.lc_select(run.ctx, t, 1.0, N)
+            dev = torch.empty(max(st["payload_bytes"], 256), dtype=torch.uint8, device="cuda")
+            if st["payload_bytes"]:
+                res = LC.lc_pack_selected(run.ctx, dev.data_ptr(), st["payload_bytes"], 0)
+                assert res["done"] == 1
+            versions.append({"step": t, "mask": mask, "buf": dev[:st["payload_bytes"]]})
+            for l in sampled:
+                if mask[l]:
+                    truth[(l, t)] = run.host_layer(l, ("weight", "exp_avg", "exp_avg_sq"))
+            log(f"  t={t}: {st['n_selected']} layers, {st['payload_bytes'] / 1e9:.2f} GB on the device")
+        t_fail = 4
+        expect_idx = O.plan_versions([{"step": v["step"], "mask": v["mask"]} for v in versions], N, t_fail)
+        expect = [versions[i]["step"] for i in expect_idx]
+        stamps = sorted(set(expect))
+        log(f"  composite timestamps for t_fail={t_fail}: {stamps}")
+        assert len(stamps) >= 3
+        # fail-stop: live state lost
+        for a in (run.state.weight, run.state.shadow, run.state.exp_avg, run.state.exp_avg_sq):
+            a.zero_()
+        torch.cuda.synchronize()
+        cv = [{"step": v["step"], "mask": v["mask"], "payload": v["buf"].data_ptr() if v["buf"].numel() else 0,
+               "payload_bytes": v["buf"].numel()} for v in versions]
+        chosen = LC.lc_restore_composite(run.ctx, cv, t_fail, N)
+        assert chosen.tolist() == expect
+        _, d, tl = LC.lc_read_state(run.ctx, N)
+        assert tl.tolist() == expect and not d.any()
+        assert torch.equal(run.state.shadow, run.state.weight)
+        for l in sampled:
+            now = run.host_layer(l, ("weight", "exp_avg", "exp_avg_sq"))
+            for a, b in zip(now, truth[(l, expect[l])]):
+                for k in ("weight", "exp_avg", "exp_avg_sq"):
+                    assert np.array_equal(a[k].view(np.uint8), b[k].view(np.uint8)), (l, k)
+        # restore -> re-pack round trip of every layer against the chosen records
+        ctx2 = LC.lc_init_layout(run.layout)
+        try:
+            buf = torch.empty(max(run.R) + 4096, dtype=torch.uint8, device="cuda")
+            rank, l = 0, 0
+            while True:
+                res = LC.lc_pack_selected(ctx2, buf.data_ptr(), buf.numel(), rank)
+                off = 0
+                for _ in range(res["n_packed"]):
+                    v = versions[expect_idx[l]]
+                    voff = sum(run.R[j] for j in range(l) if v["mask"][j])
+                    ref = v["buf"][voff:voff + run.R[l]]
+                    if ref.device.type != "cuda":
+                        ref = ref.to("cuda", non_blocking=False)
+                    assert torch.equal(buf[off:off + run.R[l]], ref), f"layer {l}"
+                    off += run.R[l]
+                    l += 1
+                if res["done"]:
+                    break
+                rank = res["next_rank"]
+            assert l == N
+        finally:
+            LC.lc_destroy(ctx2)
+    finally:
+        run.close()
