@@ -31,7 +31,7 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-CHUNK_BYTES = int(os.environ.get("LC_CHUNK_BYTES", 16 * 1024))  # score chunk (bytes of W per partial)
+CHUNK_BYTES = int(os.environ.get("LC_CHUNK_BYTES", 8 * 1024))  # score chunk (bytes of W per partial)
 METRIC = "GB/s of model state scored+packed per decision step (% of HBM peak); ms/step"
 
 

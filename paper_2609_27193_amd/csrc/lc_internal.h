@@ -13,10 +13,16 @@ namespace lc {
 // segment, so every layer owns a contiguous range of chunks and one fp64
 // (sum|W-S|, sum|S|) pair per chunk is reduced in a fixed order per layer.
 #ifndef LC_CHUNK_BYTES
-#define LC_CHUNK_BYTES (16u * 1024u)
+#define LC_CHUNK_BYTES (8u * 1024u)
+#endif
+#ifndef LC_XCD_REMAP
+#define LC_XCD_REMAP 1
+#endif
+#ifndef LC_MAX_GRID_BLOCKS
+#define LC_MAX_GRID_BLOCKS 0  // 0: only the dispatch limit caps a grid (testing builds set it low)
 #endif
 #ifndef LC_PIECE_BYTES
-#define LC_PIECE_BYTES (16u * 1024u)
+#define LC_PIECE_BYTES (8u * 1024u)
 #endif
 constexpr uint32_t kScoreThreads = 256;
 constexpr uint32_t kChunkBytes = LC_CHUNK_BYTES;
@@ -24,7 +30,7 @@ constexpr uint32_t kChunkBytes = LC_CHUNK_BYTES;
 // segment); records are laid out so that every unit starts 256-B aligned.
 constexpr uint32_t kCopyThreads = 256;
 constexpr uint32_t kPieceBytes = LC_PIECE_BYTES;
-static_assert(kChunkBytes % (16u * kScoreThreads * 4u) == 0, "score tiling: 4 vectors per thread per round");
+static_assert(kChunkBytes % (16u * kScoreThreads) == 0, "score tiling: whole vectors per thread");
 static_assert(kPieceBytes % (16u * kCopyThreads) == 0, "pack tiling");
 constexpr uint32_t kRecordAlign = 256u;
 constexpr uint32_t kFinalizeThreads = 1024;

@@ -70,6 +70,23 @@ __device__ __forceinline__ void elem_copy(const uint8_t* src, uint8_t* dst, uint
   }
 }
 
+__device__ __forceinline__ uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
+// Work item x of a launch of G blocks.  Workgroups are dispatched round-robin
+// over the 8 XCDs; with LC_XCD_REMAP each XCD instead walks one contiguous
+// eighth of the items (a bijection on the first 8*floor(G/8) items, identity
+// on the rest), which keeps each XCD's in-flight accesses within a narrow
+// address window.
+__device__ __forceinline__ uint32_t remap_xcd(uint32_t x, uint32_t G) {
+#if LC_XCD_REMAP
+  const uint32_t full = G - G % 8u;
+  return x < full ? (x % 8u) * (full / 8u) + x / 8u : x;
+#else
+  (void)G;
+  return x;
+#endif
+}
+
 // ---- wave64 / block reductions of an fp64 pair, fixed order ------------------
 __device__ __forceinline__ double dpp_f64(double v, int ctrl_sel) {
   int lo = __double2loint(v), hi = __double2hiint(v);
@@ -118,20 +135,18 @@ __device__ __forceinline__ void block_sum2(double& a, double& b) {
   }
 }
 
-// ---- score: one block per chunk ------------------------------------------------
+// ---- score: one chunk per block and iteration ---------------------------------
 // Streams W and S of one chunk once; writes (sum|W-S|, sum|S|) in fp64.  In
 // ACCUM mode the same pass stores W into S (the next step's W(t-1)).
 template <int DT, bool ACCUM>
-__global__ __launch_bounds__(kScoreThreads) void score_kernel(const DeviceTables t) {
+__device__ __forceinline__ void score_chunk(const DeviceTables& t, uint32_t c) {
   constexpr uint32_t ESZ = DT == 1 ? 2 : 4;
   constexpr uint32_t CE = kChunkBytes / ESZ;  // elements per chunk
   constexpr uint32_t EPV = 16 / ESZ;          // elements per 16-B vector
   constexpr uint32_t NV = CE / EPV;           // vectors per full chunk
   constexpr uint32_t VPT = NV / kScoreThreads;
-  constexpr uint32_t U = 4;                   // vectors per thread per round
+  constexpr uint32_t U = VPT < 4 ? VPT : 4;   // vectors per thread per round
   static_assert(VPT % U == 0, "tiling");
-
-  const uint32_t c = blockIdx.x;
   const uint32_t tid = threadIdx.x;
   const ScoreSeg sg = t.segs[t.chunk_seg[c]];
   const uint64_t e0 = static_cast<uint64_t>(c - sg.chunk_begin) * CE;
@@ -187,6 +202,24 @@ __global__ __launch_bounds__(kScoreThreads) void score_kernel(const DeviceTables
   }
   block_sum2<kScoreThreads>(a, b);
   if (tid == 0) t.partials[c] = make_double2(a, b);
+}
+
+// LOOP = false: one chunk per block (the common case; the chunk's tables are
+// read before any store, so they stay on the scalar path).  LOOP = true: the
+// grid is capped by the dispatch limit and blocks take several rounds.
+template <int DT, bool ACCUM, bool LOOP>
+__global__ __launch_bounds__(kScoreThreads) void score_kernel(const DeviceTables t) {
+  if constexpr (!LOOP) {
+    score_chunk<DT, ACCUM>(t, remap_xcd(blockIdx.x, gridDim.x));
+  } else {
+    for (uint64_t base = 0; base < t.n_chunks; base += gridDim.x) {
+      const uint64_t left = t.n_chunks - base;
+      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
+      if (blockIdx.x >= span) return;
+      score_chunk<DT, ACCUM>(t, static_cast<uint32_t>(base + remap_xcd(blockIdx.x, span)));
+      __syncthreads();  // the block reduction's LDS is reused by the next round
+    }
+  }
 }
 
 // ---- finalize: Eq. 1 and Eq. 2 per layer, one block per layer -----------------
@@ -329,15 +362,15 @@ __device__ __forceinline__ void copy_piece(const uint8_t* __restrict__ src, uint
   }
 }
 
-__device__ __forceinline__ uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
+
 
 // ---- pack: selected records into the staging buffer ---------------------------
-// One block per piece of the selected records of ranks [first, last).
+// Work item q is piece q (relative to piece_base) of the selected records of
+// ranks [first, last); records are written from staging offset
+// sel_rec_prefix[first] - rec_base.
 template <bool REFRESH>
-__global__ __launch_bounds__(kCopyThreads) void pack_kernel(const DeviceTables t, uint32_t first,
-                                                            uint32_t last, uint64_t piece_base,
-                                                            uint64_t rec_base, uint8_t* staging) {
-  const uint64_t q = piece_base + blockIdx.x;
+__device__ __forceinline__ void pack_piece(const DeviceTables& t, uint32_t first, uint32_t last, uint64_t q,
+                                           uint64_t rec_base, uint8_t* staging) {
   uint32_t lo = first, hi = last;  // sel_piece_prefix[lo] <= q < sel_piece_prefix[hi]
   while (hi - lo > 1) {
     const uint32_t mid = (lo + hi) >> 1;
@@ -360,11 +393,27 @@ __global__ __launch_bounds__(kCopyThreads) void pack_kernel(const DeviceTables t
   }
 }
 
+template <bool REFRESH, bool LOOP>
+__global__ __launch_bounds__(kCopyThreads) void pack_kernel(const DeviceTables t, uint32_t first,
+                                                            uint32_t last, uint64_t piece_base,
+                                                            uint64_t n_pieces, uint64_t rec_base,
+                                                            uint8_t* staging) {
+  if constexpr (!LOOP) {
+    pack_piece<REFRESH>(t, first, last, piece_base + remap_xcd(blockIdx.x, gridDim.x), rec_base, staging);
+  } else {
+    for (uint64_t base = 0; base < n_pieces; base += gridDim.x) {
+      const uint64_t left = n_pieces - base;
+      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
+      if (blockIdx.x >= span) return;
+      pack_piece<REFRESH>(t, first, last, piece_base + base + remap_xcd(blockIdx.x, span), rec_base, staging);
+    }
+  }
+}
+
 // ---- unpack: composite restore from device-resident records --------------------
 // rank r restores layer rank_layer[r] from the record at address rank_src[r];
 // every W block also refreshes the shadow.
-__global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables t, uint32_t n_ranks) {
-  const uint64_t q = blockIdx.x;
+__device__ __forceinline__ void unpack_piece(const DeviceTables& t, uint32_t n_ranks, uint64_t q) {
   uint32_t lo = 0, hi = n_ranks;
   while (hi - lo > 1) {
     const uint32_t mid = (lo + hi) >> 1;
@@ -383,16 +432,59 @@ __global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables
   copy_piece(src, dst, dst2, len, u.vec_ok != 0 && (rec & 15) == 0);
 }
 
+template <bool LOOP>
+__global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables t, uint32_t n_ranks,
+                                                              uint64_t n_pieces) {
+  if constexpr (!LOOP) {
+    unpack_piece(t, n_ranks, remap_xcd(blockIdx.x, gridDim.x));
+  } else {
+    for (uint64_t base = 0; base < n_pieces; base += gridDim.x) {
+      const uint64_t left = n_pieces - base;
+      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
+      if (blockIdx.x >= span) return;
+      unpack_piece(t, n_ranks, base + remap_xcd(blockIdx.x, span));
+    }
+  }
+}
+
+// Blocks per launch: one per work item up to the dispatch limit of 2^32
+// work-items per dimension; beyond it the kernels loop.
+__host__ inline uint32_t grid_for(uint64_t items, uint32_t threads) {
+  uint64_t cap = (0xFFFFFFFFull / threads) & ~7ull;
+  if (LC_MAX_GRID_BLOCKS > 0 && cap > LC_MAX_GRID_BLOCKS) cap = LC_MAX_GRID_BLOCKS;
+  return static_cast<uint32_t>(items < cap ? items : cap);
+}
+
+template <int DT, bool ACCUM>
+void launch_score_t(const DeviceTables& t, hipStream_t st) {
+  const uint32_t g = grid_for(t.n_chunks, kScoreThreads);
+  if (g == t.n_chunks)
+    hipLaunchKernelGGL((score_kernel<DT, ACCUM, false>), dim3(g), dim3(kScoreThreads), 0, st, t);
+  else
+    hipLaunchKernelGGL((score_kernel<DT, ACCUM, true>), dim3(g), dim3(kScoreThreads), 0, st, t);
+}
+
+template <bool REFRESH>
+void launch_pack_t(const DeviceTables& t, uint32_t first, uint32_t last, uint64_t piece_base, uint64_t n_pieces,
+                   uint64_t rec_base, uint8_t* stg, hipStream_t st) {
+  const uint32_t g = grid_for(n_pieces, kCopyThreads);
+  if (g == n_pieces)
+    hipLaunchKernelGGL((pack_kernel<REFRESH, false>), dim3(g), dim3(kCopyThreads), 0, st, t, first, last,
+                       piece_base, n_pieces, rec_base, stg);
+  else
+    hipLaunchKernelGGL((pack_kernel<REFRESH, true>), dim3(g), dim3(kCopyThreads), 0, st, t, first, last,
+                       piece_base, n_pieces, rec_base, stg);
+}
+
 }  // namespace
 
 hipError_t launch_score(const DeviceTables& t, hipStream_t st) {
-  const dim3 grid(t.n_chunks), block(kScoreThreads);
   if (t.dtype == 1) {
-    if (t.mode == 0) hipLaunchKernelGGL((score_kernel<1, true>), grid, block, 0, st, t);
-    else hipLaunchKernelGGL((score_kernel<1, false>), grid, block, 0, st, t);
+    if (t.mode == 0) launch_score_t<1, true>(t, st);
+    else launch_score_t<1, false>(t, st);
   } else {
-    if (t.mode == 0) hipLaunchKernelGGL((score_kernel<2, true>), grid, block, 0, st, t);
-    else hipLaunchKernelGGL((score_kernel<2, false>), grid, block, 0, st, t);
+    if (t.mode == 0) launch_score_t<2, true>(t, st);
+    else launch_score_t<2, false>(t, st);
   }
   hipLaunchKernelGGL(finalize_kernel, dim3(t.n_layers), dim3(kFinalizeThreads), 0, st, t);
   return hipGetLastError();
@@ -407,18 +499,18 @@ hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, i
 hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last_rank,
                        uint64_t piece_base, uint64_t n_pieces, uint64_t rec_base, void* staging,
                        int refresh_shadow, hipStream_t st) {
-  const dim3 grid(static_cast<uint32_t>(n_pieces)), block(kCopyThreads);
   uint8_t* stg = static_cast<uint8_t*>(staging);
-  if (refresh_shadow)
-    hipLaunchKernelGGL(pack_kernel<true>, grid, block, 0, st, t, first_rank, last_rank, piece_base, rec_base, stg);
-  else
-    hipLaunchKernelGGL(pack_kernel<false>, grid, block, 0, st, t, first_rank, last_rank, piece_base, rec_base, stg);
+  if (refresh_shadow) launch_pack_t<true>(t, first_rank, last_rank, piece_base, n_pieces, rec_base, stg, st);
+  else launch_pack_t<false>(t, first_rank, last_rank, piece_base, n_pieces, rec_base, stg, st);
   return hipGetLastError();
 }
 
 hipError_t launch_unpack(const DeviceTables& t, uint32_t n_ranks, uint64_t n_pieces, hipStream_t st) {
-  hipLaunchKernelGGL(unpack_kernel, dim3(static_cast<uint32_t>(n_pieces)), dim3(kCopyThreads), 0, st, t,
-                     n_ranks);
+  const uint32_t g = grid_for(n_pieces, kCopyThreads);
+  if (g == n_pieces)
+    hipLaunchKernelGGL(unpack_kernel<false>, dim3(g), dim3(kCopyThreads), 0, st, t, n_ranks, n_pieces);
+  else
+    hipLaunchKernelGGL(unpack_kernel<true>, dim3(g), dim3(kCopyThreads), 0, st, t, n_ranks, n_pieces);
   return hipGetLastError();
 }
 

@@ -480,7 +480,6 @@ lc_status lc_pack_selected(lc_ctx* c, void* staging, uint64_t capacity, uint32_t
     if (reinterpret_cast<uintptr_t>(staging) % kRecordAlign)
       return fail(LC_ERR_INVALID_ARG, "staging must be %u-byte aligned", kRecordAlign);
     const uint64_t pieces = c->sel_piece_prefix[last] - c->sel_piece_prefix[first_rank];
-    if (pieces >= (1ull << 32) / kCopyThreads) return fail(LC_ERR_INVALID_ARG, "pack range too large for one launch");
     LC_HIP(c, launch_pack(c->dt, first_rank, last, c->sel_piece_prefix[first_rank], pieces,
                           c->sel_rec_prefix[first_rank], staging, c->mode == LC_MODE_SNAPSHOT, c->stream));
     for (uint32_t r = first_rank; r < last; ++r)
@@ -577,7 +576,6 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
     st = upload(c, c->dt.rank_piece_prefix, rank_pp);
     if (st != LC_OK) return st;
     const uint64_t pieces = rank_pp.back();
-    if (pieces >= (1ull << 32) / kCopyThreads) return fail(LC_ERR_INVALID_ARG, "restore too large for one launch");
     LC_HIP(c, launch_unpack(c->dt, static_cast<uint32_t>(rank_layer.size()), pieces, c->stream));
   }
   // host-resident records: one copy per block, then S <- W
