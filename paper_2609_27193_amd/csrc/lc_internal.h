@@ -18,6 +18,9 @@ namespace lc {
 #ifndef LC_XCD_REMAP
 #define LC_XCD_REMAP 1
 #endif
+#ifndef LC_XCD_RUN
+#define LC_XCD_RUN 0  // 0: each XCD takes one contiguous eighth; g > 0: interleaved runs of g items
+#endif
 #ifndef LC_MAX_GRID_BLOCKS
 #define LC_MAX_GRID_BLOCKS 0  // 0: only the dispatch limit caps a grid (testing builds set it low)
 #endif

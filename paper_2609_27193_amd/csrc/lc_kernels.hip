@@ -78,7 +78,14 @@ __device__ __forceinline__ uint64_t round_up(uint64_t x, uint64_t a) { return (x
 // on the rest), which keeps each XCD's in-flight accesses within a narrow
 // address window.
 __device__ __forceinline__ uint32_t remap_xcd(uint32_t x, uint32_t G) {
-#if LC_XCD_REMAP
+#if LC_XCD_REMAP && LC_XCD_RUN > 0
+  // runs of LC_XCD_RUN consecutive items per XCD, the XCDs' runs interleaved
+  constexpr uint32_t R = 8u * LC_XCD_RUN;
+  const uint32_t full = G - G % R;
+  if (x >= full) return x;
+  const uint32_t xcd = x % 8u, k = x / 8u;
+  return (k / LC_XCD_RUN) * R + xcd * LC_XCD_RUN + k % LC_XCD_RUN;
+#elif LC_XCD_REMAP
   const uint32_t full = G - G % 8u;
   return x < full ? (x % 8u) * (full / 8u) + x / 8u : x;
 #else
