@@ -160,6 +160,52 @@ def plan_versions(versions: Sequence[dict], n_layers: int, t_fail: int) -> List[
     return choice
 
 
+# ----------------------------------------------------------------------------
+# AdamW with drift taken from the update itself (Section 3.4, "Reusing the
+# optimizer update to compute drift").  The paper trains with AdamW
+# (Section 4.1) but does not restate it; this follows the published
+# definition (Adam with bias correction, decoupled weight decay):
+#   m <- b1 m + (1 - b1) g ;  v <- b2 v + (1 - b2) g^2
+#   m_hat = m / (1 - b1^t) ;  v_hat = v / (1 - b2^t)
+#   p <- p (1 - lr wd) - lr m_hat / (sqrt(v_hat) + eps)
+# evaluated in fp32 (the optimizer state's precision) with every operation
+# rounded once, in this order; the per-step scalars are formed in fp64 and
+# rounded to fp32 once.  Drift is Eq. 1 on the optimizer's parameters:
+# u = mean|p_new - p_old| / (mean|p_old| + eps_w).
+
+
+def adamw_scalars(lr: float, beta1: float, beta2: float, eps: float, weight_decay: float, t: int) -> dict:
+    f = np.float32
+    return {"b1": f(beta1), "omb1": f(1.0 - beta1), "b2": f(beta2), "omb2": f(1.0 - beta2),
+            "c1": f(1.0 / (1.0 - beta1 ** t)), "c2": f(1.0 / (1.0 - beta2 ** t)),
+            "eps": f(eps), "lr": f(lr), "decay": f(1.0 - lr * weight_decay)}
+
+
+def adamw_update(p: np.ndarray, m: np.ndarray, v: np.ndarray, g: np.ndarray, sc: dict, decayed: bool):
+    """One AdamW step on fp32 arrays; returns (p_new, m_new, v_new)."""
+    f = np.float32
+    g = g.astype(f)
+    m_new = (sc["b1"] * m).astype(f) + (sc["omb1"] * g).astype(f)
+    v_new = (sc["b2"] * v).astype(f) + (sc["omb2"] * (g * g).astype(f)).astype(f)
+    m_hat = (m_new * sc["c1"]).astype(f)
+    v_hat = (v_new * sc["c2"]).astype(f)
+    denom = (np.sqrt(v_hat).astype(f) + sc["eps"]).astype(f)
+    upd = (m_hat / denom).astype(f)
+    p1 = (p * sc["decay"]).astype(f) if decayed else p.astype(f)
+    p_new = (p1 - (sc["lr"] * upd).astype(f)).astype(f)
+    return p_new, m_new.astype(f), v_new.astype(f)
+
+
+def bf16_round(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits, round to nearest even (NaN kept as a quiet NaN)."""
+    b = x.astype(np.float32).view(np.uint32).astype(np.uint64)
+    r = ((b + np.uint64(0x7FFF) + ((b >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)).astype(np.uint16)
+    nan = np.isnan(x)
+    if nan.any():
+        r[nan] = np.uint16(0x7FC0)
+    return r
+
+
 class LayerCheckOracle:
     """Stateful mirror of the decision step on host arrays."""
 
@@ -208,6 +254,44 @@ class LayerCheckOracle:
         self.mask = np.ones(n_layers, dtype=np.uint8)
         self.mask_step = self.t_base
         self.unpacked = set(range(n_layers))
+
+    # -- Section 3.4: AdamW step with the drift taken from the update --------
+    def adamw_step_score(self, step: int, grads, lr: float, beta1: float, beta2: float, eps: float,
+                         weight_decay: float, adam_t: int, decayed=None) -> None:
+        """``grads``: one fp32 array per segment (bf16 gradients widened
+        exactly); ``decayed``: per-segment weight-decay flags (the paper's
+        with/without weight-decay parameter groups, Section 3.4), all True
+        when None."""
+        if step <= self.last_step:
+            raise OracleError(LC_ERR_BAD_STATE, "decision steps must strictly increase")
+        if self.mode != MODE_ACCUM:
+            raise OracleError(LC_ERR_BAD_STATE, "the fused optimizer step accumulates (ACCUM mode)")
+        sc = adamw_scalars(lr, beta1, beta2, eps, weight_decay, adam_t)
+        segs = [s for g in self.by_layer for s in g]
+        for i, (s, g) in enumerate(zip(segs, grads)):
+            if s.master is not None:
+                p_old = s.master.copy()
+            else:
+                p_old = widen(s.weight, self.dtype).astype(np.float32)
+            dec = True if decayed is None else bool(decayed[i])
+            p_new, m_new, v_new = adamw_update(p_old, s.exp_avg, s.exp_avg_sq, g, sc, dec)
+            s.exp_avg[...] = m_new
+            s.exp_avg_sq[...] = v_new
+            if s.master is not None:
+                s.master[...] = p_new
+            s.weight[...] = bf16_round(p_new) if self.dtype == DT_BF16 else p_new
+            s._p_old = p_old
+            s._p_new = p_new
+        for l, g in enumerate(self.by_layer):
+            _, _, _, u = layer_update_score([s._p_new for s in g], [s._p_old for s in g], DT_F32, self.eps_w)
+            self.u[l] = u
+            self.delta[l] = self.delta[l] + u
+            for s in g:
+                del s._p_old, s._p_new
+        self.last_step = step
+        self.scored_step = step
+        self.unpacked = set()
+        self.mask = None
 
     # -- Eq. 1-2 -------------------------------------------------------------
     def score(self, step: int) -> None:

@@ -8,6 +8,7 @@ import pytest
 
 from oracle import layercheck_oracle as O
 from tests import oracle_pins as P
+from tests import test_oracle_adamw as A
 from tests.test_bruteforce_tiny import run_bruteforce
 
 SRC = open(O.__file__).read()
@@ -26,7 +27,10 @@ MUTANTS = {
                  "            if mask[l]:  # Eq. 4: reset on persist\n"),
     "no_timestamp": ("                self.delta[l] = 0.0\n                self.t_last[l] = step\n        self.scored_step = None",
                      "                self.delta[l] = 0.0\n        self.scored_step = None"),
-    "accum_overwrites": ("self.delta[l] = self.delta[l] + u", "self.delta[l] = u"),
+    "accum_overwrites": ("            if self.mode == MODE_ACCUM:\n                self.delta[l] = self.delta[l] + u",
+                         "            if self.mode == MODE_ACCUM:\n                self.delta[l] = u"),
+    "adamw_accum_overwrites": ("            self.u[l] = u\n            self.delta[l] = self.delta[l] + u",
+                               "            self.u[l] = u\n            self.delta[l] = u"),
     "accum_shadow_stale": ("        if self.mode == MODE_ACCUM:\n            # the next step's",
                            "        if False:\n            # the next step's"),
     "forced_count_wrong": ("forced[l] = 0 if by_drift else 1", "forced[l] = 1 if by_age else 0"),
@@ -41,6 +45,17 @@ MUTANTS = {
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "capacity_off_by_record": ("total + self.R[sel[last]] <= capacity", "total + self.R[sel[last]] < capacity"),
+    "adamw_no_bias_correction": ('"c1": f(1.0 / (1.0 - beta1 ** t)), "c2": f(1.0 / (1.0 - beta2 ** t)),',
+                                 '"c1": f(1.0), "c2": f(1.0),'),
+    "adamw_coupled_decay": ("    g = g.astype(f)\n    m_new", "    g = (g.astype(f) + (1.0 - sc['decay']) / sc['lr'] * p).astype(f) if decayed else g.astype(f)\n    m_new"),
+    "adamw_decay_ignores_group": ("p1 = (p * sc[\"decay\"]).astype(f) if decayed else p.astype(f)",
+                                  "p1 = (p * sc[\"decay\"]).astype(f)"),
+    "adamw_eps_inside_sqrt": ("denom = (np.sqrt(v_hat).astype(f) + sc[\"eps\"]).astype(f)",
+                              "denom = np.sqrt((v_hat + sc[\"eps\"]).astype(f)).astype(f)"),
+    "adamw_drift_on_new_params": ("_, _, _, u = layer_update_score([s._p_new for s in g], [s._p_old for s in g], DT_F32, self.eps_w)",
+                                  "_, _, _, u = layer_update_score([s._p_old for s in g], [s._p_new for s in g], DT_F32, self.eps_w)"),
+    "adamw_weights_not_rounded": ("s.weight[...] = bf16_round(p_new) if self.dtype == DT_BF16 else p_new",
+                                  "s.weight[...] = (p_new.view(np.uint32) >> 16).astype(np.uint16) if self.dtype == DT_BF16 else p_new"),
 }
 
 
@@ -69,6 +84,9 @@ def all_checks(M):
     yield lambda: M.record_bytes([128], 2, True) == 14 * 128 or (_ for _ in ()).throw(AssertionError())
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
         yield lambda mode=mode: run_bruteforce(M, mode, O.DT_BF16, 0, steps=12)
+    for chk in (A.test_first_step_is_lr_times_sign, A.test_decoupled_weight_decay_on_zero_gradient,
+                A.test_matches_torch_adamw_over_steps, A.test_fused_step_drift_is_eq1_on_the_parameters):
+        yield lambda chk=chk: chk(M)
 
 
 def test_unmutated_passes_everything():
