@@ -69,7 +69,9 @@ typedef struct {
   uint32_t reserved;  /* must be 0                                            */
   uint64_t numel;     /* > 0                                                  */
   void *weight;       /* device, live weights W (bf16 or fp32)                */
-  void *shadow;       /* device, shadow copy S, same dtype; written by the lib */
+  void *shadow;       /* device, shadow copy S, same dtype; written by the lib.
+                         May be NULL for every segment in LC_MODE_ACCUM when the
+                         drift comes from lc_adamw_step_score (no S then)      */
   float *master;      /* device fp32 master copy; NULL iff !has_master        */
   float *exp_avg;     /* device fp32 Adam first moment m                      */
   float *exp_avg_sq;  /* device fp32 Adam second moment v                     */
@@ -131,7 +133,7 @@ lc_status lc_query_layout(const lc_layout_desc *d, uint64_t *numel_out,
  * layer (Section 3.2; the base full checkpoint of Section 3.4 counts as the
  * last persist).  The base selection (every layer, at t_base) is left
  * pending so the caller can pack the base version with lc_pack_selected.
- * Enqueued on d->stream; returns after the enqueue. */
+ * Work runs on d->stream; returns once the device state is ready. */
 lc_status lc_init_layout(const lc_layout_desc *d, lc_ctx **out);
 
 /* Eq. 1-2 for every layer at decision step `step` (> every earlier step and
@@ -175,6 +177,40 @@ lc_status lc_pack_selected(lc_ctx *c, void *staging, uint64_t capacity, uint32_t
  * restore has completed on the device. */
 lc_status lc_restore_composite(lc_ctx *c, const lc_version *versions, uint32_t n_versions,
                                int64_t t_fail, int64_t *chosen_step_out);
+
+/* Hyper-parameters of one AdamW step (decoupled weight decay, bias-corrected
+ * moments).  The per-step scalars 1 - beta, 1 / (1 - beta^t) and
+ * 1 - lr * weight_decay are formed in double and rounded to float once. */
+typedef struct {
+  double lr;           /* learning rate of this step, >= 0                     */
+  double beta1;        /* first-moment decay, in [0, 1)                        */
+  double beta2;        /* second-moment decay, in [0, 1)                       */
+  double eps;          /* added to sqrt(v_hat), > 0                            */
+  double weight_decay; /* decoupled decay for segments flagged in decay_mask   */
+  int64_t adam_step;   /* bias-correction step count t >= 1                    */
+} lc_adamw_params;
+
+/* The optimizer step with the drift taken from the update itself (Section 3.4,
+ * "Reusing the optimizer update to compute drift"; AdamW as trained in
+ * Section 4.1).  For every element, in fp32 with one rounding per operation:
+ *   m <- b1 m + (1-b1) g;  v <- b2 v + (1-b2) g*g;
+ *   p_new = p * (1 - lr wd) - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
+ * where p is the fp32 master (or the weights themselves when there is no
+ * master); the master, m, v and the weights (round-to-nearest-even image of
+ * p_new) are written back.  Eq. 1 is applied to the parameters before and
+ * after the update, u_l = mean|p_new - p| / (mean|p| + eps_w), and Eq. 2 adds
+ * it to Delta_l.  One pass over the optimizer state: no shadow read or write.
+ *   grads:      host array [n_segments] of device pointers, one gradient per
+ *               segment, numel elements of grad_dtype (LC_DT_BF16 or LC_DT_F32)
+ *   decay_mask: host array [n_segments] of 0/1 (weight decay applies), or
+ *               NULL for all segments (the paper's with/without weight-decay
+ *               parameter groups)
+ * Requires LC_MODE_ACCUM and `step` greater than every earlier step; follows
+ * the same call sequence as lc_score_layers (select and pack next).  The
+ * shadow is left as it was, so lc_score_layers is refused afterwards until a
+ * restore re-synchronises it.  Asynchronous. */
+lc_status lc_adamw_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,
+                              const uint8_t *decay_mask, const lc_adamw_params *p);
 
 /* Synchronises the stream and copies the per-layer state to host arrays of
  * n_layers entries (any may be NULL): the last scores u_l, accumulators

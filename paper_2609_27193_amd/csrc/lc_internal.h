@@ -60,6 +60,29 @@ struct CopyUnit {
   uint32_t pad;
 };
 
+// One segment as the fused optimizer kernel sees it (static part).
+struct OptSeg {
+  uint64_t w;            // weights (bf16 or fp32)
+  uint64_t master;       // fp32 master, 0 when absent
+  uint64_t m;            // fp32 Adam first moment
+  uint64_t v;            // fp32 Adam second moment
+  uint64_t numel;
+  uint32_t chunk_begin;  // same chunks as the score kernel
+  uint32_t vec_ok;       // master/m/v 16-B aligned and weights aligned to 4 elements
+};
+
+// Per-call part: gradient address and weight-decay flag of each segment.
+struct GradSeg {
+  uint64_t grad;
+  uint32_t decay;
+  uint32_t vec_ok;  // gradient aligned to 4 elements
+};
+
+// fp32 scalars of one AdamW step, formed in fp64 on the host and rounded once.
+struct AdamScalars {
+  float b1, omb1, b2, omb2, c1, c2, eps, lr, decay;
+};
+
 // Written by the select kernel, copied to pinned host memory, followed by the
 // 0/1 mask of n_layers bytes.
 struct SelectHeader {
@@ -101,6 +124,8 @@ struct DeviceTables {
   uint64_t* sel_rec_prefix;           // [N+1] record byte offsets by rank
   uint64_t* sel_piece_prefix;         // [N+1] piece offsets by rank
   SelectHeader* result;               // header + mask[N]
+  const OptSeg* opt_segs;              // [n_segments]
+  const GradSeg* grad_segs;           // [n_segments], refreshed per optimizer call
   // restore scratch
   uint32_t* rank_layer;               // [N]
   uint64_t* rank_src;                 // [N]
@@ -116,5 +141,7 @@ hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last
                        void* staging, int refresh_shadow, hipStream_t st);
 hipError_t launch_unpack(const DeviceTables& t, uint32_t n_ranks, uint64_t n_pieces,
                          hipStream_t st);
+hipError_t launch_adamw(const DeviceTables& t, int grad_dtype, int has_master, const AdamScalars& sc,
+                        hipStream_t st);
 
 }  // namespace lc

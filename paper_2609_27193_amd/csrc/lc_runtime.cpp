@@ -45,6 +45,8 @@ struct HostLayout {
   std::vector<uint64_t> rec_bytes;        // [N]
   std::vector<uint64_t> layer_pieces;     // [N]
   std::vector<ScoreSeg> score_segs;
+  std::vector<OptSeg> opt_segs;
+  bool has_shadow = true;
   std::vector<uint32_t> chunk_seg;
   std::vector<uint32_t> layer_chunk_begin;  // [N+1]
   std::vector<CopyUnit> units;
@@ -79,6 +81,9 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
   L.layer_seg_begin.assign(N + 1, 0);
   L.numel.assign(N, 0);
   int64_t prev = -1;
+  L.has_shadow = d->segments[0].shadow != nullptr;
+  if (!L.has_shadow && d->mode != LC_MODE_ACCUM)
+    return fail(LC_ERR_INVALID_ARG, "a layout without shadow copies needs LC_MODE_ACCUM");
   for (uint32_t i = 0; i < d->n_segments; ++i) {
     const lc_segment& s = L.segs[i];
     if (s.layer >= N) return fail(LC_ERR_INVALID_ARG, "segment %u: layer %u out of range", i, s.layer);
@@ -89,15 +94,18 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
     if (s.reserved != 0) return fail(LC_ERR_INVALID_ARG, "segment %u: reserved field must be 0", i);
     if (s.numel == 0) return fail(LC_ERR_INVALID_ARG, "segment %u: numel is 0", i);
     if (s.numel > (1ull << 46)) return fail(LC_ERR_INVALID_ARG, "segment %u: numel too large", i);
-    if (!s.weight || !s.shadow || !s.exp_avg || !s.exp_avg_sq)
+    if (!s.weight || !s.exp_avg || !s.exp_avg_sq)
       return fail(LC_ERR_INVALID_ARG, "segment %u: NULL array pointer", i);
+    if ((s.shadow != nullptr) != L.has_shadow)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: shadow must be given for every segment or for none", i);
     if ((s.master != nullptr) != L.has_master)
       return fail(LC_ERR_INVALID_ARG, "segment %u: master must be %s", i, L.has_master ? "non-NULL" : "NULL");
     const uintptr_t wa = reinterpret_cast<uintptr_t>(s.weight), sa = reinterpret_cast<uintptr_t>(s.shadow);
     if (wa % L.esz || sa % L.esz || reinterpret_cast<uintptr_t>(s.exp_avg) % 4 ||
         reinterpret_cast<uintptr_t>(s.exp_avg_sq) % 4 || reinterpret_cast<uintptr_t>(s.master) % 4)
       return fail(LC_ERR_INVALID_ARG, "segment %u: misaligned pointer", i);
-    if (s.weight == s.shadow) return fail(LC_ERR_INVALID_ARG, "segment %u: weight and shadow alias", i);
+    if (L.has_shadow && s.weight == s.shadow)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: weight and shadow alias", i);
     if (static_cast<int64_t>(s.layer) != prev) L.layer_seg_begin[s.layer] = i;
     prev = s.layer;
     L.numel[s.layer] += s.numel;
@@ -128,6 +136,15 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
     for (uint64_t j = 0; j < k; ++j) L.chunk_seg.push_back(i);
     nchunks += k;
     L.score_segs.push_back(ss);
+    OptSeg os;
+    os.w = ss.w;
+    os.master = reinterpret_cast<uint64_t>(s.master);
+    os.m = reinterpret_cast<uint64_t>(s.exp_avg);
+    os.v = reinterpret_cast<uint64_t>(s.exp_avg_sq);
+    os.numel = s.numel;
+    os.chunk_begin = ss.chunk_begin;
+    os.vec_ok = (os.w % (4 * L.esz) == 0 && os.master % 16 == 0 && os.m % 16 == 0 && os.v % 16 == 0) ? 1u : 0u;
+    L.opt_segs.push_back(os);
     L.layer_chunk_begin[s.layer + 1] = static_cast<uint32_t>(nchunks);
   }
 
@@ -179,6 +196,11 @@ struct lc_ctx {
   DeviceTables dt{};
   std::vector<void*> allocations;
   SelectHeader* h_result = nullptr;  // pinned: header + mask[N]
+  GradSeg* h_grad = nullptr;         // pinned: per-call gradient table
+  GradSeg* d_grad = nullptr;
+  hipEvent_t grad_event = nullptr;   // marks the upload of h_grad
+  bool grad_event_pending = false;
+  bool shadow_valid = false;         // S holds what the score pass expects
 
   // state machine
   bool poisoned = false;
@@ -231,6 +253,10 @@ void free_all(lc_ctx* c) {
   c->allocations.clear();
   if (c->h_result) (void)hipHostFree(c->h_result);
   c->h_result = nullptr;
+  if (c->h_grad) (void)hipHostFree(c->h_grad);
+  c->h_grad = nullptr;
+  if (c->grad_event) (void)hipEventDestroy(c->grad_event);
+  c->grad_event = nullptr;
 }
 
 lc_status check_ctx(lc_ctx* c) {
@@ -358,6 +384,9 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
     LC_TRY(dev_alloc(c, &r8, sizeof(SelectHeader) + N));
     result = reinterpret_cast<SelectHeader*>(r8);
   }
+  OptSeg* opt_segs;
+  LC_TRY(dev_alloc(c, &opt_segs, L.opt_segs.size()));
+  LC_TRY(dev_alloc(c, &c->d_grad, L.opt_segs.size()));
   LC_TRY(dev_alloc(c, &rank_layer, N));
   LC_TRY(dev_alloc(c, &rank_src, N));
   LC_TRY(dev_alloc(c, &rpp, N + 1));
@@ -369,12 +398,22 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
       return bail(fail(LC_ERR_OOM, "hipHostMalloc failed: %s", hipGetErrorString(e)));
     }
     c->h_result = static_cast<SelectHeader*>(h);
+    h = nullptr;
+    e = hipHostMalloc(&h, sizeof(GradSeg) * L.opt_segs.size(), hipHostMallocDefault);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return bail(fail(LC_ERR_OOM, "hipHostMalloc failed: %s", hipGetErrorString(e)));
+    }
+    c->h_grad = static_cast<GradSeg*>(h);
+    e = hipEventCreateWithFlags(&c->grad_event, hipEventDisableTiming);
+    if (e != hipSuccess) return bail(fail(LC_ERR_HIP, "hipEventCreate failed: %s", hipGetErrorString(e)));
   }
   t.segs = segs; t.chunk_seg = chunk_seg; t.layer_chunk_begin = lcb; t.partials = partials;
   t.u = u; t.delta = delta; t.t_last = t_last; t.k0 = k0; t.numel = numel; t.rec_bytes = rec;
   t.layer_pieces = lpieces; t.units = units; t.piece_unit = piece_unit; t.layer_piece_begin = lpb;
   t.sel_layer = sel_layer; t.sel_rec_prefix = srp; t.sel_piece_prefix = spp; t.result = result;
   t.rank_layer = rank_layer; t.rank_src = rank_src; t.rank_piece_prefix = rpp;
+  t.opt_segs = opt_segs; t.grad_segs = c->d_grad;
 
   std::vector<double> zeros(N, 0.0), k0v(d->k0, d->k0 + N);
   std::vector<int64_t> tl(N, d->t_base);
@@ -391,8 +430,11 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
   LC_TRY(upload(c, units, L.units));
   LC_TRY(upload(c, piece_unit, L.piece_unit));
   LC_TRY(upload(c, lpb, L.layer_piece_begin));
+  LC_TRY(upload(c, opt_segs, L.opt_segs));
   // S <- W for every segment (Section 3.2: drift is measured from the base)
+  c->shadow_valid = L.has_shadow;
   for (const lc_segment& s : L.segs) {
+    if (!L.has_shadow) break;
     hipError_t e = hipMemcpyAsync(s.shadow, s.weight, s.numel * L.esz, hipMemcpyDeviceToDevice, c->stream);
     if (e != hipSuccess) return bail(fail(LC_ERR_HIP, "shadow init copy failed: %s", hipGetErrorString(e)));
   }
@@ -413,6 +455,10 @@ lc_status lc_score_layers(lc_ctx* c, int64_t step) {
   if (step <= c->last_step)
     return fail(LC_ERR_BAD_STATE, "step %lld must exceed the previous step %lld", static_cast<long long>(step),
                 static_cast<long long>(c->last_step));
+  if (!c->shadow_valid)
+    return fail(LC_ERR_BAD_STATE, c->L.has_shadow
+                                      ? "the shadow is stale after lc_adamw_step_score; restore to re-synchronise it"
+                                      : "the layout has no shadow copies; use lc_adamw_step_score");
   if (c->mode == LC_MODE_SNAPSHOT && c->pending) {
     if (!c->result_on_host) {
       st = fetch_result(c);
@@ -609,7 +655,67 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
   c->scored = false;
   c->have_selection = false;
   c->pending = false;
+  c->shadow_valid = L.has_shadow;
   c->result_on_host = false;
+  return LC_OK;
+}
+
+lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
+                              const uint8_t* decay_mask, const lc_adamw_params* p) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (!grads || !p) return fail(LC_ERR_INVALID_ARG, "grads and params must be non-NULL");
+  if (grad_dtype != LC_DT_BF16 && grad_dtype != LC_DT_F32)
+    return fail(LC_ERR_INVALID_ARG, "unknown gradient dtype %d", grad_dtype);
+  if (!(p->lr >= 0.0) || !std::isfinite(p->lr)) return fail(LC_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!(p->beta1 >= 0.0 && p->beta1 < 1.0) || !(p->beta2 >= 0.0 && p->beta2 < 1.0))
+    return fail(LC_ERR_INVALID_ARG, "betas must lie in [0, 1)");
+  if (!(p->eps > 0.0) || !std::isfinite(p->eps)) return fail(LC_ERR_INVALID_ARG, "eps must be finite and > 0");
+  if (!(p->weight_decay >= 0.0) || !std::isfinite(p->weight_decay))
+    return fail(LC_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  if (p->adam_step < 1) return fail(LC_ERR_INVALID_ARG, "adam_step must be >= 1");
+  if (c->mode != LC_MODE_ACCUM) return fail(LC_ERR_BAD_STATE, "the fused optimizer step needs LC_MODE_ACCUM");
+  if (step <= c->last_step)
+    return fail(LC_ERR_BAD_STATE, "step %lld must exceed the previous step %lld", static_cast<long long>(step),
+                static_cast<long long>(c->last_step));
+  const size_t ns = c->L.opt_segs.size();
+  const uint32_t gsz = grad_dtype == LC_DT_BF16 ? 2 : 4;
+  for (size_t i = 0; i < ns; ++i) {
+    const uintptr_t g = reinterpret_cast<uintptr_t>(grads[i]);
+    if (!g) return fail(LC_ERR_INVALID_ARG, "gradient of segment %zu is NULL", i);
+    if (g % gsz) return fail(LC_ERR_INVALID_ARG, "gradient of segment %zu is misaligned", i);
+    if (decay_mask && decay_mask[i] > 1) return fail(LC_ERR_INVALID_ARG, "decay_mask must be 0/1");
+  }
+  // the pinned table may still feed the previous call's upload
+  if (c->grad_event_pending) LC_HIP(c, hipEventSynchronize(c->grad_event));
+  for (size_t i = 0; i < ns; ++i) {
+    const uint64_t g = reinterpret_cast<uint64_t>(grads[i]);
+    c->h_grad[i].grad = g;
+    c->h_grad[i].decay = decay_mask ? decay_mask[i] : 1u;
+    c->h_grad[i].vec_ok = g % (4 * gsz) == 0 ? 1u : 0u;
+  }
+  LC_HIP(c, hipMemcpyAsync(c->d_grad, c->h_grad, sizeof(GradSeg) * ns, hipMemcpyHostToDevice, c->stream));
+  LC_HIP(c, hipEventRecord(c->grad_event, c->stream));
+  c->grad_event_pending = true;
+  const double t = static_cast<double>(p->adam_step);
+  AdamScalars sc;
+  sc.b1 = static_cast<float>(p->beta1);
+  sc.omb1 = static_cast<float>(1.0 - p->beta1);
+  sc.b2 = static_cast<float>(p->beta2);
+  sc.omb2 = static_cast<float>(1.0 - p->beta2);
+  sc.c1 = static_cast<float>(1.0 / (1.0 - std::pow(p->beta1, t)));
+  sc.c2 = static_cast<float>(1.0 / (1.0 - std::pow(p->beta2, t)));
+  sc.eps = static_cast<float>(p->eps);
+  sc.lr = static_cast<float>(p->lr);
+  sc.decay = static_cast<float>(1.0 - p->lr * p->weight_decay);
+  LC_HIP(c, launch_adamw(c->dt, grad_dtype, c->L.has_master ? 1 : 0, sc, c->stream));
+  c->last_step = step;
+  c->scored = true;
+  c->scored_step = step;
+  c->have_selection = false;
+  c->pending = false;
+  c->result_on_host = false;
+  c->shadow_valid = false;
   return LC_OK;
 }
 

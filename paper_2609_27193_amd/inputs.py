@@ -223,7 +223,8 @@ WORKLOADS = {
 # Seeds and per-layer update scales
 # ----------------------------------------------------------------------------
 
-ARRAY_IDS = {"init": 1, "update": 2, "exp_avg": 3, "exp_avg_sq": 4, "scale": 5, "misc": 6}
+ARRAY_IDS = {"init": 1, "update": 2, "exp_avg": 3, "exp_avg_sq": 4, "scale": 5, "misc": 6, "grad": 7,
+             "direction": 8}
 _M64 = (1 << 64) - 1
 
 
@@ -398,6 +399,29 @@ class SyntheticState:
             del delta
         self._redraw_moments(t)
         self.step_index = t
+
+    # -- synthetic gradients for an optimizer-driven run ------------------
+    def gradients(self, t: int, dtype=None):
+        """Flat gradient tensor for step ``t``: per element N(0, 1) noise plus
+        4 * s_l times a fixed per-element direction of layer l, so layers with
+        a larger update scale see more consistent gradients and an Adam-type
+        optimizer moves them further.  Returned in ``dtype`` (bf16 default)."""
+        torch = self.torch
+        dtype = torch.bfloat16 if dtype is None else dtype
+        g = torch.empty(self.spec.numel, dtype=dtype, device=self.device)
+        for li in range(self.spec.n_layers):
+            a, b = self.layer_range(li)
+            x = self._randn(b - a, seed_of(self.spec.seed, li, 0, "grad", t))
+            d = self._randn(b - a, seed_of(self.spec.seed, li, 0, "direction", 0))
+            x.add_(d, alpha=4.0 * float(self.scales[li]))
+            g[a:b] = x.to(dtype)
+            del x, d
+        return g
+
+    def decay_mask(self):
+        """Weight decay applies to matrices and embeddings, not to norms and
+        biases (the paper's with/without weight-decay parameter groups)."""
+        return [0 if s.kind in ("norm", "bias") else 1 for s in self.segments]
 
     # -- views -------------------------------------------------------------
     def seg_views(self, seg: SegmentView):

@@ -24,7 +24,8 @@ LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
-            "lc_restore_composite", "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
+            "lc_restore_composite", "lc_adamw_step_score", "lc_read_state", "lc_record_bytes", "lc_destroy",
+            "lc_last_error")
 
 
 class lc_segment(C.Structure):
@@ -56,6 +57,11 @@ class lc_version(C.Structure):
                 ("payload_bytes", C.c_uint64)]
 
 
+class lc_adamw_params(C.Structure):
+    _fields_ = [("lr", C.c_double), ("beta1", C.c_double), ("beta2", C.c_double), ("eps", C.c_double),
+                ("weight_decay", C.c_double), ("adam_step", C.c_int64)]
+
+
 class LCError(RuntimeError):
     def __init__(self, code: int, func: str, msg: str):
         super().__init__(f"{func} failed with status {code}: {msg}")
@@ -80,6 +86,8 @@ def load_library(path: str = LIB_PATH):
             "lc_select": (C.c_int, [C.c_void_p, C.c_int64, C.c_double, P(C.c_uint8), P(lc_select_stats)]),
             "lc_pack_selected": (C.c_int, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint32, P(lc_pack_result)]),
             "lc_restore_composite": (C.c_int, [C.c_void_p, P(lc_version), C.c_uint32, C.c_int64, P(C.c_int64)]),
+            "lc_adamw_step_score": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_void_p), C.c_int32, P(C.c_uint8),
+                                              P(lc_adamw_params)]),
             "lc_read_state": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double), P(C.c_int64)]),
             "lc_record_bytes": (C.c_uint64, [C.c_void_p, C.c_uint32]),
             "lc_destroy": (C.c_int, [C.c_void_p]),
@@ -118,7 +126,7 @@ class LayoutDesc:
                  stream: int = 0):
         self._segs = (lc_segment * len(segments))()
         for i, s in enumerate(segments):
-            self._segs[i] = lc_segment(s.layer, 0, s.numel, s.weight, s.shadow, s.master or None,
+            self._segs[i] = lc_segment(s.layer, 0, s.numel, s.weight, s.shadow or None, s.master or None,
                                        s.exp_avg, s.exp_avg_sq)
         if len(k0) != n_layers:
             raise ValueError(f"k0 has {len(k0)} entries for {n_layers} layers")
@@ -183,6 +191,19 @@ def lc_restore_composite(ctx, versions: Sequence[dict], t_fail: int, n_layers: i
                                                chosen.ctypes.data_as(C.POINTER(C.c_int64))),
            "lc_restore_composite")
     return chosen
+
+
+def lc_adamw_step_score(ctx, step: int, grads: Sequence[int], grad_dtype: int, lr: float, beta1: float,
+                        beta2: float, eps: float, weight_decay: float, adam_step: int,
+                        decay_mask: Optional[Sequence[int]] = None) -> None:
+    """grads: one device address per segment, in layout order."""
+    g = (C.c_void_p * len(grads))(*[int(x) for x in grads])
+    dm = None
+    if decay_mask is not None:
+        dm_arr = np.ascontiguousarray(decay_mask, dtype=np.uint8)
+        dm = dm_arr.ctypes.data_as(C.POINTER(C.c_uint8))
+    prm = lc_adamw_params(lr, beta1, beta2, eps, weight_decay, adam_step)
+    _check(load_library().lc_adamw_step_score(ctx, step, g, grad_dtype, dm, C.byref(prm)), "lc_adamw_step_score")
 
 
 def lc_read_state(ctx, n_layers: int):

@@ -205,6 +205,29 @@ class Pair:
         if g.master is not None:
             g.master.copy_(torch.from_numpy(self.hM))
 
+    def fused_step(self, t, adam_t, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, wd=0.01, grad_dtype="bf16",
+                   lr_scale=1.0, capacity=None):
+        """One AdamW step with the drift taken from the update, on both sides,
+        then select and pack."""
+        torch = self.torch
+        gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
+        g = self.gen.gradients(t, gdt)
+        dg = g.to("cuda")
+        gf = g.float().numpy()  # exact widening of bf16 gradients
+        decay = self.gen.decay_mask()
+        ptrs = [dg[s.offset:s.offset + s.numel].data_ptr() for s in self.gen.segments]
+        LC.lc_adamw_step_score(self.ctx, t, ptrs, LC.LC_DT_BF16 if grad_dtype == "bf16" else LC.LC_DT_F32,
+                               lr, beta1, beta2, eps, wd, adam_t, decay)
+        self.orc.adamw_step_score(t, [gf[s.offset:s.offset + s.numel] for s in self.gen.segments],
+                                  lr, beta1, beta2, eps, wd, adam_t, decay)
+        u, d, tl = LC.lc_read_state(self.ctx, self.N)
+        assert rel_ok(u, self.orc.u), (t, u, self.orc.u)
+        assert rel_ok(d, self.orc.delta), (t, d, self.orc.delta)
+        self.check_arrays()  # optimizer state and weights bit-exact
+        mask, st = self.select(t, lr_scale, d, tl)
+        self.pack(t, mask, capacity)
+        return mask, st
+
     def step(self, t, lr_scale=1.0, capacity=None):
         self.advance(t)
         d, tl = self.score(t)
