@@ -314,7 +314,7 @@ class SyntheticState:
     entry per parameter tensor in layer order.
     """
 
-    def __init__(self, spec: ModelSpec, device="cpu", init: bool = True):
+    def __init__(self, spec: ModelSpec, device="cpu", init: bool = True, shadow: bool = True):
         import torch
         self.torch = torch
         self.spec = spec
@@ -324,7 +324,7 @@ class SyntheticState:
         P = spec.numel
         wdt = torch.bfloat16 if spec.weight_dtype == "bf16" else torch.float32
         self.weight = torch.empty(P, dtype=wdt, device=self.device)
-        self.shadow = torch.empty(P, dtype=wdt, device=self.device)
+        self.shadow = torch.empty(P, dtype=wdt, device=self.device) if shadow else None
         self.master = torch.empty(P, dtype=torch.float32, device=self.device) if spec.has_master else None
         self.exp_avg = torch.empty(P, dtype=torch.float32, device=self.device)
         self.exp_avg_sq = torch.empty(P, dtype=torch.float32, device=self.device)
@@ -426,7 +426,7 @@ class SyntheticState:
     # -- views -------------------------------------------------------------
     def seg_views(self, seg: SegmentView):
         sl = slice(seg.offset, seg.offset + seg.numel)
-        return (self.weight[sl], self.shadow[sl],
+        return (self.weight[sl], None if self.shadow is None else self.shadow[sl],
                 None if self.master is None else self.master[sl],
                 self.exp_avg[sl], self.exp_avg_sq[sl])
 

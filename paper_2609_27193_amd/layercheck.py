@@ -112,7 +112,7 @@ class Segment:
     layer: int
     numel: int
     weight: int
-    shadow: int
+    shadow: Optional[int]
     master: Optional[int]
     exp_avg: int
     exp_avg_sq: int
@@ -229,6 +229,6 @@ def segments_from_state(state) -> List[Segment]:
     out = []
     for seg in state.segments:
         w, s, m, a, v = state.seg_views(seg)
-        out.append(Segment(seg.layer, seg.numel, w.data_ptr(), s.data_ptr(),
+        out.append(Segment(seg.layer, seg.numel, w.data_ptr(), None if s is None else s.data_ptr(),
                            None if m is None else m.data_ptr(), a.data_ptr(), v.data_ptr()))
     return out
