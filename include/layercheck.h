@@ -74,7 +74,9 @@ typedef struct {
                          drift comes from lc_adamw_step_score (no S then)      */
   float *master;      /* device fp32 master copy; NULL iff !has_master        */
   float *exp_avg;     /* device fp32 Adam first moment m                      */
-  float *exp_avg_sq;  /* device fp32 Adam second moment v                     */
+  float *exp_avg_sq;  /* device fp32 Adam second moment v.  Both may be NULL for
+                         every segment: records then hold the weights (and
+                         master) only, the SGD variant of Section 4.7          */
 } lc_segment;
 
 typedef struct {
@@ -157,7 +159,7 @@ lc_status lc_select(lc_ctx *c, int64_t step, double lr_scale, uint8_t *mask_out,
  * layers of rank >= first_rank (ranks count selected layers in ascending id)
  * into `staging` (device, 256-byte aligned), as many whole records as fit in
  * `capacity` bytes.  Record of layer l: its W blocks, then master (if
- * present), exp_avg and exp_avg_sq blocks; one block per segment in layout
+ * present), exp_avg and exp_avg_sq blocks (if present); one block per segment in layout
  * order holding the raw little-endian bytes, zero-padded to a multiple of 256
  * bytes.  Records are concatenated without gaps.  SNAPSHOT mode also sets
  * S <- W for the packed layers in the same pass.  Returns LC_ERR_CAPACITY if

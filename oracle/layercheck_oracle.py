@@ -108,14 +108,18 @@ def padded(nbytes: int) -> int:
     return (nbytes + PAD - 1) // PAD * PAD
 
 
-def _arrays_in_record(has_master: bool) -> List[str]:
-    return ["weight"] + (["master"] if has_master else []) + ["exp_avg", "exp_avg_sq"]
+def _arrays_in_record(has_master: bool, has_moments: bool = True) -> List[str]:
+    """Weights and their optimizer tensors (Section 3.2); without Adam moments
+    (the SGD variant of Section 4.7) a record holds the weights only."""
+    return (["weight"] + (["master"] if has_master else [])
+            + (["exp_avg", "exp_avg_sq"] if has_moments else []))
 
 
-def record_bytes(seg_numels: Sequence[int], weight_itemsize: int, has_master: bool) -> int:
+def record_bytes(seg_numels: Sequence[int], weight_itemsize: int, has_master: bool,
+                 has_moments: bool = True) -> int:
     """Size of one layer's packed record: every (array, tensor) block padded."""
     total = 0
-    for arr in _arrays_in_record(has_master):
+    for arr in _arrays_in_record(has_master, has_moments):
         item = weight_itemsize if arr == "weight" else 4
         for n in seg_numels:
             total += padded(n * item)
@@ -219,8 +223,11 @@ class LayerCheckOracle:
         if len(k0) != n_layers or s_max < 1 or not (eps_w >= 0.0):
             raise OracleError(LC_ERR_INVALID_ARG, "bad thresholds")
         self.by_layer: List[List[OSegment]] = [[] for _ in range(n_layers)]
+        self.has_moments = segments[0].exp_avg is not None
         last = -1
         for s in segments:
+            if (s.exp_avg is None) == self.has_moments or (s.exp_avg_sq is None) == self.has_moments:
+                raise OracleError(LC_ERR_INVALID_ARG, "Adam moments must be given for every segment or none")
             if not (0 <= s.layer < n_layers) or s.layer < last or s.numel == 0:
                 raise OracleError(LC_ERR_INVALID_ARG, "segments must be grouped by ascending layer")
             if (s.master is None) == has_master:
@@ -239,7 +246,8 @@ class LayerCheckOracle:
         self.eps_w = float(eps_w)
         self.t_base = int(t_base)
         self.n = [sum(s.numel for s in g) for g in self.by_layer]
-        self.R = [record_bytes([s.numel for s in g], self.itemsize, has_master) for g in self.by_layer]
+        self.R = [record_bytes([s.numel for s in g], self.itemsize, has_master, self.has_moments)
+                  for g in self.by_layer]
         # Section 3.2: accumulators start at 0; every layer counts as persisted
         # by the base full checkpoint at t_base; the shadow starts equal to W.
         self.delta = [0.0] * n_layers
@@ -266,6 +274,8 @@ class LayerCheckOracle:
             raise OracleError(LC_ERR_BAD_STATE, "decision steps must strictly increase")
         if self.mode != MODE_ACCUM:
             raise OracleError(LC_ERR_BAD_STATE, "the fused optimizer step accumulates (ACCUM mode)")
+        if not self.has_moments:
+            raise OracleError(LC_ERR_BAD_STATE, "AdamW needs the moment arrays")
         sc = adamw_scalars(lr, beta1, beta2, eps, weight_decay, adam_t)
         segs = [s for g in self.by_layer for s in g]
         for i, (s, g) in enumerate(zip(segs, grads)):
@@ -369,7 +379,7 @@ class LayerCheckOracle:
     def layer_record(self, l: int) -> bytes:
         out = bytearray()
         g = self.by_layer[l]
-        for arr in _arrays_in_record(self.has_master):
+        for arr in _arrays_in_record(self.has_master, self.has_moments):
             for s in g:
                 raw = getattr(s, arr).tobytes()
                 out += raw
@@ -420,7 +430,7 @@ class LayerCheckOracle:
             off = sum(self.R[j] for j in range(l) if v["mask"][j])
             rec = bytes(np.asarray(v["payload"], dtype=np.uint8)[off:off + self.R[l]])
             pos = 0
-            for arr in _arrays_in_record(self.has_master):
+            for arr in _arrays_in_record(self.has_master, self.has_moments):
                 for s in self.by_layer[l]:
                     dst = getattr(s, arr)
                     nb = dst.nbytes

@@ -47,6 +47,7 @@ struct HostLayout {
   std::vector<ScoreSeg> score_segs;
   std::vector<OptSeg> opt_segs;
   bool has_shadow = true;
+  bool has_moments = true;
   std::vector<uint32_t> chunk_seg;
   std::vector<uint32_t> layer_chunk_begin;  // [N+1]
   std::vector<CopyUnit> units;
@@ -82,6 +83,7 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
   L.numel.assign(N, 0);
   int64_t prev = -1;
   L.has_shadow = d->segments[0].shadow != nullptr;
+  L.has_moments = d->segments[0].exp_avg != nullptr;
   if (!L.has_shadow && d->mode != LC_MODE_ACCUM)
     return fail(LC_ERR_INVALID_ARG, "a layout without shadow copies needs LC_MODE_ACCUM");
   for (uint32_t i = 0; i < d->n_segments; ++i) {
@@ -94,8 +96,9 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
     if (s.reserved != 0) return fail(LC_ERR_INVALID_ARG, "segment %u: reserved field must be 0", i);
     if (s.numel == 0) return fail(LC_ERR_INVALID_ARG, "segment %u: numel is 0", i);
     if (s.numel > (1ull << 46)) return fail(LC_ERR_INVALID_ARG, "segment %u: numel too large", i);
-    if (!s.weight || !s.exp_avg || !s.exp_avg_sq)
-      return fail(LC_ERR_INVALID_ARG, "segment %u: NULL array pointer", i);
+    if (!s.weight) return fail(LC_ERR_INVALID_ARG, "segment %u: NULL weight pointer", i);
+    if ((s.exp_avg != nullptr) != L.has_moments || (s.exp_avg_sq != nullptr) != L.has_moments)
+      return fail(LC_ERR_INVALID_ARG, "segment %u: Adam moments must be given for every segment or for none", i);
     if ((s.shadow != nullptr) != L.has_shadow)
       return fail(LC_ERR_INVALID_ARG, "segment %u: shadow must be given for every segment or for none", i);
     if ((s.master != nullptr) != L.has_master)
@@ -156,6 +159,7 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
     uint64_t rec = 0, pieces = 0;
     for (int arr = 0; arr < 4; ++arr) {
       if (arr == 1 && !L.has_master) continue;
+      if (arr >= 2 && !L.has_moments) continue;
       for (uint32_t i = L.layer_seg_begin[l]; i < L.layer_seg_begin[l + 1]; ++i) {
         const lc_segment& s = L.segs[i];
         CopyUnit u{};
@@ -628,11 +632,9 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
   for (const auto& hl : host_layers) {
     const uint32_t l = hl.first;
     uint32_t ub = 0;
-    for (uint32_t j = 0; j < l; ++j) {
-      const uint32_t nseg = L.layer_seg_begin[j + 1] - L.layer_seg_begin[j];
-      ub += nseg * (L.has_master ? 4 : 3);
-    }
-    const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * (L.has_master ? 4 : 3);
+    const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
+    for (uint32_t j = 0; j < l; ++j) ub += (L.layer_seg_begin[j + 1] - L.layer_seg_begin[j]) * per_seg;
+    const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * per_seg;
     for (uint32_t k = 0; k < nu; ++k) {
       const CopyUnit& u = L.units[ub + k];
       LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.arr), hl.second + u.rec_off, u.bytes,
@@ -675,6 +677,7 @@ lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads,
     return fail(LC_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
   if (p->adam_step < 1) return fail(LC_ERR_INVALID_ARG, "adam_step must be >= 1");
   if (c->mode != LC_MODE_ACCUM) return fail(LC_ERR_BAD_STATE, "the fused optimizer step needs LC_MODE_ACCUM");
+  if (!c->L.has_moments) return fail(LC_ERR_BAD_STATE, "the layout has no Adam moments");
   if (step <= c->last_step)
     return fail(LC_ERR_BAD_STATE, "step %lld must exceed the previous step %lld", static_cast<long long>(step),
                 static_cast<long long>(c->last_step));

@@ -114,8 +114,8 @@ class Segment:
     weight: int
     shadow: Optional[int]
     master: Optional[int]
-    exp_avg: int
-    exp_avg_sq: int
+    exp_avg: Optional[int]
+    exp_avg_sq: Optional[int]
 
 
 class LayoutDesc:
@@ -127,7 +127,7 @@ class LayoutDesc:
         self._segs = (lc_segment * len(segments))()
         for i, s in enumerate(segments):
             self._segs[i] = lc_segment(s.layer, 0, s.numel, s.weight, s.shadow or None, s.master or None,
-                                       s.exp_avg, s.exp_avg_sq)
+                                       s.exp_avg or None, s.exp_avg_sq or None)
         if len(k0) != n_layers:
             raise ValueError(f"k0 has {len(k0)} entries for {n_layers} layers")
         self._k0 = (C.c_double * n_layers)(*[float(x) for x in k0])

@@ -49,7 +49,7 @@ class Pair:
     """Owns one synthetic state, its device copy for the library, its host
     copy for the oracle, and both implementations."""
 
-    def __init__(self, spec, mode, k0, eps_w=1e-8, t_base=0, segments=None):
+    def __init__(self, spec, mode, k0, eps_w=1e-8, t_base=0, moments=True):
         import torch
         self.torch = torch
         self.spec = spec
@@ -74,10 +74,12 @@ class Pair:
         for s in g.segments:
             a, b = s.offset, s.offset + s.numel
             osegs.append(O.OSegment(s.layer, self.hW[a:b], self.hS[a:b],
-                                    None if self.hM is None else self.hM[a:b], self.hm[a:b], self.hv[a:b]))
+                                    None if self.hM is None else self.hM[a:b],
+                                    self.hm[a:b] if moments else None, self.hv[a:b] if moments else None))
             lsegs.append(LC.Segment(s.layer, s.numel, self.dW[a:b].data_ptr(), self.dS[a:b].data_ptr(),
                                     None if self.dM is None else self.dM[a:b].data_ptr(),
-                                    self.dm[a:b].data_ptr(), self.dv[a:b].data_ptr()))
+                                    self.dm[a:b].data_ptr() if moments else None,
+                                    self.dv[a:b].data_ptr() if moments else None))
         self.lsegs = lsegs
         self.orc = O.LayerCheckOracle(osegs, self.N, self.dtype, spec.has_master, mode, self.k0,
                                       spec.s_max, eps_w=eps_w, t_base=t_base)

@@ -37,13 +37,13 @@ def test_exports_every_declared_symbol(lib):
 FAKE = 0x7F0000000000  # never dereferenced by lc_query_layout
 
 
-def fake_segments(sizes, esz=2, master=True, offset=0):
+def fake_segments(sizes, esz=2, master=True, offset=0, moments=True):
     segs, addr = [], FAKE + offset
     for l, layer in enumerate(sizes):
         for n in layer:
             step = (n * 4 + 255) // 256 * 256
             segs.append(LC.Segment(l, n, addr, addr + step, addr + 2 * step if master else None,
-                                   addr + 3 * step, addr + 4 * step))
+                                   addr + 3 * step if moments else None, addr + 4 * step if moments else None))
             addr += 5 * step
     return segs
 
@@ -66,6 +66,21 @@ def test_record_bytes_match_oracle(lib, sizes, dtype, master):
     assert numel == [sum(l) for l in sizes]
     esz = 2 if dtype == LC.LC_DT_BF16 else 4
     assert rec == [O.record_bytes(l, esz, master) for l in sizes]
+
+
+@pytest.mark.parametrize("master", [True, False])
+def test_weights_only_records_match_oracle(lib, master):
+    """The SGD variant (Section 4.7): records hold the weights (and master)
+    without Adam moments."""
+    sizes = [[4097, 5], [128]]
+    segs = fake_segments(sizes, master=master, moments=False)
+    _, rec = LC.lc_query_layout(desc(segs, 2, has_master=master))
+    assert rec == [O.record_bytes(l, 2, master, has_moments=False) for l in sizes]
+    assert O.record_bytes([128], 2, True, has_moments=False) == 6 * 128
+    mixed = fake_segments(sizes, master=master, moments=False)
+    mixed[1].exp_avg = FAKE + (1 << 30)
+    with pytest.raises(LC.LCError):
+        LC.lc_query_layout(desc(mixed, 2, has_master=master))
 
 
 def _expect(code, fn):

@@ -35,7 +35,7 @@ MUTANTS = {
                            "        if False:\n            # the next step's"),
     "forced_count_wrong": ("forced[l] = 0 if by_drift else 1", "forced[l] = 1 if by_age else 0"),
     "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
-    "moments_swapped": ('+ ["exp_avg", "exp_avg_sq"]', '+ ["exp_avg_sq", "exp_avg"]'),
+    "moments_swapped": ('["exp_avg", "exp_avg_sq"] if has_moments', '["exp_avg_sq", "exp_avg"] if has_moments'),
     "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),
     "restore_ignores_t_fail": ('if v["step"] <= t_fail and v["mask"][l]:', 'if v["mask"][l]:'),
     "restore_offset_counts_all": ('off = sum(self.R[j] for j in range(l) if v["mask"][j])',

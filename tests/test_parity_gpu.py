@@ -226,3 +226,39 @@ def test_scores_bitwise_reproducible_and_zero_change():
     finally:
         pa.close()
         pb.close()
+
+
+def tied_spec():
+    """Tied lm_head (Section 2.2): N = B + 2 layer groups, as for the paper's
+    Qwen2.5-3B and Llama-3.2-1B; reduced width."""
+    return I.ModelSpec(name="tied-reduced", layers=I._decoder_layers(192, 512, 3, 500, 6, 2, tied=True),
+                       weight_dtype="bf16", has_master=True, scale_rule="loguniform_2dec_embed0.1",
+                       target_fraction=0.2, s_max=4)
+
+
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_weights_only_records_sgd_variant(mode):
+    """Records without Adam moments (Section 4.7), capacity-limited packs and a
+    composite restore, against the oracle."""
+    spec = reduced_8b()
+    p = Pair(spec, mode, k0_for(spec, 0.01), moments=False)
+    try:
+        assert p.R == [O.record_bytes([t.numel for t in l.tensors], 2, True, has_moments=False)
+                       for l in spec.layers]
+        p.pack(0, np.ones(p.N, np.uint8))
+        run_steps(p, range(1, 7), capacity=lambda t: max(p.R) if t % 2 else None)
+        _restore_and_compare(p, 5, "device")
+    finally:
+        p.close()
+
+
+def test_tied_embedding_layout():
+    spec = tied_spec()
+    assert spec.n_layers == 3 + 2
+    p = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 0.01))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        run_steps(p, range(1, 6))
+        p.check_arrays()
+    finally:
+        p.close()
