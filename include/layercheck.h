@@ -214,6 +214,60 @@ typedef struct {
 lc_status lc_adamw_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,
                               const uint8_t *decay_mask, const lc_adamw_params *p);
 
+/* ---- Persistence store (Section 3.5 "Metadata-driven reconstruction") ------
+ * A directory of version files plus an append-only manifest recording the
+ * persistence history: per version its step, its layer mask and its payload
+ * (records in the lc_pack_selected format).  A version is visible once its
+ * file is complete and fsync'ed and its manifest line ("LCV1 <step> <bytes>
+ * <file> <mask as 0/1 characters>") is written and fsync'ed; on open, torn or
+ * inconsistent lines and files of the wrong size are ignored.  A store is
+ * used from one thread; it owns one writer thread. */
+typedef struct lc_store lc_store;
+
+/* Opens (creating the directory itself, not its parents) the store of a
+ * layout with the given per-layer record sizes (lc_query_layout /
+ * lc_record_bytes).  buffer_bytes sizes each of the four pinned drain buffers
+ * (0: 256 MiB). */
+lc_status lc_store_open(const char *dir, uint32_t n_layers, const uint64_t *record_bytes, uint64_t buffer_bytes,
+                        lc_store **out);
+
+/* Appends one version: `payload` holds the records of the layers in `mask`
+ * (host [n_layers], 0/1), payload_bytes their total size.  Device payloads
+ * (e.g. the staging buffer of lc_pack_selected) are copied out through the
+ * pinned buffers on a store-owned stream that first waits for the work
+ * already enqueued on `stream` (hipStream_t, NULL = null stream); `stream`
+ * then waits for those copies, so later work on it may reuse the buffer.  The
+ * call returns once every copy is enqueued (it blocks while the drain buffers
+ * are full); the files are written by the writer thread.  Host payloads are
+ * written before the call returns.  A layer may be stored at most once per
+ * step (several versions of one step must have disjoint masks). */
+lc_status lc_store_append(lc_store *s, int64_t step, const uint8_t *mask, const void *payload,
+                          uint64_t payload_bytes, void *stream);
+
+/* Waits until every appended version is durable and visible. */
+lc_status lc_store_sync(lc_store *s);
+
+/* Visible versions, in manifest order. */
+lc_status lc_store_count(lc_store *s, uint32_t *n_out);
+lc_status lc_store_entry(lc_store *s, uint32_t i, int64_t *step_out, uint8_t *mask_out /* [n_layers] or NULL */,
+                         uint64_t *bytes_out);
+
+/* The reconstruction plan (Section 3.5 step 1) over the visible versions:
+ * per layer the greatest stored step <= t_fail holding it (host
+ * [n_layers]); LC_ERR_NO_VERSION / LC_ERR_INVALID_ARG as for
+ * lc_restore_composite. */
+lc_status lc_store_plan(lc_store *s, int64_t t_fail, int64_t *chosen_step_out);
+
+/* Composite recovery from the store (Section 3.5 steps 2-3): reads only the
+ * chosen record of every layer (double-buffered pinned reads, several reader
+ * threads) and restores it into the context's arrays exactly as
+ * lc_restore_composite does.  The context's layout must match the store's
+ * record sizes.  Returns after the restore has completed. */
+lc_status lc_store_restore(lc_store *s, lc_ctx *c, int64_t t_fail, int64_t *chosen_step_out);
+
+/* Waits for pending writes, stops the writer and frees the store. */
+lc_status lc_store_close(lc_store *s);
+
 /* Synchronises the stream and copies the per-layer state to host arrays of
  * n_layers entries (any may be NULL): the last scores u_l, accumulators
  * Delta_l and last-persist steps t_l. */

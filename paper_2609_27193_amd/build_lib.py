@@ -12,13 +12,13 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblayercheck.so")
-SOURCES = ["lc_runtime.cpp", "lc_kernels.hip"]
+SOURCES = ["lc_runtime.cpp", "lc_store.cpp", "lc_kernels.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",
     "-ffp-contract=off",                      # keep the fp64 score formula unfused
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
-    "-Wall", "-Wno-unused-result",
+    "-Wall", "-Wno-unused-result", "-pthread",
     "-I", os.path.join(ROOT, "include"),
 ]
 

@@ -13,48 +13,16 @@
 #include <vector>
 
 #include "../../include/layercheck.h"
+#include "lc_ctx.h"
 #include "lc_internal.h"
 
 using namespace lc;
 
+thread_local std::string lc::g_error;
+
 namespace {
 
-thread_local std::string g_error;
-
-lc_status fail(lc_status st, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof(buf), fmt, ap);
-  va_end(ap);
-  g_error = buf;
-  return st;
-}
-
 uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
-
-// Host-side layout derived from a descriptor (no GPU work).
-struct HostLayout {
-  uint32_t N = 0;
-  int dtype = 0;
-  uint32_t esz = 0;
-  bool has_master = false;
-  std::vector<lc_segment> segs;
-  std::vector<uint32_t> layer_seg_begin;  // [N+1]
-  std::vector<uint64_t> numel;            // [N]
-  std::vector<uint64_t> rec_bytes;        // [N]
-  std::vector<uint64_t> layer_pieces;     // [N]
-  std::vector<ScoreSeg> score_segs;
-  std::vector<OptSeg> opt_segs;
-  bool has_shadow = true;
-  bool has_moments = true;
-  std::vector<uint32_t> chunk_seg;
-  std::vector<uint32_t> layer_chunk_begin;  // [N+1]
-  std::vector<CopyUnit> units;
-  std::vector<uint32_t> piece_unit;
-  std::vector<uint64_t> layer_piece_begin;  // [N+1]
-  uint64_t total_numel = 0;
-};
 
 lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
   if (!d) return fail(LC_ERR_INVALID_ARG, "descriptor is NULL");
@@ -190,36 +158,6 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
 
 }  // namespace
 
-struct lc_ctx {
-  HostLayout L;
-  int mode = 0;
-  int64_t s_max = 1;
-  double eps_w = 0;
-  int64_t t_base = 0;
-  hipStream_t stream = nullptr;
-  DeviceTables dt{};
-  std::vector<void*> allocations;
-  SelectHeader* h_result = nullptr;  // pinned: header + mask[N]
-  GradSeg* h_grad = nullptr;         // pinned: per-call gradient table
-  GradSeg* d_grad = nullptr;
-  hipEvent_t grad_event = nullptr;   // marks the upload of h_grad
-  bool grad_event_pending = false;
-  bool shadow_valid = false;         // S holds what the score pass expects
-
-  // state machine
-  bool poisoned = false;
-  int64_t last_step = 0;
-  bool scored = false;
-  int64_t scored_step = 0;
-  bool have_selection = false; // a selection (or the base) exists to pack
-  bool pending = false;        // a selection whose records are not all packed
-  bool result_on_host = false; // h_result reflects the pending selection
-  std::vector<uint32_t> sel;            // selected layers, ascending
-  std::vector<uint64_t> sel_rec_prefix, sel_piece_prefix;
-  std::vector<uint8_t> rank_packed;
-  uint32_t n_unpacked = 0;
-};
-
 namespace {
 
 #define LC_HIP(ctx, call)                                                                  \
@@ -308,6 +246,44 @@ lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode) {
 }
 
 }  // namespace
+
+namespace lc {
+
+lc_status restore_layer_from_host(lc_ctx* c, uint32_t l, const uint8_t* record) {
+  const HostLayout& L = c->L;
+  const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
+  uint32_t ub = 0;
+  for (uint32_t j = 0; j < l; ++j) ub += (L.layer_seg_begin[j + 1] - L.layer_seg_begin[j]) * per_seg;
+  const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * per_seg;
+  for (uint32_t k = 0; k < nu; ++k) {
+    const CopyUnit& u = L.units[ub + k];
+    LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.arr), record + u.rec_off, u.bytes, hipMemcpyHostToDevice,
+                             c->stream));
+    if (u.shadow)
+      LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.shadow), reinterpret_cast<void*>(u.arr), u.bytes,
+                               hipMemcpyDeviceToDevice, c->stream));
+  }
+  return LC_OK;
+}
+
+lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& steps) {
+  const uint32_t N = c->L.N;
+  std::vector<double> zeros(N, 0.0);
+  lc_status st = upload(c, c->dt.delta, zeros);
+  if (st != LC_OK) return st;
+  st = upload(c, c->dt.t_last, steps);
+  if (st != LC_OK) return st;
+  LC_HIP(c, hipStreamSynchronize(c->stream));
+  c->last_step = t_fail;
+  c->scored = false;
+  c->have_selection = false;
+  c->pending = false;
+  c->shadow_valid = c->L.has_shadow;
+  c->result_on_host = false;
+  return LC_OK;
+}
+
+}  // namespace lc
 
 extern "C" {
 
@@ -630,35 +606,14 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
   }
   // host-resident records: one copy per block, then S <- W
   for (const auto& hl : host_layers) {
-    const uint32_t l = hl.first;
-    uint32_t ub = 0;
-    const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
-    for (uint32_t j = 0; j < l; ++j) ub += (L.layer_seg_begin[j + 1] - L.layer_seg_begin[j]) * per_seg;
-    const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * per_seg;
-    for (uint32_t k = 0; k < nu; ++k) {
-      const CopyUnit& u = L.units[ub + k];
-      LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.arr), hl.second + u.rec_off, u.bytes,
-                               hipMemcpyHostToDevice, c->stream));
-      if (u.shadow)
-        LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.shadow), reinterpret_cast<void*>(u.arr), u.bytes,
-                                 hipMemcpyDeviceToDevice, c->stream));
-    }
+    st = restore_layer_from_host(c, hl.first, hl.second);
+    if (st != LC_OK) return st;
   }
-  std::vector<double> zeros(N, 0.0);
   std::vector<int64_t> steps(N);
   for (uint32_t l = 0; l < N; ++l) steps[l] = v[choice[l]].step;
-  st = upload(c, c->dt.delta, zeros);
+  st = restore_finish(c, t_fail, steps);
   if (st != LC_OK) return st;
-  st = upload(c, c->dt.t_last, steps);
-  if (st != LC_OK) return st;
-  LC_HIP(c, hipStreamSynchronize(c->stream));
   if (chosen_step_out) std::memcpy(chosen_step_out, steps.data(), N * sizeof(int64_t));
-  c->last_step = t_fail;
-  c->scored = false;
-  c->have_selection = false;
-  c->pending = false;
-  c->shadow_valid = L.has_shadow;
-  c->result_on_host = false;
   return LC_OK;
 }
 

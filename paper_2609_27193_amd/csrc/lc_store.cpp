@@ -1,0 +1,614 @@
+// Persistence store: the durable side of selective persistence and the
+// metadata-driven reconstruction of Section 3.5.
+//
+// A store is a directory of version files (one payload each: the records of
+// the layers packed at one step, in the lc_pack_selected format) and an
+// append-only manifest.  A version becomes visible only after its file is
+// complete and fsync'ed and its manifest line is written and fsync'ed, so a
+// crash leaves at most an ignored partial file.  Device payloads are drained
+// through a ring of pinned host buffers on a store-owned stream; a writer
+// thread writes each buffer as soon as its copy completes, so the caller's
+// stream is released as soon as the staging buffer has been read.
+#include <fcntl.h>
+#include <sys/stat.h>
+#include <sys/types.h>
+#include <unistd.h>
+
+#include <algorithm>
+#include <atomic>
+#include <cerrno>
+#include <condition_variable>
+#include <cstring>
+#include <deque>
+#include <map>
+#include <mutex>
+#include <new>
+#include <string>
+#include <thread>
+#include <vector>
+
+#include "lc_ctx.h"
+
+using namespace lc;
+
+namespace {
+
+struct StoredVersion {
+  int64_t step = 0;
+  std::vector<uint8_t> mask;
+  uint64_t bytes = 0;
+  std::string file;
+};
+
+struct WriteJob {
+  int fd = -1;
+  uint64_t file_off = 0;
+  uint64_t len = 0;
+  int slot = -1;                   // pinned ring slot, or -1 for a caller host buffer
+  const uint8_t* host_src = nullptr;
+  bool last = false;               // the version is complete after this job
+  size_t version = 0;              // index into lc_store::writing
+};
+
+bool write_all(int fd, const uint8_t* p, uint64_t n, uint64_t off) {
+  while (n > 0) {
+    const ssize_t w = pwrite(fd, p, n > (1ull << 30) ? (1ull << 30) : n, static_cast<off_t>(off));
+    if (w < 0) {
+      if (errno == EINTR) continue;
+      return false;
+    }
+    p += w;
+    n -= static_cast<uint64_t>(w);
+    off += static_cast<uint64_t>(w);
+  }
+  return true;
+}
+
+bool read_all(int fd, uint8_t* p, uint64_t n, uint64_t off) {
+  while (n > 0) {
+    const ssize_t r = pread(fd, p, n > (1ull << 30) ? (1ull << 30) : n, static_cast<off_t>(off));
+    if (r < 0) {
+      if (errno == EINTR) continue;
+      return false;
+    }
+    if (r == 0) return false;
+    p += r;
+    n -= static_cast<uint64_t>(r);
+    off += static_cast<uint64_t>(r);
+  }
+  return true;
+}
+
+std::string mask_string(const std::vector<uint8_t>& m) {
+  std::string s(m.size(), '0');
+  for (size_t i = 0; i < m.size(); ++i) s[i] = m[i] ? '1' : '0';
+  return s;
+}
+
+}  // namespace
+
+struct lc_store {
+  std::string dir;
+  uint32_t N = 0;
+  std::vector<uint64_t> R;
+  std::vector<StoredVersion> durable;  // visible versions, manifest order
+  std::vector<StoredVersion> writing;  // being written (indices stay valid until sync)
+  int manifest_fd = -1;
+  uint64_t seq = 0;
+  uint64_t skipped = 0;                // manifest lines ignored at open
+  // drain pipeline
+  uint64_t slot_bytes = 0;
+  uint32_t n_slots = 0;
+  bool gpu_ready = false;
+  hipStream_t copy_stream = nullptr;
+  hipEvent_t caller_ready = nullptr, copies_done = nullptr;
+  std::vector<uint8_t*> slots;
+  std::vector<hipEvent_t> slot_events;
+  std::vector<int> slot_free;
+  std::mutex mu;
+  std::condition_variable cv;
+  std::deque<WriteJob> queue;
+  uint64_t outstanding = 0;            // jobs queued or being written
+  bool stop = false;
+  std::string writer_error;
+  std::thread writer;
+};
+
+namespace {
+
+void writer_loop(lc_store* s) {
+  for (;;) {
+    WriteJob job;
+    {
+      std::unique_lock<std::mutex> lk(s->mu);
+      s->cv.wait(lk, [&] { return s->stop || !s->queue.empty(); });
+      if (s->queue.empty()) return;
+      job = s->queue.front();
+      s->queue.pop_front();
+    }
+    std::string err;
+    const uint8_t* src = job.host_src;
+    if (job.slot >= 0) {
+      const hipError_t e = hipEventSynchronize(s->slot_events[job.slot]);
+      if (e != hipSuccess) err = std::string("device-to-host copy failed: ") + hipGetErrorString(e);
+      src = s->slots[job.slot];
+    }
+    if (err.empty() && job.len && !write_all(job.fd, src, job.len, job.file_off))
+      err = std::string("write failed: ") + std::strerror(errno);
+    if (job.last) {
+      std::unique_lock<std::mutex> lk(s->mu);
+      StoredVersion v = s->writing[job.version];
+      lk.unlock();
+      if (err.empty() && fsync(job.fd) != 0) err = std::string("fsync failed: ") + std::strerror(errno);
+      close(job.fd);
+      if (err.empty()) {
+        const std::string line = "LCV1 " + std::to_string(v.step) + " " + std::to_string(v.bytes) + " " + v.file +
+                                 " " + mask_string(v.mask) + "\n";
+        if (!write_all(s->manifest_fd, reinterpret_cast<const uint8_t*>(line.data()), line.size(),
+                       static_cast<uint64_t>(lseek(s->manifest_fd, 0, SEEK_END))) ||
+            fsync(s->manifest_fd) != 0)
+          err = std::string("manifest write failed: ") + std::strerror(errno);
+      }
+      lk.lock();
+      if (err.empty()) s->durable.push_back(v);
+    }
+    std::lock_guard<std::mutex> lk(s->mu);
+    if (!err.empty() && s->writer_error.empty()) s->writer_error = err;
+    if (job.slot >= 0) s->slot_free[job.slot] = 1;
+    --s->outstanding;
+    s->cv.notify_all();
+  }
+}
+
+lc_status parse_manifest(lc_store* s) {
+  std::string text;
+  {
+    char buf[1 << 16];
+    for (;;) {
+      const ssize_t r = read(s->manifest_fd, buf, sizeof(buf));
+      if (r < 0) {
+        if (errno == EINTR) continue;
+        return fail(LC_ERR_INVALID_ARG, "cannot read the manifest: %s", std::strerror(errno));
+      }
+      if (r == 0) break;
+      text.append(buf, static_cast<size_t>(r));
+    }
+  }
+  size_t pos = 0;
+  while (pos < text.size()) {
+    const size_t nl = text.find('\n', pos);
+    if (nl == std::string::npos) {  // torn last line: never durable, cut it off
+      ++s->skipped;
+      if (ftruncate(s->manifest_fd, static_cast<off_t>(pos)) != 0 || fsync(s->manifest_fd) != 0)
+        return fail(LC_ERR_INVALID_ARG, "cannot repair the manifest: %s", std::strerror(errno));
+      break;
+    }
+    const std::string line = text.substr(pos, nl - pos);
+    pos = nl + 1;
+    char tag[8] = {0}, file[256] = {0};
+    long long step = 0;
+    unsigned long long bytes = 0;
+    if (s->N > (1u << 20) ||
+        sscanf(line.c_str(), "%7s %lld %llu %255s", tag, &step, &bytes, file) != 4 || std::strcmp(tag, "LCV1")) {
+      ++s->skipped;
+      continue;
+    }
+    const size_t mp = line.rfind(' ');
+    const std::string ms = mp == std::string::npos ? "" : line.substr(mp + 1);
+    if (ms.size() != s->N) {
+      ++s->skipped;
+      continue;
+    }
+    StoredVersion v;
+    v.step = step;
+    v.bytes = bytes;
+    v.file = file;
+    v.mask.resize(s->N);
+    uint64_t need = 0;
+    bool ok = true;
+    for (uint32_t l = 0; l < s->N; ++l) {
+      if (ms[l] != '0' && ms[l] != '1') ok = false;
+      v.mask[l] = ms[l] == '1';
+      if (v.mask[l]) need += s->R[l];
+    }
+    struct stat sb;
+    const std::string path = s->dir + "/" + v.file;
+    if (!ok || need != v.bytes || stat(path.c_str(), &sb) != 0 || static_cast<uint64_t>(sb.st_size) != v.bytes) {
+      ++s->skipped;
+      continue;
+    }
+    unsigned long long q = 0;
+    if (sscanf(v.file.c_str(), "v%llu_", &q) == 1) s->seq = std::max<uint64_t>(s->seq, q + 1);
+    s->durable.push_back(v);
+  }
+  return LC_OK;
+}
+
+lc_status ensure_gpu(lc_store* s) {
+  if (s->gpu_ready) return LC_OK;
+  hipError_t e = hipStreamCreateWithFlags(&s->copy_stream, hipStreamNonBlocking);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->caller_ready, hipEventDisableTiming);
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->copies_done, hipEventDisableTiming);
+  if (e != hipSuccess) return fail(LC_ERR_HIP, "store stream setup failed: %s", hipGetErrorString(e));
+  for (uint32_t k = 0; k < s->n_slots; ++k) {
+    void* p = nullptr;
+    e = hipHostMalloc(&p, s->slot_bytes, hipHostMallocDefault);
+    if (e != hipSuccess) return fail(LC_ERR_OOM, "pinned drain buffer: %s", hipGetErrorString(e));
+    s->slots.push_back(static_cast<uint8_t*>(p));
+    hipEvent_t ev;
+    e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
+    if (e != hipSuccess) return fail(LC_ERR_HIP, "event create failed: %s", hipGetErrorString(e));
+    s->slot_events.push_back(ev);
+    s->slot_free.push_back(1);
+  }
+  s->gpu_ready = true;
+  return LC_OK;
+}
+
+// Per layer, the index of the durable version it is restored from (Section 3.5).
+lc_status plan_store(lc_store* s, int64_t t_fail, std::vector<size_t>& choice) {
+  choice.assign(s->N, 0);
+  for (uint32_t l = 0; l < s->N; ++l) {
+    long best = -1;
+    bool dup = false;
+    for (size_t i = 0; i < s->durable.size(); ++i) {
+      const StoredVersion& v = s->durable[i];
+      if (v.step > t_fail || !v.mask[l]) continue;
+      if (best < 0 || v.step > s->durable[best].step) {
+        best = static_cast<long>(i);
+        dup = false;
+      } else if (v.step == s->durable[best].step) {
+        dup = true;
+      }
+    }
+    if (best < 0)
+      return fail(LC_ERR_NO_VERSION, "layer %u: no persisted version at step <= %lld", l,
+                  static_cast<long long>(t_fail));
+    if (dup) return fail(LC_ERR_INVALID_ARG, "layer %u: two stored versions at one step", l);
+    choice[l] = static_cast<size_t>(best);
+  }
+  return LC_OK;
+}
+
+lc_status wait_idle(lc_store* s) {
+  std::unique_lock<std::mutex> lk(s->mu);
+  s->cv.wait(lk, [&] { return s->outstanding == 0; });
+  s->writing.clear();
+  if (!s->writer_error.empty()) return fail(LC_ERR_INVALID_ARG, "store: %s", s->writer_error.c_str());
+  return LC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* record_bytes, uint64_t buffer_bytes,
+                        lc_store** out) {
+  if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (!dir || !*dir || n_layers == 0 || !record_bytes) return fail(LC_ERR_INVALID_ARG, "bad store arguments");
+  for (uint32_t l = 0; l < n_layers; ++l)
+    if (record_bytes[l] == 0 || record_bytes[l] % kRecordAlign)
+      return fail(LC_ERR_INVALID_ARG, "record_bytes[%u] must be a positive multiple of %u", l, kRecordAlign);
+  if (mkdir(dir, 0755) != 0 && errno != EEXIST)
+    return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", dir, std::strerror(errno));
+  lc_store* s = new (std::nothrow) lc_store();
+  if (!s) return fail(LC_ERR_OOM, "host allocation failed");
+  s->dir = dir;
+  s->N = n_layers;
+  s->R.assign(record_bytes, record_bytes + n_layers);
+  s->slot_bytes = std::max<uint64_t>(buffer_bytes ? buffer_bytes : (256ull << 20), 1ull << 20);
+  s->slot_bytes = (s->slot_bytes + 4095) / 4096 * 4096;
+  s->n_slots = 4;
+  const std::string mpath = s->dir + "/manifest.lcm";
+  s->manifest_fd = open(mpath.c_str(), O_RDWR | O_CREAT, 0644);
+  if (s->manifest_fd < 0) {
+    delete s;
+    return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", mpath.c_str(), std::strerror(errno));
+  }
+  lc_status st = parse_manifest(s);
+  if (st != LC_OK) {
+    close(s->manifest_fd);
+    delete s;
+    return st;
+  }
+  s->writer = std::thread(writer_loop, s);
+  *out = s;
+  return LC_OK;
+}
+
+lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const void* payload, uint64_t bytes,
+                          void* stream) {
+  if (!s || !mask) return fail(LC_ERR_INVALID_ARG, "store and mask must be non-NULL");
+  StoredVersion v;
+  v.step = step;
+  v.bytes = bytes;
+  v.mask.assign(mask, mask + s->N);
+  uint64_t need = 0;
+  for (uint32_t l = 0; l < s->N; ++l) {
+    if (mask[l] > 1) return fail(LC_ERR_INVALID_ARG, "mask must be 0/1");
+    if (mask[l]) need += s->R[l];
+  }
+  if (need != bytes)
+    return fail(LC_ERR_INVALID_ARG, "payload_bytes %llu != %llu for the mask",
+                static_cast<unsigned long long>(bytes), static_cast<unsigned long long>(need));
+  if (bytes && !payload) return fail(LC_ERR_INVALID_ARG, "payload is NULL");
+  {
+    std::lock_guard<std::mutex> lk(s->mu);
+    if (!s->writer_error.empty()) return fail(LC_ERR_BAD_STATE, "store failed earlier: %s", s->writer_error.c_str());
+    for (const auto* list : {&s->durable, &s->writing})
+      for (const StoredVersion& o : *list)
+        if (o.step == step)
+          for (uint32_t l = 0; l < s->N; ++l)
+            if (o.mask[l] && mask[l]) return fail(LC_ERR_INVALID_ARG, "layer %u already stored at this step", l);
+  }
+  bool device = false;
+  if (bytes) {
+    hipPointerAttribute_t attr;
+    const hipError_t e = hipPointerGetAttributes(&attr, payload);
+    if (e == hipSuccess && attr.type == hipMemoryTypeDevice) device = true;
+    else (void)hipGetLastError();
+  }
+  char name[96];
+  snprintf(name, sizeof(name), "v%010llu_s%lld.lcr", static_cast<unsigned long long>(s->seq++),
+           static_cast<long long>(step));
+  v.file = name;
+  const std::string path = s->dir + "/" + v.file;
+  const int fd = open(path.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
+  if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", path.c_str(), std::strerror(errno));
+  size_t vi;
+  {
+    std::lock_guard<std::mutex> lk(s->mu);
+    vi = s->writing.size();
+    s->writing.push_back(v);
+  }
+  if (!device) {
+    // host payload (or empty): written from the caller's buffer before returning
+    WriteJob job;
+    job.fd = fd;
+    job.len = bytes;
+    job.host_src = static_cast<const uint8_t*>(payload);
+    job.last = true;
+    job.version = vi;
+    {
+      std::lock_guard<std::mutex> lk(s->mu);
+      s->queue.push_back(job);
+      ++s->outstanding;
+    }
+    s->cv.notify_all();
+    return wait_idle(s);
+  }
+  lc_status st = ensure_gpu(s);
+  if (st != LC_OK) {
+    close(fd);
+    return st;
+  }
+  hipStream_t cs = static_cast<hipStream_t>(stream);
+  hipError_t e = hipEventRecord(s->caller_ready, cs);
+  if (e == hipSuccess) e = hipStreamWaitEvent(s->copy_stream, s->caller_ready, 0);
+  if (e != hipSuccess) {
+    close(fd);
+    return fail(LC_ERR_HIP, "stream ordering failed: %s", hipGetErrorString(e));
+  }
+  const uint8_t* src = static_cast<const uint8_t*>(payload);
+  for (uint64_t off = 0; off < bytes; off += s->slot_bytes) {
+    const uint64_t len = std::min<uint64_t>(s->slot_bytes, bytes - off);
+    int slot = -1;
+    {
+      std::unique_lock<std::mutex> lk(s->mu);
+      s->cv.wait(lk, [&] {
+        if (!s->writer_error.empty()) return true;
+        for (uint32_t k = 0; k < s->n_slots; ++k)
+          if (s->slot_free[k]) return true;
+        return false;
+      });
+      if (!s->writer_error.empty()) return fail(LC_ERR_BAD_STATE, "store: %s", s->writer_error.c_str());
+      for (uint32_t k = 0; k < s->n_slots; ++k)
+        if (s->slot_free[k]) {
+          slot = static_cast<int>(k);
+          s->slot_free[k] = 0;
+          break;
+        }
+    }
+    e = hipMemcpyAsync(s->slots[slot], src + off, len, hipMemcpyDeviceToHost, s->copy_stream);
+    if (e == hipSuccess) e = hipEventRecord(s->slot_events[slot], s->copy_stream);
+    if (e != hipSuccess) return fail(LC_ERR_HIP, "drain copy failed: %s", hipGetErrorString(e));
+    WriteJob job;
+    job.fd = fd;
+    job.file_off = off;
+    job.len = len;
+    job.slot = slot;
+    job.last = off + len == bytes;
+    job.version = vi;
+    {
+      std::lock_guard<std::mutex> lk(s->mu);
+      s->queue.push_back(job);
+      ++s->outstanding;
+    }
+    s->cv.notify_all();
+  }
+  // the caller's later work (the next pack into the same staging) waits for the copies
+  e = hipEventRecord(s->copies_done, s->copy_stream);
+  if (e == hipSuccess) e = hipStreamWaitEvent(cs, s->copies_done, 0);
+  if (e != hipSuccess) return fail(LC_ERR_HIP, "stream ordering failed: %s", hipGetErrorString(e));
+  return LC_OK;
+}
+
+lc_status lc_store_sync(lc_store* s) {
+  if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
+  return wait_idle(s);
+}
+
+lc_status lc_store_count(lc_store* s, uint32_t* n_out) {
+  if (!s || !n_out) return fail(LC_ERR_INVALID_ARG, "bad arguments");
+  std::lock_guard<std::mutex> lk(s->mu);
+  *n_out = static_cast<uint32_t>(s->durable.size());
+  return LC_OK;
+}
+
+lc_status lc_store_entry(lc_store* s, uint32_t i, int64_t* step_out, uint8_t* mask_out, uint64_t* bytes_out) {
+  if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
+  std::lock_guard<std::mutex> lk(s->mu);
+  if (i >= s->durable.size()) return fail(LC_ERR_INVALID_ARG, "entry %u out of range", i);
+  const StoredVersion& v = s->durable[i];
+  if (step_out) *step_out = v.step;
+  if (mask_out) std::memcpy(mask_out, v.mask.data(), s->N);
+  if (bytes_out) *bytes_out = v.bytes;
+  return LC_OK;
+}
+
+lc_status lc_store_plan(lc_store* s, int64_t t_fail, int64_t* chosen_step_out) {
+  if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
+  lc_status st = wait_idle(s);
+  if (st != LC_OK) return st;
+  std::vector<size_t> choice;
+  st = plan_store(s, t_fail, choice);
+  if (st != LC_OK) return st;
+  if (chosen_step_out)
+    for (uint32_t l = 0; l < s->N; ++l) chosen_step_out[l] = s->durable[choice[l]].step;
+  return LC_OK;
+}
+
+lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chosen_step_out) {
+  if (!s || !c) return fail(LC_ERR_INVALID_ARG, "store and context must be non-NULL");
+  if (c->poisoned) return fail(LC_ERR_BAD_STATE, "context is poisoned by an earlier HIP error");
+  if (c->L.N != s->N || c->L.rec_bytes != s->R)
+    return fail(LC_ERR_INVALID_ARG, "the context's layout differs from the store's");
+  lc_status st = wait_idle(s);
+  if (st != LC_OK) return st;
+  std::vector<size_t> choice;
+  st = plan_store(s, t_fail, choice);
+  if (st != LC_OK) return st;
+  // offset of each layer's record inside its chosen version file
+  std::vector<uint64_t> off(s->N, 0);
+  for (uint32_t l = 0; l < s->N; ++l) {
+    const StoredVersion& v = s->durable[choice[l]];
+    uint64_t o = 0;
+    for (uint32_t j = 0; j < l; ++j)
+      if (v.mask[j]) o += s->R[j];
+    off[l] = o;
+  }
+  std::map<size_t, int> fds;
+  for (size_t i : choice) {
+    if (fds.count(i)) continue;
+    const std::string path = s->dir + "/" + s->durable[i].file;
+    const int fd = open(path.c_str(), O_RDONLY);
+    if (fd < 0) {
+      for (auto& kv : fds) close(kv.second);
+      return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", path.c_str(), std::strerror(errno));
+    }
+    fds[i] = fd;
+  }
+  // two pinned buffers: files are read into one while the GPU copies the other
+  const uint64_t max_rec = *std::max_element(s->R.begin(), s->R.end());
+  const uint64_t B = std::max<uint64_t>(max_rec, s->slot_bytes * s->n_slots);
+  uint8_t* buf[2] = {nullptr, nullptr};
+  hipEvent_t done[2] = {nullptr, nullptr};
+  auto cleanup = [&]() {
+    for (int k = 0; k < 2; ++k) {
+      if (done[k]) (void)hipEventSynchronize(done[k]), (void)hipEventDestroy(done[k]);
+      if (buf[k]) (void)hipHostFree(buf[k]);
+    }
+    for (auto& kv : fds) close(kv.second);
+  };
+  for (int k = 0; k < 2; ++k) {
+    void* p = nullptr;
+    hipError_t e = hipHostMalloc(&p, B, hipHostMallocDefault);
+    if (e != hipSuccess) {
+      cleanup();
+      return fail(LC_ERR_OOM, "pinned restore buffer: %s", hipGetErrorString(e));
+    }
+    buf[k] = static_cast<uint8_t*>(p);
+    e = hipEventCreateWithFlags(&done[k], hipEventDisableTiming);
+    if (e != hipSuccess) {
+      cleanup();
+      return fail(LC_ERR_HIP, "event create failed: %s", hipGetErrorString(e));
+    }
+  }
+  bool used[2] = {false, false};
+  uint32_t l = 0;
+  int k = 0;
+  while (l < s->N) {
+    uint32_t end = l;
+    uint64_t fill = 0;
+    while (end < s->N && fill + s->R[end] <= B) fill += s->R[end++];
+    if (used[k] && hipEventSynchronize(done[k]) != hipSuccess) {
+      cleanup();
+      c->poisoned = true;
+      return fail(LC_ERR_HIP, "restore copy failed");
+    }
+    // read the batch with a few threads, 64 MiB at a time
+    struct Piece { int fd; uint64_t src; uint8_t* dst; uint64_t len; };
+    std::vector<Piece> pieces;
+    uint64_t pos = 0;
+    for (uint32_t j = l; j < end; ++j) {
+      for (uint64_t o = 0; o < s->R[j]; o += (64ull << 20)) {
+        const uint64_t len = std::min<uint64_t>(64ull << 20, s->R[j] - o);
+        pieces.push_back({fds[choice[j]], off[j] + o, buf[k] + pos + o, len});
+      }
+      pos += s->R[j];
+    }
+    std::atomic<size_t> next{0};
+    std::atomic<bool> ok{true};
+    const unsigned nt = std::min<size_t>(8, pieces.size());
+    std::vector<std::thread> readers;
+    for (unsigned r = 0; r < nt; ++r)
+      readers.emplace_back([&] {
+        for (size_t i; (i = next.fetch_add(1)) < pieces.size();)
+          if (!read_all(pieces[i].fd, pieces[i].dst, pieces[i].len, pieces[i].src)) ok = false;
+      });
+    for (auto& th : readers) th.join();
+    if (!ok) {
+      cleanup();
+      return fail(LC_ERR_INVALID_ARG, "reading a stored record failed");
+    }
+    pos = 0;
+    for (uint32_t j = l; j < end; ++j) {
+      st = restore_layer_from_host(c, j, buf[k] + pos);
+      if (st != LC_OK) {
+        cleanup();
+        return st;
+      }
+      pos += s->R[j];
+    }
+    if (hipEventRecord(done[k], c->stream) != hipSuccess) {
+      cleanup();
+      c->poisoned = true;
+      return fail(LC_ERR_HIP, "event record failed");
+    }
+    used[k] = true;
+    l = end;
+    k ^= 1;
+  }
+  std::vector<int64_t> steps(s->N);
+  for (uint32_t j = 0; j < s->N; ++j) steps[j] = s->durable[choice[j]].step;
+  st = restore_finish(c, t_fail, steps);
+  cleanup();
+  if (st != LC_OK) return st;
+  if (chosen_step_out) std::memcpy(chosen_step_out, steps.data(), s->N * sizeof(int64_t));
+  return LC_OK;
+}
+
+lc_status lc_store_close(lc_store* s) {
+  if (!s) return LC_OK;
+  lc_status st = wait_idle(s);
+  {
+    std::lock_guard<std::mutex> lk(s->mu);
+    s->stop = true;
+  }
+  s->cv.notify_all();
+  if (s->writer.joinable()) s->writer.join();
+  if (s->gpu_ready) {
+    (void)hipStreamSynchronize(s->copy_stream);
+    for (uint8_t* p : s->slots) (void)hipHostFree(p);
+    for (hipEvent_t e : s->slot_events) (void)hipEventDestroy(e);
+    (void)hipEventDestroy(s->caller_ready);
+    (void)hipEventDestroy(s->copies_done);
+    (void)hipStreamDestroy(s->copy_stream);
+  }
+  if (s->manifest_fd >= 0) close(s->manifest_fd);
+  delete s;
+  return st;
+}
+
+}  // extern "C"

@@ -24,8 +24,9 @@ LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
-            "lc_restore_composite", "lc_adamw_step_score", "lc_read_state", "lc_record_bytes", "lc_destroy",
-            "lc_last_error")
+            "lc_restore_composite", "lc_adamw_step_score", "lc_store_open", "lc_store_append", "lc_store_sync",
+            "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore", "lc_store_close",
+            "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
 
 
 class lc_segment(C.Structure):
@@ -88,6 +89,15 @@ def load_library(path: str = LIB_PATH):
             "lc_restore_composite": (C.c_int, [C.c_void_p, P(lc_version), C.c_uint32, C.c_int64, P(C.c_int64)]),
             "lc_adamw_step_score": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_void_p), C.c_int32, P(C.c_uint8),
                                               P(lc_adamw_params)]),
+            "lc_store_open": (C.c_int, [C.c_char_p, C.c_uint32, P(C.c_uint64), C.c_uint64, P(C.c_void_p)]),
+            "lc_store_append": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint8), C.c_void_p, C.c_uint64,
+                                          C.c_void_p]),
+            "lc_store_sync": (C.c_int, [C.c_void_p]),
+            "lc_store_count": (C.c_int, [C.c_void_p, P(C.c_uint32)]),
+            "lc_store_entry": (C.c_int, [C.c_void_p, C.c_uint32, P(C.c_int64), P(C.c_uint8), P(C.c_uint64)]),
+            "lc_store_plan": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_int64)]),
+            "lc_store_restore": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, P(C.c_int64)]),
+            "lc_store_close": (C.c_int, [C.c_void_p]),
             "lc_read_state": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double), P(C.c_int64)]),
             "lc_record_bytes": (C.c_uint64, [C.c_void_p, C.c_uint32]),
             "lc_destroy": (C.c_int, [C.c_void_p]),
@@ -204,6 +214,55 @@ def lc_adamw_step_score(ctx, step: int, grads: Sequence[int], grad_dtype: int, l
         dm = dm_arr.ctypes.data_as(C.POINTER(C.c_uint8))
     prm = lc_adamw_params(lr, beta1, beta2, eps, weight_decay, adam_step)
     _check(load_library().lc_adamw_step_score(ctx, step, g, grad_dtype, dm, C.byref(prm)), "lc_adamw_step_score")
+
+
+class Store:
+    """Persistence store (a directory of version files and a manifest)."""
+
+    def __init__(self, directory: str, record_bytes: Sequence[int], buffer_bytes: int = 0):
+        self.n = len(record_bytes)
+        rb = (C.c_uint64 * self.n)(*[int(x) for x in record_bytes])
+        h = C.c_void_p()
+        _check(load_library().lc_store_open(os.fsencode(directory), self.n, rb, buffer_bytes, C.byref(h)),
+               "lc_store_open")
+        self.h = h
+
+    def append(self, step: int, mask, payload: int, payload_bytes: int, stream: int = 0) -> None:
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        _check(load_library().lc_store_append(self.h, step, m.ctypes.data_as(C.POINTER(C.c_uint8)), payload or None,
+                                              payload_bytes, stream or None), "lc_store_append")
+
+    def sync(self) -> None:
+        _check(load_library().lc_store_sync(self.h), "lc_store_sync")
+
+    def entries(self):
+        n = C.c_uint32()
+        _check(load_library().lc_store_count(self.h, C.byref(n)), "lc_store_count")
+        out = []
+        for i in range(n.value):
+            step, nbytes = C.c_int64(), C.c_uint64()
+            mask = np.zeros(self.n, dtype=np.uint8)
+            _check(load_library().lc_store_entry(self.h, i, C.byref(step), mask.ctypes.data_as(C.POINTER(C.c_uint8)),
+                                                 C.byref(nbytes)), "lc_store_entry")
+            out.append({"step": step.value, "mask": mask, "payload_bytes": nbytes.value})
+        return out
+
+    def plan(self, t_fail: int) -> np.ndarray:
+        out = np.zeros(self.n, dtype=np.int64)
+        _check(load_library().lc_store_plan(self.h, t_fail, out.ctypes.data_as(C.POINTER(C.c_int64))),
+               "lc_store_plan")
+        return out
+
+    def restore(self, ctx, t_fail: int) -> np.ndarray:
+        out = np.zeros(self.n, dtype=np.int64)
+        _check(load_library().lc_store_restore(self.h, ctx, t_fail, out.ctypes.data_as(C.POINTER(C.c_int64))),
+               "lc_store_restore")
+        return out
+
+    def close(self) -> None:
+        if self.h is not None:
+            h, self.h = self.h, None
+            _check(load_library().lc_store_close(h), "lc_store_close")
 
 
 def lc_read_state(ctx, n_layers: int):

@@ -1,0 +1,122 @@
+"""The persistence store on the CPU (host payloads): versions written as
+files plus an append-only manifest, read back after reopening, the
+reconstruction plan against the oracle's (Section 3.5), and crash
+consistency (torn or inconsistent manifest lines and files are ignored)."""
+import os
+
+import numpy as np
+import pytest
+
+from oracle import layercheck_oracle as O
+from paper_2609_27193_amd import layercheck as LC
+from tests._helpers import HostLayout
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(LC.LIB_PATH):
+        from paper_2609_27193_amd.build_lib import build
+        build()
+    return LC.load_library()
+
+
+def oracle_history(steps=8, seed=0):
+    """Payloads of an oracle run: the base at step 0, then every selection."""
+    sizes = [[300, 7], [64], [129, 3, 3], [1], [500]]
+    lay = HostLayout(sizes, seed=seed)
+    N = len(sizes)
+    orc = O.LayerCheckOracle(lay.segs, N, O.DT_BF16, True, O.MODE_ACCUM, [0.03] * N, s_max=3)
+    versions = [{"step": 0, "mask": np.ones(N, np.uint8), "payload": orc.pack(0, 1 << 40)[0]}]
+    for t in range(1, steps + 1):
+        lay.step([4.0, 0.3, 1.0, 0.02, 2.0])
+        orc.score(t)
+        mask, _ = orc.select(t, 1.0)
+        versions.append({"step": t, "mask": mask, "payload": orc.pack(0, 1 << 40)[0]})
+    return orc, versions
+
+
+def test_append_reopen_and_plan(lib, tmp_path):
+    orc, versions = oracle_history()
+    d = str(tmp_path / "store")
+    st = LC.Store(d, orc.R)
+    for v in versions:
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    st.sync()
+    st.close()
+    st = LC.Store(d, orc.R)  # reopen: the manifest is the persistence history
+    ent = st.entries()
+    assert [e["step"] for e in ent] == [v["step"] for v in versions]
+    for e, v in zip(ent, versions):
+        assert np.array_equal(e["mask"], v["mask"]) and e["payload_bytes"] == len(v["payload"])
+    files = sorted(f for f in os.listdir(d) if f.endswith(".lcr"))
+    for f, v in zip(files, versions):
+        assert open(os.path.join(d, f), "rb").read() == bytes(v["payload"])
+    for t_fail in range(0, 10):
+        expect = [versions[i]["step"] for i in O.plan_versions(versions, orc.N, t_fail)]
+        assert st.plan(t_fail).tolist() == expect
+    with pytest.raises(LC.LCError) as e:
+        st.plan(-1)
+    assert e.value.code == LC.LC_ERR_NO_VERSION
+    st.close()
+
+
+def test_append_validation(lib, tmp_path):
+    orc, versions = oracle_history(steps=2)
+    st = LC.Store(str(tmp_path / "s"), orc.R)
+    v = versions[1]
+    with pytest.raises(LC.LCError) as e:  # size does not match the mask
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data, len(v["payload"]) + 256)
+    assert e.value.code == LC.LC_ERR_INVALID_ARG
+    st.append(0, versions[0]["mask"], versions[0]["payload"].ctypes.data, len(versions[0]["payload"]))
+    with pytest.raises(LC.LCError):  # a layer twice at one step
+        st.append(0, versions[0]["mask"], versions[0]["payload"].ctypes.data, len(versions[0]["payload"]))
+    # disjoint masks at one step are fine (a selection packed in several calls)
+    m1 = np.zeros(orc.N, np.uint8)
+    m1[0] = 1
+    m2 = np.zeros(orc.N, np.uint8)
+    m2[2] = 1
+    p1 = np.zeros(orc.R[0], np.uint8)
+    p2 = np.zeros(orc.R[2], np.uint8)
+    st.append(5, m1, p1.ctypes.data, len(p1))
+    st.append(5, m2, p2.ctypes.data, len(p2))
+    assert st.plan(5).tolist() == [5, 0, 5, 0, 0]
+    st.close()
+    with pytest.raises(LC.LCError):
+        LC.Store(str(tmp_path / "bad"), [100, 256])  # record sizes are 256-byte multiples
+
+
+def test_crash_consistency(lib, tmp_path):
+    orc, versions = oracle_history(steps=4)
+    d = str(tmp_path / "c")
+    st = LC.Store(d, orc.R)
+    for v in versions:
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    st.close()
+    files = sorted(f for f in os.listdir(d) if f.endswith(".lcr"))
+    sized = [f for f, v in zip(files, versions) if len(v["payload"])]
+    # (1) a version whose file lost its tail is dropped
+    victim = sized[-1]
+    with open(os.path.join(d, victim), "r+b") as f:
+        f.truncate(os.path.getsize(os.path.join(d, victim)) - 256)
+    # (2) a garbage line, (3) a line for a file that does not exist,
+    # (4) a torn last line, (5) an orphan version file with no line
+    with open(os.path.join(d, "manifest.lcm"), "a") as f:
+        f.write("not a manifest line\n")
+        f.write("LCV1 9 256 v9999999999_s9.lcr " + "1" + "0" * (orc.N - 1) + "\n")
+        f.write("LCV1 10 25")
+    open(os.path.join(d, "v0000000777_s12.lcr"), "wb").write(b"\0" * 512)
+    st = LC.Store(d, orc.R)
+    kept = [e["step"] for e in st.entries()]
+    dropped = versions[files.index(victim)]["step"]
+    assert kept == [v["step"] for v in versions if v["step"] != dropped]
+    # the plan falls back past the lost version
+    survivors = [v for v in versions if v["step"] != dropped]
+    for t_fail in range(0, 5):
+        assert st.plan(t_fail).tolist() == [survivors[i]["step"] for i in O.plan_versions(survivors, orc.N, t_fail)]
+    # appends continue after the recovered history
+    v = versions[1]
+    st.append(20, v["mask"], v["payload"].ctypes.data, len(v["payload"]))
+    st.close()
+    st = LC.Store(d, orc.R)
+    assert st.entries()[-1]["step"] == 20
+    st.close()
