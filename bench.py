@@ -51,6 +51,9 @@ def parse():
                     help="also run one plain 4 GiB device copy (counter calibration)")
     ap.add_argument("--adamw", action="store_true",
                     help="drive the state with the fused AdamW + drift step instead of the standalone score")
+    ap.add_argument("--store-bench", default=None, metavar="DIR",
+                    help="measure draining packed records into a persistence store in DIR and restoring "
+                         "from it (default workload llama3.2-1b)")
     ap.add_argument("--k0", type=float, default=None,
                     help="base threshold (skips the calibration window)")
     ap.add_argument("--json-out", default=None)
@@ -165,6 +168,8 @@ def main():
     from paper_2609_27193_amd import inputs as I
     from paper_2609_27193_amd import layercheck as LC
 
+    if args.store_bench:
+        return main_store(args, I.WORKLOADS["llama3.2-1b" if args.workload == "llama3-8b" else args.workload]())
     spec = I.WORKLOADS[args.workload]()
     if args.adamw:
         return main_adamw(args, spec)
@@ -303,6 +308,104 @@ def main():
     if args.json_out:
         with open(args.json_out, "w") as f:
             f.write(line + "\n")
+
+
+def main_store(args, spec):
+    """Persistence path: drain the full base version (every layer) and the
+    selections of a few decision steps from device staging into a store
+    (pinned ring, writer threads, fsync), then restore the composite state
+    from the store.  Per step it times how long the staging buffer is held
+    (the device-to-host copies, against a plain pinned copy of the same size
+    as the host-link ceiling) and how long until the version is durable.
+    Rates are over the payload bytes; the restore reads files the same
+    process wrote, so they may come from the page cache."""
+    import shutil
+    import torch
+    from paper_2609_27193_amd import inputs as I
+    from paper_2609_27193_amd import layercheck as LC
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    LC.load_library()
+    state = I.SyntheticState(spec, device=dev)
+    segs = LC.segments_from_state(state)
+    dtype = LC.LC_DT_BF16 if spec.weight_dtype == "bf16" else LC.LC_DT_F32
+    k0 = [(args.k0 or 0.03) * (10.0 if l.name == "embed_tokens" else 1.0) for l in spec.layers]
+    layout = LC.LayoutDesc(segs, spec.n_layers, dtype, spec.has_master, LC.LC_MODE_ACCUM, k0, spec.s_max,
+                           stream=stream.cuda_stream)
+    _, rec = LC.lc_query_layout(layout)
+    total = sum(rec)
+    staging = torch.empty(total, dtype=torch.uint8, device=dev)
+    ctx = LC.lc_init_layout(layout)
+    ring = 4 << 30
+    # host-link ceiling: one plain device-to-pinned copy of the ring's size
+    pinned = torch.empty(ring, dtype=torch.uint8, pin_memory=True)
+    for _ in range(2):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        pinned.copy_(staging[:ring], non_blocking=True)
+        e1.record()
+        torch.cuda.synchronize()
+    link_gbs = ring / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    del pinned
+    log(f"[bench] host link: device-to-pinned copy of {ring / 2**30:.0f} GiB at {link_gbs:.1f} GB/s")
+    if os.path.exists(args.store_bench):
+        shutil.rmtree(args.store_bench)
+    store = LC.Store(args.store_bench, rec, buffer_bytes=ring)
+    res = LC.lc_pack_selected(ctx, staging.data_ptr(), total, 0)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    store.append(0, np.ones(spec.n_layers, np.uint8), staging.data_ptr(), res["bytes_written"], stream.cuda_stream)
+    t_append = time.perf_counter() - t0
+    store.sync()
+    t_base = time.perf_counter() - t0
+    log(f"[bench] base version {total / 1e9:.2f} GB: append returned after {t_append:.2f} s, durable after "
+        f"{t_base:.2f} s -> {total / t_base / 1e9:.2f} GB/s")
+    drained, release_s, durable_s, call_s = 0, 0.0, 0.0, 0.0
+    for t in range(1, 7):
+        state.step(t)
+        LC.lc_score_layers(ctx, t)
+        mask, st = LC.lc_select(ctx, t, 1.0, spec.n_layers)
+        r = LC.lc_pack_selected(ctx, staging.data_ptr(), total, 0)
+        torch.cuda.synchronize()
+        a = time.perf_counter()
+        store.append(t, mask, staging.data_ptr(), r["bytes_written"], stream.cuda_stream)
+        b = time.perf_counter()
+        stream.synchronize()  # the staging buffer is free again
+        c = time.perf_counter()
+        store.sync()
+        d = time.perf_counter()
+        call_s += b - a
+        release_s += c - a
+        durable_s += d - a
+        drained += r["bytes_written"]
+        log(f"[bench] t={t}: {st['n_selected']} layers, {r['bytes_written'] / 1e9:.2f} GB: append {b - a:.3f} s, "
+            f"staging free after {c - a:.3f} s, durable after {d - a:.3f} s")
+    # fail-stop: lose the live state, recover the composite from the store
+    for tnsr in (state.weight, state.shadow, state.master, state.exp_avg, state.exp_avg_sq):
+        if tnsr is not None:
+            tnsr.zero_()
+    torch.cuda.synchronize()
+    t_fail = 5
+    a = time.perf_counter()
+    chosen = store.restore(ctx, t_fail)
+    restore_s = time.perf_counter() - a
+    store.close()
+    LC.lc_destroy(ctx)
+    out = {"metric": "persistence store: drain and composite-restore GB/s", "unit": "GB/s",
+           "config": {"workload": f"{spec.name}-shaped state", "params": spec.numel, "layer_groups": spec.n_layers,
+                      "record_set_gb": round(total / 1e9, 3), "ring_gib": ring >> 30},
+           "host_link_gbs": round(link_gbs, 2),
+           "drain_base_gbs": round(total / t_base / 1e9, 3),
+           "steps_gb": round(drained / 1e9, 3),
+           "steps_append_call_s": round(call_s, 3),
+           "steps_staging_release_gbs": round(drained / release_s / 1e9, 2),
+           "steps_durable_gbs": round(drained / durable_s / 1e9, 3),
+           "restore_gbs": round(total / restore_s / 1e9, 3), "restore_s": round(restore_s, 3),
+           "restored_timestamps": sorted(set(int(x) for x in chosen))}
+    print(json.dumps(out), flush=True)
+    shutil.rmtree(args.store_bench, ignore_errors=True)
 
 
 ADAMW = dict(lr=1e-5, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)

@@ -221,13 +221,16 @@ lc_status lc_adamw_step_score(lc_ctx *c, int64_t step, const void *const *grads,
  * file is complete and fsync'ed and its manifest line ("LCV1 <step> <bytes>
  * <file> <mask as 0/1 characters>") is written and fsync'ed; on open, torn or
  * inconsistent lines and files of the wrong size are ignored.  A store is
- * used from one thread; it owns one writer thread. */
+ * used from one thread; it owns a small pool of writer threads, and versions
+ * become visible in the order they were appended. */
 typedef struct lc_store lc_store;
 
 /* Opens (creating the directory itself, not its parents) the store of a
  * layout with the given per-layer record sizes (lc_query_layout /
- * lc_record_bytes).  buffer_bytes sizes each of the four pinned drain buffers
- * (0: 256 MiB). */
+ * lc_record_bytes).  buffer_bytes is the size of the pinned drain ring
+ * (0: 1 GiB; at least 1 MiB), cut into slots of at most 64 MiB: a device
+ * payload that fits in it is copied out at host-link speed while the files
+ * are written behind it.  The ring is allocated on the first device append. */
 lc_status lc_store_open(const char *dir, uint32_t n_layers, const uint64_t *record_bytes, uint64_t buffer_bytes,
                         lc_store **out);
 
@@ -237,8 +240,8 @@ lc_status lc_store_open(const char *dir, uint32_t n_layers, const uint64_t *reco
  * pinned buffers on a store-owned stream that first waits for the work
  * already enqueued on `stream` (hipStream_t, NULL = null stream); `stream`
  * then waits for those copies, so later work on it may reuse the buffer.  The
- * call returns once every copy is enqueued (it blocks while the drain buffers
- * are full); the files are written by the writer thread.  Host payloads are
+ * call returns once every copy is enqueued (it blocks while the ring is full);
+ * the files are written by the writer threads.  Host payloads are
  * written before the call returns.  A layer may be stored at most once per
  * step (several versions of one step must have disjoint masks). */
 lc_status lc_store_append(lc_store *s, int64_t step, const uint8_t *mask, const void *payload,

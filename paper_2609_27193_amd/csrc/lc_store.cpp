@@ -6,9 +6,10 @@
 // append-only manifest.  A version becomes visible only after its file is
 // complete and fsync'ed and its manifest line is written and fsync'ed, so a
 // crash leaves at most an ignored partial file.  Device payloads are drained
-// through a ring of pinned host buffers on a store-owned stream; a writer
-// thread writes each buffer as soon as its copy completes, so the caller's
-// stream is released as soon as the staging buffer has been read.
+// through a ring of pinned host buffers on a store-owned stream; a small pool
+// of writer threads writes each buffer as soon as its copy completes, so the
+// caller's stream is released as soon as the staging buffer has been read.
+// Versions are made durable in the order they were appended.
 #include <fcntl.h>
 #include <sys/stat.h>
 #include <sys/types.h>
@@ -17,6 +18,7 @@
 #include <algorithm>
 #include <atomic>
 #include <cerrno>
+#include <cstdlib>
 #include <condition_variable>
 #include <cstring>
 #include <deque>
@@ -33,20 +35,27 @@ using namespace lc;
 
 namespace {
 
+constexpr int kWriters = 4;  // concurrent pwrite()s of drained buffers
+
 struct StoredVersion {
   int64_t step = 0;
   std::vector<uint8_t> mask;
   uint64_t bytes = 0;
   std::string file;
+  int fd = -1;              // open while being written
+  int dfd = -1;             // the same file opened for direct I/O, or -1
+  uint64_t remaining = 0;   // bytes not yet written (or abandoned)
+  bool enqueued_all = false;
+  bool failed = false;      // a write or the drain failed: the version is dropped
 };
 
 struct WriteJob {
   int fd = -1;
+  int dfd = -1;                    // direct-I/O descriptor for block-aligned parts, or -1
   uint64_t file_off = 0;
   uint64_t len = 0;
   int slot = -1;                   // pinned ring slot, or -1 for a caller host buffer
   const uint8_t* host_src = nullptr;
-  bool last = false;               // the version is complete after this job
   size_t version = 0;              // index into lc_store::writing
 };
 
@@ -62,6 +71,30 @@ bool write_all(int fd, const uint8_t* p, uint64_t n, uint64_t off) {
     off += static_cast<uint64_t>(w);
   }
   return true;
+}
+
+constexpr uint64_t kDirectBlock = 4096;  // O_DIRECT offset/length/address granule
+
+// Writes the block-aligned head of a buffer with direct I/O (the data goes
+// to the device, skipping the page cache) and the rest through the page
+// cache; falls back to buffered writes if the file system refuses direct I/O.
+bool write_slot(int fd, int dfd, const uint8_t* p, uint64_t n, uint64_t off) {
+  uint64_t head = dfd >= 0 && off % kDirectBlock == 0 && reinterpret_cast<uintptr_t>(p) % kDirectBlock == 0
+                      ? n / kDirectBlock * kDirectBlock
+                      : 0;
+  while (head > 0) {
+    const uint64_t piece = head > (1ull << 30) ? (1ull << 30) : head;
+    const ssize_t w = pwrite(dfd, p, piece, static_cast<off_t>(off));
+    if (w < 0 && errno == EINTR) continue;
+    if (w <= 0 || static_cast<uint64_t>(w) % kDirectBlock) {
+      if (w > 0) {
+        p += w, n -= static_cast<uint64_t>(w), off += static_cast<uint64_t>(w);
+      }
+      break;  // refused or short: the rest goes through the page cache
+    }
+    p += w, n -= static_cast<uint64_t>(w), off += static_cast<uint64_t>(w), head -= static_cast<uint64_t>(w);
+  }
+  return write_all(fd, p, n, off);
 }
 
 bool read_all(int fd, uint8_t* p, uint64_t n, uint64_t off) {
@@ -92,7 +125,9 @@ struct lc_store {
   uint32_t N = 0;
   std::vector<uint64_t> R;
   std::vector<StoredVersion> durable;  // visible versions, manifest order
-  std::vector<StoredVersion> writing;  // being written (indices stay valid until sync)
+  std::vector<StoredVersion> writing;  // being written, append order (indices stay valid until idle)
+  size_t next_final = 0;               // writing[] below this index are finalised
+  bool finalising = false;             // one thread at a time makes versions durable
   int manifest_fd = -1;
   uint64_t seq = 0;
   uint64_t skipped = 0;                // manifest lines ignored at open
@@ -111,53 +146,127 @@ struct lc_store {
   uint64_t outstanding = 0;            // jobs queued or being written
   bool stop = false;
   std::string writer_error;
-  std::thread writer;
+  std::vector<std::thread> writers;
 };
 
 namespace {
 
+// Makes a completed version durable: fsync its file, then append and fsync
+// its manifest line.
+std::string finalise(lc_store* s, const StoredVersion& v) {
+  std::string err;
+  if (v.dfd >= 0) close(v.dfd);
+  if (fsync(v.fd) != 0) err = std::string("fsync failed: ") + std::strerror(errno);
+  close(v.fd);
+  if (!err.empty()) return err;
+  const std::string line = "LCV1 " + std::to_string(v.step) + " " + std::to_string(v.bytes) + " " + v.file + " " +
+                           mask_string(v.mask) + "\n";
+  const off_t end = lseek(s->manifest_fd, 0, SEEK_END);
+  if (end < 0 ||
+      !write_all(s->manifest_fd, reinterpret_cast<const uint8_t*>(line.data()), line.size(),
+                 static_cast<uint64_t>(end)) ||
+      fsync(s->manifest_fd) != 0)
+    err = std::string("manifest write failed: ") + std::strerror(errno);
+  return err;
+}
+
+bool complete(const StoredVersion& v) { return v.enqueued_all && v.remaining == 0; }
+
+// Finalises complete versions in append order, so the manifest lists them in
+// the order they were appended.  Called with s->mu held; drops it around the
+// file system calls.  Only one thread finalises at a time; a version that
+// completes meanwhile is picked up by that thread's next check.
+void advance(lc_store* s, std::unique_lock<std::mutex>& lk) {
+  if (s->finalising) return;
+  s->finalising = true;
+  while (s->next_final < s->writing.size() && complete(s->writing[s->next_final])) {
+    const StoredVersion v = s->writing[s->next_final];
+    lk.unlock();
+    std::string err;
+    if (v.failed) {
+      close(v.fd);
+      if (v.dfd >= 0) close(v.dfd);
+    }
+    else err = finalise(s, v);
+    lk.lock();
+    if (!err.empty() && s->writer_error.empty()) s->writer_error = err;
+    if (err.empty() && !v.failed) s->durable.push_back(v);
+    s->writing[s->next_final].fd = -1;
+    ++s->next_final;
+  }
+  s->finalising = false;
+}
+
 void writer_loop(lc_store* s) {
+  // Direct I/O cannot read pinned (device-mapped) host memory, so each writer
+  // copies a drained slot into an ordinary page-aligned buffer of its own,
+  // frees the slot at once and writes from there.
+  uint8_t* bounce = nullptr;
   for (;;) {
     WriteJob job;
     {
       std::unique_lock<std::mutex> lk(s->mu);
       s->cv.wait(lk, [&] { return s->stop || !s->queue.empty(); });
-      if (s->queue.empty()) return;
+      if (s->queue.empty()) break;
       job = s->queue.front();
       s->queue.pop_front();
     }
     std::string err;
     const uint8_t* src = job.host_src;
-    if (job.slot >= 0) {
+    int dfd = -1;
+    bool slot_held = job.slot >= 0;
+    if (slot_held) {
       const hipError_t e = hipEventSynchronize(s->slot_events[job.slot]);
       if (e != hipSuccess) err = std::string("device-to-host copy failed: ") + hipGetErrorString(e);
       src = s->slots[job.slot];
-    }
-    if (err.empty() && job.len && !write_all(job.fd, src, job.len, job.file_off))
-      err = std::string("write failed: ") + std::strerror(errno);
-    if (job.last) {
-      std::unique_lock<std::mutex> lk(s->mu);
-      StoredVersion v = s->writing[job.version];
-      lk.unlock();
-      if (err.empty() && fsync(job.fd) != 0) err = std::string("fsync failed: ") + std::strerror(errno);
-      close(job.fd);
-      if (err.empty()) {
-        const std::string line = "LCV1 " + std::to_string(v.step) + " " + std::to_string(v.bytes) + " " + v.file +
-                                 " " + mask_string(v.mask) + "\n";
-        if (!write_all(s->manifest_fd, reinterpret_cast<const uint8_t*>(line.data()), line.size(),
-                       static_cast<uint64_t>(lseek(s->manifest_fd, 0, SEEK_END))) ||
-            fsync(s->manifest_fd) != 0)
-          err = std::string("manifest write failed: ") + std::strerror(errno);
+      if (err.empty() && job.dfd >= 0 && !bounce) {
+        void* p = nullptr;
+        if (posix_memalign(&p, kDirectBlock, s->slot_bytes) == 0) bounce = static_cast<uint8_t*>(p);
       }
-      lk.lock();
-      if (err.empty()) s->durable.push_back(v);
+      if (err.empty() && job.dfd >= 0 && bounce) {
+        std::memcpy(bounce, src, job.len);
+        src = bounce;
+        dfd = job.dfd;
+        {
+          std::lock_guard<std::mutex> lk(s->mu);
+          s->slot_free[job.slot] = 1;
+        }
+        s->cv.notify_all();
+        slot_held = false;
+      }
     }
-    std::lock_guard<std::mutex> lk(s->mu);
-    if (!err.empty() && s->writer_error.empty()) s->writer_error = err;
-    if (job.slot >= 0) s->slot_free[job.slot] = 1;
+    if (err.empty() && job.len && !write_slot(job.fd, dfd, src, job.len, job.file_off))
+      err = std::string("write failed: ") + std::strerror(errno);
+    std::unique_lock<std::mutex> lk(s->mu);
+    StoredVersion& w = s->writing[job.version];
+    w.remaining -= job.len;
+    if (!err.empty()) {
+      w.failed = true;
+      if (s->writer_error.empty()) s->writer_error = err;
+    }
+    if (slot_held) s->slot_free[job.slot] = 1;
+    advance(s, lk);
     --s->outstanding;
+    lk.unlock();
     s->cv.notify_all();
   }
+  free(bounce);
+}
+
+// An append that fails after registering its version: the bytes it did not
+// queue are written off and the version is dropped once its queued writes end.
+void abandon(lc_store* s, size_t vi, uint64_t unqueued, const char* why) {
+  std::unique_lock<std::mutex> lk(s->mu);
+  StoredVersion& w = s->writing[vi];
+  w.remaining -= unqueued;
+  w.enqueued_all = true;
+  w.failed = true;
+  if (s->writer_error.empty()) s->writer_error = why;
+  ++s->outstanding;  // the in-line advance below counts as a job
+  advance(s, lk);
+  --s->outstanding;
+  lk.unlock();
+  s->cv.notify_all();
 }
 
 lc_status parse_manifest(lc_store* s) {
@@ -272,8 +381,9 @@ lc_status plan_store(lc_store* s, int64_t t_fail, std::vector<size_t>& choice) {
 
 lc_status wait_idle(lc_store* s) {
   std::unique_lock<std::mutex> lk(s->mu);
-  s->cv.wait(lk, [&] { return s->outstanding == 0; });
+  s->cv.wait(lk, [&] { return s->outstanding == 0 && s->next_final == s->writing.size(); });
   s->writing.clear();
+  s->next_final = 0;
   if (!s->writer_error.empty()) return fail(LC_ERR_INVALID_ARG, "store: %s", s->writer_error.c_str());
   return LC_OK;
 }
@@ -297,9 +407,12 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
   s->dir = dir;
   s->N = n_layers;
   s->R.assign(record_bytes, record_bytes + n_layers);
-  s->slot_bytes = std::max<uint64_t>(buffer_bytes ? buffer_bytes : (256ull << 20), 1ull << 20);
+  // the ring: buffer_bytes of pinned memory in slots of at most 64 MiB, at
+  // least 2 per writer so copies run ahead of the writes
+  const uint64_t ring = std::max<uint64_t>(buffer_bytes ? buffer_bytes : (1ull << 30), 1ull << 20);
+  s->slot_bytes = std::min<uint64_t>(64ull << 20, ring / (2 * kWriters));
   s->slot_bytes = (s->slot_bytes + 4095) / 4096 * 4096;
-  s->n_slots = 4;
+  s->n_slots = static_cast<uint32_t>(std::max<uint64_t>(2 * kWriters, ring / s->slot_bytes));
   const std::string mpath = s->dir + "/manifest.lcm";
   s->manifest_fd = open(mpath.c_str(), O_RDWR | O_CREAT, 0644);
   if (s->manifest_fd < 0) {
@@ -312,7 +425,7 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
     delete s;
     return st;
   }
-  s->writer = std::thread(writer_loop, s);
+  for (int i = 0; i < kWriters; ++i) s->writers.emplace_back(writer_loop, s);
   *out = s;
   return LC_OK;
 }
@@ -357,37 +470,48 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
   const int fd = open(path.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
   if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", path.c_str(), std::strerror(errno));
   size_t vi;
+  v.fd = fd;
+  // device payloads leave the pinned ring by direct I/O where the file system allows it
+  v.dfd = device ? open(path.c_str(), O_WRONLY | O_DIRECT) : -1;
+  v.remaining = bytes;
+  v.enqueued_all = !device;
   {
     std::lock_guard<std::mutex> lk(s->mu);
     vi = s->writing.size();
     s->writing.push_back(v);
   }
   if (!device) {
-    // host payload (or empty): written from the caller's buffer before returning
-    WriteJob job;
-    job.fd = fd;
-    job.len = bytes;
-    job.host_src = static_cast<const uint8_t*>(payload);
-    job.last = true;
-    job.version = vi;
+    // host payload (or empty): written from the caller's buffer, in pieces
+    // the writers share, before returning
+    constexpr uint64_t kPiece = 64ull << 20;
     {
       std::lock_guard<std::mutex> lk(s->mu);
-      s->queue.push_back(job);
-      ++s->outstanding;
+      uint64_t off = 0;
+      do {
+        WriteJob job;
+        job.fd = fd;
+        job.file_off = off;
+        job.len = std::min<uint64_t>(kPiece, bytes - off);
+        job.host_src = static_cast<const uint8_t*>(payload) + off;
+        job.version = vi;
+        s->queue.push_back(job);
+        ++s->outstanding;
+        off += job.len;
+      } while (off < bytes);
     }
     s->cv.notify_all();
     return wait_idle(s);
   }
   lc_status st = ensure_gpu(s);
   if (st != LC_OK) {
-    close(fd);
+    abandon(s, vi, bytes, "drain buffers could not be set up");
     return st;
   }
   hipStream_t cs = static_cast<hipStream_t>(stream);
   hipError_t e = hipEventRecord(s->caller_ready, cs);
   if (e == hipSuccess) e = hipStreamWaitEvent(s->copy_stream, s->caller_ready, 0);
   if (e != hipSuccess) {
-    close(fd);
+    abandon(s, vi, bytes, "stream ordering failed");
     return fail(LC_ERR_HIP, "stream ordering failed: %s", hipGetErrorString(e));
   }
   const uint8_t* src = static_cast<const uint8_t*>(payload);
@@ -402,7 +526,12 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
           if (s->slot_free[k]) return true;
         return false;
       });
-      if (!s->writer_error.empty()) return fail(LC_ERR_BAD_STATE, "store: %s", s->writer_error.c_str());
+      if (!s->writer_error.empty()) {
+        const std::string why = s->writer_error;
+        lk.unlock();
+        abandon(s, vi, bytes - off, why.c_str());
+        return fail(LC_ERR_BAD_STATE, "store: %s", why.c_str());
+      }
       for (uint32_t k = 0; k < s->n_slots; ++k)
         if (s->slot_free[k]) {
           slot = static_cast<int>(k);
@@ -412,16 +541,20 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
     }
     e = hipMemcpyAsync(s->slots[slot], src + off, len, hipMemcpyDeviceToHost, s->copy_stream);
     if (e == hipSuccess) e = hipEventRecord(s->slot_events[slot], s->copy_stream);
-    if (e != hipSuccess) return fail(LC_ERR_HIP, "drain copy failed: %s", hipGetErrorString(e));
+    if (e != hipSuccess) {
+      abandon(s, vi, bytes - off, "drain copy failed");
+      return fail(LC_ERR_HIP, "drain copy failed: %s", hipGetErrorString(e));
+    }
     WriteJob job;
     job.fd = fd;
+    job.dfd = v.dfd;
     job.file_off = off;
     job.len = len;
     job.slot = slot;
-    job.last = off + len == bytes;
     job.version = vi;
     {
       std::lock_guard<std::mutex> lk(s->mu);
+      if (off + len == bytes) s->writing[vi].enqueued_all = true;
       s->queue.push_back(job);
       ++s->outstanding;
     }
@@ -501,7 +634,7 @@ lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chos
   }
   // two pinned buffers: files are read into one while the GPU copies the other
   const uint64_t max_rec = *std::max_element(s->R.begin(), s->R.end());
-  const uint64_t B = std::max<uint64_t>(max_rec, s->slot_bytes * s->n_slots);
+  const uint64_t B = std::max<uint64_t>(max_rec, std::min<uint64_t>(s->slot_bytes * s->n_slots, 1ull << 30));
   uint8_t* buf[2] = {nullptr, nullptr};
   hipEvent_t done[2] = {nullptr, nullptr};
   auto cleanup = [&]() {
@@ -597,7 +730,8 @@ lc_status lc_store_close(lc_store* s) {
     s->stop = true;
   }
   s->cv.notify_all();
-  if (s->writer.joinable()) s->writer.join();
+  for (auto& w : s->writers)
+    if (w.joinable()) w.join();
   if (s->gpu_ready) {
     (void)hipStreamSynchronize(s->copy_stream);
     for (uint8_t* p : s->slots) (void)hipHostFree(p);

@@ -195,6 +195,17 @@ def llama3_70b_shard_spec(world: int = 8, rank: int = 0) -> ModelSpec:
         description="one 1/8 ZeRO-3 shard of a Llama-3-70B-shaped state, S_max=10")
 
 
+def llama32_1b_spec() -> ModelSpec:
+    """Llama-3.2-1B shape (tied lm_head: N = 18, as in the paper's Table 1),
+    used for the persistence-store measurement, whose whole record set
+    (17.3 GB) fits a local disk."""
+    return ModelSpec(
+        name="llama-3.2-1b", weight_dtype="bf16", has_master=True,
+        layers=_decoder_layers(2048, 8192, 16, 128256, 32, 8, tied=True),
+        scale_rule="loguniform_2dec_embed0.1", target_fraction=0.20, s_max=8,
+        description="Llama-3.2-1B-shaped state (tied embeddings), bf16 W + fp32 master/m/v")
+
+
 def _full_70b_layers():
     return _decoder_layers(8192, 28672, 80, 128256, 64, 8)
 
@@ -217,6 +228,7 @@ WORKLOADS = {
     "llama2-13b": llama2_13b_spec,
     "qwen2.5-14b": qwen25_14b_spec,
     "llama3-70b-shard0": llama3_70b_shard_spec,
+    "llama3.2-1b": llama32_1b_spec,
 }
 
 # ----------------------------------------------------------------------------

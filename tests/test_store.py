@@ -120,3 +120,25 @@ def test_crash_consistency(lib, tmp_path):
     st = LC.Store(d, orc.R)
     assert st.entries()[-1]["step"] == 20
     st.close()
+
+
+def test_large_host_payload_in_pieces(lib, tmp_path):
+    """A host payload larger than one write piece is split over the writer
+    threads; the file must hold it byte for byte, and versions appended one
+    after another keep their order in the manifest."""
+    R = [72 << 20, 256, 8 << 20]
+    rng = np.random.default_rng(7)
+    payload = rng.integers(0, 256, sum(R), dtype=np.uint8)
+    d = str(tmp_path / "big")
+    st = LC.Store(d, R)
+    st.append(0, np.ones(3, np.uint8), payload.ctypes.data, payload.nbytes)
+    part = payload[R[0]:R[0] + R[1] + R[2]]
+    st.append(1, np.array([0, 1, 1], np.uint8), part.ctypes.data, part.nbytes)
+    st.close()
+    st = LC.Store(d, R)
+    assert [e["step"] for e in st.entries()] == [0, 1]
+    assert st.plan(1).tolist() == [0, 1, 1]
+    st.close()
+    files = sorted(f for f in os.listdir(d) if f.endswith(".lcr"))
+    assert np.array_equal(np.fromfile(os.path.join(d, files[0]), np.uint8), payload)
+    assert np.array_equal(np.fromfile(os.path.join(d, files[1]), np.uint8), part)
