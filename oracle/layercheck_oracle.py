@@ -20,6 +20,9 @@ What it computes, in the paper's notation:
 * Section 3.3 staleness guard: persist l also when t - t_l >= S_max.
 * Eq. 4: a persisted layer gets Delta_l <- 0 and t_l <- t.
 * Section 3.3 reporting metric: size-weighted staleness sum_l n_l (t - t_l) / sum_l n_l.
+* Section 3.4 warm-up: no selective persistence during the warm-up window,
+  then a full base checkpoint, after which every layer counts as persisted
+  at the base step (``rebase``).
 * Section 3.1 / Eq. 8 recovery: each layer takes its newest persisted record
   with step <= t_fail; the base full checkpoint is simply a version holding
   every layer.
@@ -346,6 +349,28 @@ class LayerCheckOracle:
         self.mask_step = step
         self.unpacked = {l for l in range(self.N) if mask[l]}
         return mask.copy(), self.stats(step, mask, n_forced)
+
+    # -- Section 3.4 warm-up and base checkpoint ------------------------------
+    def rebase(self, step: int) -> None:
+        """A full base checkpoint at ``step``: the end of the warm-up window
+        during which selective persistence is off, or any later full
+        checkpoint.  Every layer counts as persisted at ``step`` (Delta_l = 0,
+        t_l = step, S = W) and every layer is selected for packing; any
+        selection still pending is replaced.  ``step`` may equal the last
+        optimizer or score step (the rebase follows that step's update)."""
+        if step < self.last_step:
+            raise OracleError(LC_ERR_BAD_STATE, "a base checkpoint cannot precede the last step")
+        for l, g in enumerate(self.by_layer):
+            self.delta[l] = 0.0
+            self.t_last[l] = step
+            for s in g:
+                if s.shadow is not None:
+                    s.shadow[...] = s.weight
+        self.last_step = step
+        self.scored_step = None
+        self.mask = np.ones(self.N, dtype=np.uint8)
+        self.mask_step = step
+        self.unpacked = set(range(self.N))
 
     def stats(self, step: int, mask: np.ndarray, n_forced: int) -> dict:
         ages = [step - self.t_last[l] for l in range(self.N)]

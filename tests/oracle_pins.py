@@ -20,6 +20,8 @@ invariants and the paper's Table 1 figures):
 * Records: 14 bytes per parameter for bf16 + fp32 master + m + v (Section 4.1
   with Table 1); padded blocks hold the raw bytes in order.
 * Recovery: newest version <= t_fail per layer; round trip is bit-exact.
+* Section 3.4 base checkpoint: a rebase resets Delta, t_l and the shadow and
+  selects every layer.
 """
 from __future__ import annotations
 
@@ -218,6 +220,50 @@ def check_k0_extremes(cls):
         assert mask.tolist() == [t % 2 == 0] * 3
         assert st["n_forced"] == (3 if t % 2 == 0 else 0)
         orc.pack(0, 1 << 40)
+
+
+def check_rebase(cls, mode=O.MODE_ACCUM):
+    # Section 3.4: a full base checkpoint at the end of the warm-up window.
+    # (1) It resets Delta and t_l: u(1) = 2^-7 exactly, then the rebase at
+    # step 1; at step 2, u(2) = 2^-8 / (0.5 + 2^-8) < K0 = 1.5 * 2^-7, which
+    # only a reset keeps below K in ACCUM mode; W then stays put.  Both layers
+    # are forced S_max = 3 steps after the rebase, not after the old base.
+    segs = _const_layout(2)
+    orc = cls(segs, 2, O.DT_F32, True, mode, [1.5 * 2.0 ** -7, 1e300], s_max=3, eps_w=0.0)
+    orc.pack(0, 1 << 30)
+    for s in segs:
+        s.weight[...] = 0.5 + 2.0 ** -8
+    orc.score(1)  # warm-up: scored, no selection
+    assert orc.delta == [2.0 ** -7] * 2
+    orc.rebase(1)
+    expect_error(lambda: orc.select(1, 1.0), O.LC_ERR_BAD_STATE)  # the rebase is the decision
+    payload, res = orc.pack(0, 1 << 30)
+    assert res["n_packed"] == 2 and res["bytes_written"] == sum(orc.R)
+    assert bytes(payload) == orc.layer_record(0) + orc.layer_record(1)
+    expect_error(lambda: orc.rebase(0), O.LC_ERR_BAD_STATE)  # before the last step
+    for s in segs:
+        s.weight[...] = 0.5 + 2 * 2.0 ** -8
+    for t in (2, 3, 4):
+        orc.score(t)
+        mask, st = orc.select(t, 1.0)
+        assert mask.tolist() == [int(t == 4)] * 2, (mode, t, mask)
+        assert st["max_age"] == (0 if t == 4 else t - 1) and st["n_forced"] == (2 if t == 4 else 0)
+        orc.pack(0, 1 << 30)
+    # (2) It re-synchronises the shadow: W moves at steps 1 and 2 with no
+    # score (a warm-up that does not score), rebase at 2; the score at 3 must
+    # measure one step, 2^-8 / (0.5 + 2^-7) < K0, not three.
+    segs = _const_layout(1)
+    orc = cls(segs, 1, O.DT_F32, True, mode, [1.5 * 2.0 ** -7], s_max=100, eps_w=0.0)
+    orc.pack(0, 1 << 30)
+    for t in (1, 2):
+        segs[0].weight[...] = 0.5 + t * 2.0 ** -8
+    orc.rebase(2)
+    orc.pack(0, 1 << 30)
+    segs[0].weight[...] = 0.5 + 3 * 2.0 ** -8
+    orc.score(3)
+    assert orc.u[0] == (2.0 ** -8) / (0.5 + 2.0 ** -7)
+    mask, _ = orc.select(3, 1.0)
+    assert mask.tolist() == [0]
 
 
 def check_stats_invariants(cls, mode=O.MODE_ACCUM):

@@ -44,6 +44,12 @@ MUTANTS = {
                                  "            self.delta[l] = 0.0"),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
+    "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
+                           "            self.t_last[l] = step\n            for s in g:"),
+    "rebase_keeps_timestamps": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
+                                "            self.delta[l] = 0.0\n            for s in g:"),
+    "rebase_keeps_shadow": ("                if s.shadow is not None:\n                    s.shadow[...] = s.weight",
+                            "                pass"),
     "capacity_off_by_record": ("total + self.R[sel[last]] <= capacity", "total + self.R[sel[last]] < capacity"),
     "adamw_no_bias_correction": ('"c1": f(1.0 / (1.0 - beta1 ** t)), "c2": f(1.0 / (1.0 - beta2 ** t)),',
                                  '"c1": f(1.0), "c2": f(1.0),'),
@@ -81,6 +87,7 @@ def all_checks(M):
         yield lambda mode=mode: P.check_staleness_period(cls, mode)
         yield lambda mode=mode: P.check_stats_invariants(cls, mode)
         yield lambda mode=mode: P.check_restore_roundtrip(cls, mode)
+        yield lambda mode=mode: P.check_rebase(cls, mode)
     yield lambda: M.record_bytes([128], 2, True) == 14 * 128 or (_ for _ in ()).throw(AssertionError())
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
         yield lambda mode=mode: run_bruteforce(M, mode, O.DT_BF16, 0, steps=12)

@@ -29,6 +29,11 @@ def test_staleness_period(mode):
 
 
 @pytest.mark.parametrize("mode", [O.MODE_ACCUM, O.MODE_SNAPSHOT])
+def test_rebase(mode):
+    P.check_rebase(O.LayerCheckOracle, mode)
+
+
+@pytest.mark.parametrize("mode", [O.MODE_ACCUM, O.MODE_SNAPSHOT])
 def test_stats_invariants(mode):
     P.check_stats_invariants(O.LayerCheckOracle, mode)
 
