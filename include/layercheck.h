@@ -192,6 +192,18 @@ typedef struct {
   int64_t adam_step;   /* bias-correction step count t >= 1                    */
 } lc_adamw_params;
 
+/* Full base checkpoint at `step` (Section 3.4: selective persistence stays
+ * off during the warm-up window, which ends with a full checkpoint that is
+ * the fallback for rarely updated layers).  Every layer counts as persisted
+ * at `step`: Delta_l = 0, t_l = step, S <- W when the layout has a shadow.
+ * Every layer is selected, as after lc_select, for lc_pack_selected to pack
+ * (any selection still pending is dropped).  `step` must not precede the
+ * last scored, optimizer or restore step; it may equal it (the warm-up's last
+ * optimizer step, then its base).  Warm-up steps before it call
+ * lc_adamw_step_score (or nothing) and skip lc_select.  Synchronises the
+ * stream.  LC_ERR_BAD_STATE for an earlier step or a poisoned context. */
+lc_status lc_rebase(lc_ctx *c, int64_t step);
+
 /* The optimizer step with the drift taken from the update itself (Section 3.4,
  * "Reusing the optimizer update to compute drift"; AdamW as trained in
  * Section 4.1).  For every element, in fp32 with one rounding per operation:

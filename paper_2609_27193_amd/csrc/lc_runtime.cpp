@@ -617,6 +617,33 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
   return LC_OK;
 }
 
+lc_status lc_rebase(lc_ctx* c, int64_t step) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (step < c->last_step)
+    return fail(LC_ERR_BAD_STATE, "the base step %lld precedes the last step %lld", static_cast<long long>(step),
+                static_cast<long long>(c->last_step));
+  const uint32_t N = c->L.N;
+  std::vector<double> zeros(N, 0.0);
+  std::vector<int64_t> tl(N, step);
+  st = upload(c, c->dt.delta, zeros);
+  if (st != LC_OK) return st;
+  st = upload(c, c->dt.t_last, tl);
+  if (st != LC_OK) return st;
+  for (const lc_segment& sg : c->L.segs) {
+    if (!c->L.has_shadow) break;
+    LC_HIP(c, hipMemcpyAsync(sg.shadow, sg.weight, sg.numel * c->L.esz, hipMemcpyDeviceToDevice, c->stream));
+  }
+  c->shadow_valid = c->L.has_shadow;
+  st = enqueue_select(c, step, 1.0, 1);
+  if (st != LC_OK) return st;
+  // the uploads read host vectors that end with this call
+  LC_HIP(c, hipStreamSynchronize(c->stream));
+  c->last_step = step;
+  c->scored = false;
+  return LC_OK;
+}
+
 lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
                               const uint8_t* decay_mask, const lc_adamw_params* p) {
   lc_status st = check_ctx(c);

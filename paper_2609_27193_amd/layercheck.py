@@ -24,7 +24,7 @@ LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
-            "lc_restore_composite", "lc_adamw_step_score", "lc_store_open", "lc_store_append", "lc_store_sync",
+            "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_store_open", "lc_store_append", "lc_store_sync",
             "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore", "lc_store_close",
             "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
 
@@ -87,6 +87,7 @@ def load_library(path: str = LIB_PATH):
             "lc_select": (C.c_int, [C.c_void_p, C.c_int64, C.c_double, P(C.c_uint8), P(lc_select_stats)]),
             "lc_pack_selected": (C.c_int, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint32, P(lc_pack_result)]),
             "lc_restore_composite": (C.c_int, [C.c_void_p, P(lc_version), C.c_uint32, C.c_int64, P(C.c_int64)]),
+            "lc_rebase": (C.c_int, [C.c_void_p, C.c_int64]),
             "lc_adamw_step_score": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_void_p), C.c_int32, P(C.c_uint8),
                                               P(lc_adamw_params)]),
             "lc_store_open": (C.c_int, [C.c_char_p, C.c_uint32, P(C.c_uint64), C.c_uint64, P(C.c_void_p)]),
@@ -201,6 +202,10 @@ def lc_restore_composite(ctx, versions: Sequence[dict], t_fail: int, n_layers: i
                                                chosen.ctypes.data_as(C.POINTER(C.c_int64))),
            "lc_restore_composite")
     return chosen
+
+
+def lc_rebase(ctx, step: int) -> None:
+    _check(load_library().lc_rebase(ctx, step), "lc_rebase")
 
 
 def lc_adamw_step_score(ctx, step: int, grads: Sequence[int], grad_dtype: int, lr: float, beta1: float,

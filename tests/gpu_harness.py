@@ -207,10 +207,19 @@ class Pair:
         if g.master is not None:
             g.master.copy_(torch.from_numpy(self.hM))
 
+    def rebase(self, t):
+        """A full base checkpoint at t on both sides (every layer selected)."""
+        LC.lc_rebase(self.ctx, t)
+        self.orc.rebase(t)
+        u, d, tl = LC.lc_read_state(self.ctx, self.N)
+        assert not d.any() and tl.tolist() == [t] * self.N == list(self.orc.t_last)
+        self.check_arrays()
+        return np.ones(self.N, np.uint8)
+
     def fused_step(self, t, adam_t, lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, wd=0.01, grad_dtype="bf16",
-                   lr_scale=1.0, capacity=None):
+                   lr_scale=1.0, capacity=None, decide=True):
         """One AdamW step with the drift taken from the update, on both sides,
-        then select and pack."""
+        then (with ``decide``) select and pack."""
         torch = self.torch
         gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
         g = self.gen.gradients(t, gdt)
@@ -226,6 +235,8 @@ class Pair:
         assert rel_ok(u, self.orc.u), (t, u, self.orc.u)
         assert rel_ok(d, self.orc.delta), (t, d, self.orc.delta)
         self.check_arrays()  # optimizer state and weights bit-exact
+        if not decide:
+            return None, None
         mask, st = self.select(t, lr_scale, d, tl)
         self.pack(t, mask, capacity)
         return mask, st
