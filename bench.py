@@ -67,16 +67,28 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def measured_traffic(workload: str, mode: str):
-    """HBM bytes per score launch from committed rocprofv3 counter runs, only
-    if they were taken on the current kernel source."""
-    path = os.path.join(ROOT, "profiles", f"score_kernel_{workload}_{mode}_pmc.json")
+def measured_traffic(kernel: str, workload: str, mode: str):
+    """HBM bytes per launch of ``kernel`` from committed rocprofv3 counter
+    runs, only if they were taken on the current kernel source."""
+    path = os.path.join(ROOT, "profiles", f"{kernel}_{workload}_{mode}_pmc.json")
     if not os.path.exists(path):
         return None
     d = json.load(open(path))
     if d.get("kernel_source_hash") != kernel_source_hash():
         return None
     return d.get("hbm_bytes_per_launch")
+
+
+def copy_calibration(dev):
+    """One plain 4 GiB device-to-device copy, for scaling the HBM byte
+    counters of a profiling run."""
+    import torch
+    a_ = torch.empty(1 << 30, dtype=torch.float32, device=dev)
+    b_ = torch.empty_like(a_)
+    a_.fill_(1.0)
+    b_.copy_(a_)
+    torch.cuda.synchronize()
+    del a_, b_
 
 
 def calibrate_k0(u_hist: np.ndarray, embed_mask: np.ndarray, s_max: int, target: float) -> float:
@@ -229,12 +241,7 @@ def main():
     opt_b = 4 * (3 if spec.has_master else 2)
 
     if args.copy_calibration:
-        a_ = torch.empty(1 << 30, dtype=torch.float32, device=dev)
-        b_ = torch.empty_like(a_)
-        a_.fill_(1.0)
-        b_.copy_(a_)
-        torch.cuda.synchronize()
-        del a_, b_
+        copy_calibration(dev)
 
     rows = []
     for i in range(warmup + steps):
@@ -280,7 +287,7 @@ def main():
     pack_rows = [r for r in rows if r["pack_bytes"]]
     pack_gbs = (sum(r["pack_bytes"] for r in pack_rows) / sum(r["pack_ms"] for r in pack_rows) / 1e6
                 if pack_rows else None)
-    traffic = measured_traffic(args.workload, args.mode)
+    traffic = measured_traffic("score_kernel", args.workload, args.mode)
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "GB/s", "n_gpus": 1,
         "steps": steps, "warmup": warmup, "ms_per_step": round(tot_ms / len(rows), 4),
@@ -475,6 +482,8 @@ def main_adamw(args, spec):
     # grad (bf16) read, master/m/v read+write, weights written (and read when they are the parameters)
     opt_bytes = P * (2 + (8 if spec.has_master else 0) + 16 + (w if spec.has_master else 2 * w)) + 32 * n_chunks
     opt_b = 4 * (3 if spec.has_master else 2)
+    if args.copy_calibration:
+        copy_calibration(dev)
     rows = []
     for i in range(warmup + steps):
         t += 1
@@ -522,7 +531,8 @@ def main_adamw(args, spec):
                    "k0_base": k0_base, "opt_bytes_per_step_gb": round(opt_bytes / 1e9, 3)},
         "roofline": {"bound": "hbm", "kernel": "adamw_kernel (+finalize)",
                      "achieved": round(opt_bytes / opt_ms / 1e6, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": round(opt_bytes / opt_ms / 1e6 / HBM_PEAK_GBS, 4), "traffic": None},
+                     "frac": round(opt_bytes / opt_ms / 1e6 / HBM_PEAK_GBS, 4),
+                     "traffic": measured_traffic("adamw_kernel", args.workload, "accum")},
     }
     line = json.dumps(out)
     print(line, flush=True)
