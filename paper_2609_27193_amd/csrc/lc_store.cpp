@@ -542,6 +542,10 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
     e = hipMemcpyAsync(s->slots[slot], src + off, len, hipMemcpyDeviceToHost, s->copy_stream);
     if (e == hipSuccess) e = hipEventRecord(s->slot_events[slot], s->copy_stream);
     if (e != hipSuccess) {
+      {
+        std::lock_guard<std::mutex> lk(s->mu);
+        s->slot_free[slot] = 1;  // nothing was queued on it
+      }
       abandon(s, vi, bytes - off, "drain copy failed");
       return fail(LC_ERR_HIP, "drain copy failed: %s", hipGetErrorString(e));
     }
