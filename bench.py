@@ -54,6 +54,9 @@ def parse():
     ap.add_argument("--store-bench", default=None, metavar="DIR",
                     help="measure draining packed records into a persistence store in DIR and restoring "
                          "from it (default workload llama3.2-1b)")
+    ap.add_argument("--restore-bench", action="store_true",
+                    help="measure the composite restore from device-resident and from pinned-host versions "
+                         "(default workload llama3.2-1b)")
     ap.add_argument("--k0", type=float, default=None,
                     help="base threshold (skips the calibration window)")
     ap.add_argument("--json-out", default=None)
@@ -182,6 +185,8 @@ def main():
 
     if args.store_bench:
         return main_store(args, I.WORKLOADS["llama3.2-1b" if args.workload == "llama3-8b" else args.workload]())
+    if args.restore_bench:
+        return main_restore(args, I.WORKLOADS["llama3.2-1b" if args.workload == "llama3-8b" else args.workload]())
     spec = I.WORKLOADS[args.workload]()
     if args.adamw:
         return main_adamw(args, spec)
@@ -413,6 +418,109 @@ def main_store(args, spec):
            "restored_timestamps": sorted(set(int(x) for x in chosen))}
     print(json.dumps(out), flush=True)
     shutil.rmtree(args.store_bench, ignore_errors=True)
+
+
+def main_restore(args, spec):
+    """Composite recovery (Section 3.5) from a history of versions: the base
+    at step 0 and the selections of the following decision steps.  Timed
+    twice per placement: every version resident in device memory (the unpack
+    kernel, against the HBM roofline) and every version in pinned host memory
+    (per-block host-to-device copies, against a plain pinned copy as the
+    host-link ceiling).  Bytes: each layer's record read once, its arrays and
+    its shadow written once."""
+    import torch
+    from paper_2609_27193_amd import inputs as I
+    from paper_2609_27193_amd import layercheck as LC
+
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    stream = torch.cuda.current_stream()
+    LC.load_library()
+    state = I.SyntheticState(spec, device=dev)
+    segs = LC.segments_from_state(state)
+    dtype = LC.LC_DT_BF16 if spec.weight_dtype == "bf16" else LC.LC_DT_F32
+    k0 = [(args.k0 or 0.03) * (10.0 if l.name == "embed_tokens" else 1.0) for l in spec.layers]
+    layout = LC.LayoutDesc(segs, spec.n_layers, dtype, spec.has_master, LC.LC_MODE_ACCUM, k0, spec.s_max,
+                           stream=stream.cuda_stream)
+    numel, rec = LC.lc_query_layout(layout)
+    ctx = LC.lc_init_layout(layout)
+    versions = []
+
+    def pack(t, mask):
+        nbytes = int(sum(rec[l] for l in range(spec.n_layers) if mask[l]))
+        buf = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=dev)
+        r = LC.lc_pack_selected(ctx, buf.data_ptr(), nbytes, 0)
+        assert r["done"] and r["bytes_written"] == nbytes
+        versions.append((t, mask.copy(), buf, nbytes))
+
+    pack(0, np.ones(spec.n_layers, np.uint8))
+    n_steps = 3  # base + three selections: a mixed-timestamp composite
+    for t in range(1, n_steps + 1):
+        state.step(t)
+        LC.lc_score_layers(ctx, t)
+        mask, _ = LC.lc_select(ctx, t, 1.0, spec.n_layers)
+        pack(t, mask)
+    torch.cuda.synchronize()
+    t_fail = n_steps
+    host = [(t, m, torch.empty(max(n, 1), dtype=torch.uint8, pin_memory=True), n) for t, m, _, n in versions]
+    for (_, _, d, n), (_, _, h, _) in zip(versions, host):
+        h[:n].copy_(d[:n])
+    torch.cuda.synchronize()
+    w = spec.weight_bytes
+    opt_b = 4 * (3 if spec.has_master else 2)
+    moved = sum(numel[l] * (w + opt_b) for l in range(spec.n_layers))
+    alg_bytes = 2 * moved + w * spec.numel  # record read + arrays written + shadow written
+
+    def timed(vs):
+        best = None
+        chosen = None
+        for _ in range(3):
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a = time.perf_counter()
+            e0.record(stream)
+            chosen = LC.lc_restore_composite(
+                ctx, [{"step": t, "mask": m, "payload": b.data_ptr() if n else 0, "payload_bytes": n}
+                      for t, m, b, n in vs], t_fail, spec.n_layers)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            wall = time.perf_counter() - a
+            best = wall if best is None else min(best, wall)
+        return best, chosen
+
+    dev_s, chosen = timed(versions)
+    host_s, chosen_h = timed(host)
+    assert chosen.tolist() == chosen_h.tolist()
+    # ceilings: a plain device copy of the record set's size, and a plain pinned H2D copy
+    n_all = versions[0][3]
+    src, dst = versions[0][2], torch.empty(n_all, dtype=torch.uint8, device=dev)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record(stream)
+    dst.copy_(src[:n_all])
+    e1.record(stream)
+    torch.cuda.synchronize()
+    d2d_gbs = 2 * n_all / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    e0.record(stream)
+    dst.copy_(host[0][2][:n_all], non_blocking=True)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    h2d_gbs = n_all / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    LC.lc_destroy(ctx)
+    out = {"metric": "composite restore GB/s (records read + state and shadow written)", "unit": "GB/s",
+           "config": {"workload": f"{spec.name}-shaped state", "params": spec.numel, "layer_groups": spec.n_layers,
+                      "versions": len(versions), "t_fail": t_fail,
+                      "restored_timestamps": sorted(set(int(x) for x in chosen)),
+                      "record_set_gb": round(moved / 1e9, 3), "algorithmic_gb": round(alg_bytes / 1e9, 3)},
+           "device_versions": {"s": round(dev_s, 5), "gbs": round(alg_bytes / dev_s / 1e9, 1),
+                               "frac_of_hbm_peak": round(alg_bytes / dev_s / 1e9 / HBM_PEAK_GBS, 4),
+                               "plain_d2d_copy_gbs": round(d2d_gbs, 1)},
+           "pinned_host_versions": {"s": round(host_s, 4), "record_gbs": round(moved / host_s / 1e9, 2),
+                                    "plain_h2d_copy_gbs": round(h2d_gbs, 2)}}
+    line = json.dumps(out)
+    print(line, flush=True)
+    if args.json_out:
+        with open(args.json_out, "w") as f:
+            f.write(line + "\n")
 
 
 ADAMW = dict(lr=1e-5, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
