@@ -44,7 +44,8 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=None, help="timed decision steps (default 2*S_max)")
     ap.add_argument("--warmup", type=int, default=None, help="untimed decision steps (default S_max)")
-    ap.add_argument("--workload", default="llama3-8b")
+    ap.add_argument("--workload", default=None,
+                    help="default: llama3-8b; llama3.2-1b for --store-bench and --restore-bench")
     ap.add_argument("--mode", choices=["accum", "snapshot"], default="accum")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -183,10 +184,12 @@ def main():
     from paper_2609_27193_amd import inputs as I
     from paper_2609_27193_amd import layercheck as LC
 
+    if args.workload is None:
+        args.workload = "llama3.2-1b" if (args.store_bench or args.restore_bench) else "llama3-8b"
     if args.store_bench:
-        return main_store(args, I.WORKLOADS["llama3.2-1b" if args.workload == "llama3-8b" else args.workload]())
+        return main_store(args, I.WORKLOADS[args.workload]())
     if args.restore_bench:
-        return main_restore(args, I.WORKLOADS["llama3.2-1b" if args.workload == "llama3-8b" else args.workload]())
+        return main_restore(args, I.WORKLOADS[args.workload]())
     spec = I.WORKLOADS[args.workload]()
     if args.adamw:
         return main_adamw(args, spec)
@@ -422,9 +425,10 @@ def main_store(args, spec):
 
 def main_restore(args, spec):
     """Composite recovery (Section 3.5) from a history of versions: the base
-    at step 0 and the selections of the following decision steps.  Timed
-    twice per placement: every version resident in device memory (the unpack
-    kernel, against the HBM roofline) and every version in pinned host memory
+    at step 0 and the selections of up to three following decision steps (as
+    many as device memory holds).  Timed with every version resident in
+    device memory (the unpack kernel, against the HBM roofline) and, when the
+    record set fits in 48 GB, with every version in pinned host memory
     (per-block host-to-device copies, against a plain pinned copy as the
     host-link ceiling).  Bytes: each layer's record read once, its arrays and
     its shadow written once."""
@@ -454,18 +458,24 @@ def main_restore(args, spec):
         versions.append((t, mask.copy(), buf, nbytes))
 
     pack(0, np.ones(spec.n_layers, np.uint8))
-    n_steps = 3  # base + three selections: a mixed-timestamp composite
-    for t in range(1, n_steps + 1):
+    t_fail = 0
+    for t in range(1, 4):  # up to three selections after the base: a mixed-timestamp composite
         state.step(t)
         LC.lc_score_layers(ctx, t)
-        mask, _ = LC.lc_select(ctx, t, 1.0, spec.n_layers)
+        mask, st = LC.lc_select(ctx, t, 1.0, spec.n_layers)
+        if st["payload_bytes"] + (8 << 30) > torch.cuda.mem_get_info()[0]:
+            log(f"[bench] step {t}: {st['payload_bytes'] / 1e9:.1f} GB does not fit beside the history; stop")
+            break
         pack(t, mask)
+        t_fail = t
     torch.cuda.synchronize()
-    t_fail = n_steps
-    host = [(t, m, torch.empty(max(n, 1), dtype=torch.uint8, pin_memory=True), n) for t, m, _, n in versions]
-    for (_, _, d, n), (_, _, h, _) in zip(versions, host):
-        h[:n].copy_(d[:n])
-    torch.cuda.synchronize()
+    with_host = versions[0][3] <= (48 << 30)
+    host = []
+    if with_host:
+        host = [(t, m, torch.empty(max(n, 1), dtype=torch.uint8, pin_memory=True), n) for t, m, _, n in versions]
+        for (_, _, d, n), (_, _, h, _) in zip(versions, host):
+            h[:n].copy_(d[:n])
+        torch.cuda.synchronize()
     w = spec.weight_bytes
     opt_b = 4 * (3 if spec.has_master else 2)
     moved = sum(numel[l] * (w + opt_b) for l in range(spec.n_layers))
@@ -489,22 +499,24 @@ def main_restore(args, spec):
         return best, chosen
 
     dev_s, chosen = timed(versions)
-    host_s, chosen_h = timed(host)
-    assert chosen.tolist() == chosen_h.tolist()
-    # ceilings: a plain device copy of the record set's size, and a plain pinned H2D copy
-    n_all = versions[0][3]
-    src, dst = versions[0][2], torch.empty(n_all, dtype=torch.uint8, device=dev)
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record(stream)
-    dst.copy_(src[:n_all])
-    e1.record(stream)
-    torch.cuda.synchronize()
-    d2d_gbs = 2 * n_all / (e0.elapsed_time(e1) * 1e-3) / 1e9
-    e0.record(stream)
-    dst.copy_(host[0][2][:n_all], non_blocking=True)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    h2d_gbs = n_all / (e0.elapsed_time(e1) * 1e-3) / 1e9
+    if with_host:
+        host_s, chosen_h = timed(host)
+        assert chosen.tolist() == chosen_h.tolist()
+    # ceilings: plain copies of 4 GiB (the second of two), device-to-device and pinned host-to-device
+    n_c = min(versions[0][3], 4 << 30)
+    dst = torch.empty(n_c, dtype=torch.uint8, device=dev)
+
+    def copy_rate(src, nbytes_moved):
+        for _ in range(2):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            dst.copy_(src, non_blocking=True)
+            e1.record(stream)
+            torch.cuda.synchronize()
+        return nbytes_moved / (e0.elapsed_time(e1) * 1e-3) / 1e9
+
+    d2d_gbs = copy_rate(versions[0][2][:n_c], 2 * n_c)
+    h2d_gbs = copy_rate(host[0][2][:n_c], n_c) if with_host else None
     LC.lc_destroy(ctx)
     out = {"metric": "composite restore GB/s (records read + state and shadow written)", "unit": "GB/s",
            "config": {"workload": f"{spec.name}-shaped state", "params": spec.numel, "layer_groups": spec.n_layers,
@@ -514,8 +526,8 @@ def main_restore(args, spec):
            "device_versions": {"s": round(dev_s, 5), "gbs": round(alg_bytes / dev_s / 1e9, 1),
                                "frac_of_hbm_peak": round(alg_bytes / dev_s / 1e9 / HBM_PEAK_GBS, 4),
                                "plain_d2d_copy_gbs": round(d2d_gbs, 1)},
-           "pinned_host_versions": {"s": round(host_s, 4), "record_gbs": round(moved / host_s / 1e9, 2),
-                                    "plain_h2d_copy_gbs": round(h2d_gbs, 2)}}
+           "pinned_host_versions": ({"s": round(host_s, 4), "record_gbs": round(moved / host_s / 1e9, 2),
+                                     "plain_h2d_copy_gbs": round(h2d_gbs, 2)} if with_host else None)}
     line = json.dumps(out)
     print(line, flush=True)
     if args.json_out:

@@ -136,6 +136,53 @@ def test_restore_composite_then_continue(where):
         p.close()
 
 
+def _mean_scores(spec, steps):
+    """Per-layer mean of u over the first ``steps`` steps of the synthetic
+    trajectory, from an oracle-only dry run (no selection by drift)."""
+    from tests.gpu_harness import to_numpy_weight
+    g = I.SyntheticState(spec, device="cpu")
+    hW = to_numpy_weight(g.weight)
+    hS = np.zeros_like(hW)
+    hM = None if g.master is None else g.master.numpy().copy()
+    hm, hv = g.exp_avg.numpy().copy(), g.exp_avg_sq.numpy().copy()
+    segs = [O.OSegment(s.layer, hW[s.offset:s.offset + s.numel], hS[s.offset:s.offset + s.numel],
+                       None if hM is None else hM[s.offset:s.offset + s.numel],
+                       hm[s.offset:s.offset + s.numel], hv[s.offset:s.offset + s.numel]) for s in g.segments]
+    dt = O.DT_BF16 if spec.weight_dtype == "bf16" else O.DT_F32
+    orc = O.LayerCheckOracle(segs, spec.n_layers, dt, spec.has_master, O.MODE_ACCUM,
+                             [float("inf")] * spec.n_layers, 10 ** 9)
+    us = []
+    for t in range(1, steps + 1):
+        g.step(t)
+        hW[...] = to_numpy_weight(g.weight)
+        orc.score(t)
+        us.append(list(orc.u))
+        orc.select(t, 1.0)
+    return np.mean(us, axis=0)
+
+
+def test_restore_five_timestamps():
+    """A composite of five different timestamps (Section 3.5): per-layer
+    thresholds give each layer its own persist period (every 1, 2, 3, 4 and 5
+    steps; the final norm only by the S_max = 6 guard), twelve versions on
+    the device, recovery at t_fail = 11 mixes steps 6, 8, 9, 10 and 11."""
+    spec = reduced_qwen()
+    names = [l.name for l in spec.layers]
+    assert names == ["embed_tokens", "block_0", "block_1", "block_2", "norm", "lm_head"]
+    u = _mean_scores(spec, 4)
+    period = {"embed_tokens": 2, "block_0": 3, "block_1": 4, "block_2": 5, "lm_head": 1}
+    k0 = [u[l] * (period[n] - 0.5) if n in period else 1e9 for l, n in enumerate(names)]
+    p = Pair(spec, LC.LC_MODE_ACCUM, k0)
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        run_steps(p, range(1, 13))
+        chosen = _restore_and_compare(p, 11, "device")
+        assert sorted(set(chosen.tolist())) == [6, 8, 9, 10, 11], chosen
+        assert chosen.tolist() == [10, 9, 8, 10, 6, 11]
+    finally:
+        p.close()
+
+
 def test_restore_roundtrip_repack():
     """Restore, then re-pack every layer: each record equals the record it was
     restored from, bit for bit."""
