@@ -168,10 +168,18 @@ def cpu_baseline(state, spec, mode_name, n_layers=3):
     rec_unpadded = n * (w + 4 * (3 if spec.has_master else 2))
     pack_bytes = rec_unpadded + len(payload) + (w * n if mode == O.MODE_SNAPSHOT else 0)
     gbs = (score_bytes + pack_bytes) / elapsed / 1e9
+    cpu = "unknown CPU"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                cpu = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
     return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
             "sample": f"{len(blocks)} transformer blocks ({n} params) of the same state: "
                       f"score + select + pack in {elapsed:.2f} s, host copy {copy_s:.2f} s excluded; "
-                      f"numpy fp64, single thread"}
+                      f"numpy fp64, single thread on {cpu} ({len(os.sched_getaffinity(0))} cores visible)"}
 
 
 def main():

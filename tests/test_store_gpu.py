@@ -55,6 +55,9 @@ def test_drain_and_restore_from_store(tmp_path, maker, mode, buf):
             mask, st = p.select(t, 1.0, dl, tl)
             pack_and_drain(t, mask)
         store.sync()
+        # several versions were in flight on the writer pool; they become
+        # visible in append order
+        assert [e["step"] for e in store.entries()] == [e["step"] for e in expected]
         files = sorted(f for f in os.listdir(d) if f.endswith(".lcr"))
         assert len(files) == len(expected)
         for f, e in zip(files, expected):
