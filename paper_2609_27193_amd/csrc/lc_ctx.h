@@ -9,7 +9,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/layercheck.h"
+#include "layercheck.h"
 #include "lc_internal.h"
 
 namespace lc {

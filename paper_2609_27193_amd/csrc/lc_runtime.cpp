@@ -12,7 +12,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/layercheck.h"
+#include "layercheck.h"
 #include "lc_ctx.h"
 #include "lc_internal.h"
 
