@@ -133,3 +133,35 @@ def test_segment_larger_than_4gib_closed_form():
         assert torch.equal(S, W)
     finally:
         LC.lc_destroy(ctx)
+
+
+def many_layer_spec(n_layers=1500, seed=11):
+    """Many tiny layers of 1-3 tensors (1..300 elements each): the select
+    kernel's per-layer loops and prefix tables, and packs of hundreds of
+    records, at a layer count far above any model's."""
+    T = I.TensorSpec
+    rng = np.random.default_rng(seed)
+    layers = tuple(
+        I.LayerSpec(f"block_{l}", tuple(T(f"t{k}", int(rng.integers(1, 301)), "matrix")
+                                        for k in range(int(rng.integers(1, 4)))))
+        for l in range(n_layers))
+    return I.ModelSpec(name=f"many-{n_layers}", layers=layers, weight_dtype="bf16", has_master=True,
+                       scale_rule="loguniform_0.01_1", target_fraction=0.3, s_max=5)
+
+
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_many_layers(mode):
+    spec = many_layer_spec()
+    rng = np.random.default_rng(3)
+    p = Pair(spec, mode, list(10.0 ** rng.uniform(-2.5, -0.5, spec.n_layers)))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8), capacity=64 * 1024)
+        sel = []
+        for t in range(1, 9):
+            mask, st = p.step(t, capacity=64 * 1024 if t % 2 else None)
+            sel.append(st["n_selected"])
+        log(f"  {p.N} layers: selected per step {sel}")
+        assert min(sel) > 0 and max(sel) < p.N
+        p.check_arrays()
+    finally:
+        p.close()
