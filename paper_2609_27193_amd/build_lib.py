@@ -47,5 +47,31 @@ def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
     return out
 
 
+C_CLIENT_SRC = os.path.join(ROOT, "tests", "c_client", "lc_c_client.c")
+C_CLIENT = os.path.join(ROOT, "tests", "c_client", "lc_c_client")
+
+
+def build_c_client(verbose: bool = False, lib: str = LIB) -> str:
+    """Compile the plain-C test client of the interface (gcc, C11, HIP host
+    API only) against the in-tree library."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    cmd = ["gcc", "-std=c11", "-O2", "-Wall", "-Wextra", "-D__HIP_PLATFORM_AMD__",
+           "-I", os.path.join(rocm, "include"), "-I", os.path.join(ROOT, "include"),
+           C_CLIENT_SRC, "-o", C_CLIENT + ".tmp",
+           "-L", os.path.dirname(lib), "-l" + os.path.basename(lib)[3:-3],
+           "-L", os.path.join(rocm, "lib"), "-lamdhip64",
+           "-Wl,-rpath,$ORIGIN/../../paper_2609_27193_amd", "-Wl,-rpath," + os.path.join(rocm, "lib")]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0 or res.stderr.strip():
+        sys.stderr.write(res.stdout + res.stderr)
+        if res.returncode != 0:
+            raise RuntimeError(f"gcc failed with exit code {res.returncode}")
+    os.replace(C_CLIENT + ".tmp", C_CLIENT)
+    return C_CLIENT
+
+
 if __name__ == "__main__":
     print(build(verbose=True))
+    print(build_c_client(verbose=True))
