@@ -52,6 +52,9 @@ def parse():
                     help="also run one plain 4 GiB device copy (counter calibration)")
     ap.add_argument("--adamw", action="store_true",
                     help="drive the state with the fused AdamW + drift step instead of the standalone score")
+    ap.add_argument("--torch-adamw-reference", action="store_true",
+                    help="with --adamw: also time torch's fused AdamW (no drift) on the same parameter "
+                         "shapes, plus the bf16 weight copy, as a reference point")
     ap.add_argument("--store-bench", default=None, metavar="DIR",
                     help="measure draining packed records into a persistence store in DIR and restoring "
                          "from it (default workload llama3.2-1b)")
@@ -662,11 +665,55 @@ def main_adamw(args, spec):
                      "frac": round(opt_bytes / opt_ms / 1e6 / HBM_PEAK_GBS, 4),
                      "traffic": measured_traffic("adamw_kernel", args.workload, "accum")},
     }
+    if args.torch_adamw_reference:
+        del state, staging
+        torch.cuda.empty_cache()
+        out["torch_fused_adamw_reference"] = torch_adamw_reference(spec, dev)
     line = json.dumps(out)
     print(line, flush=True)
     if args.json_out:
         with open(args.json_out, "w") as f:
             f.write(line + "\n")
+
+
+def torch_adamw_reference(spec, dev, steps=5):
+    """torch.optim.AdamW(fused=True) over one fp32 master tensor per layer of
+    the same shapes (fp32 gradients, as that optimizer requires the
+    parameter's dtype), followed by the bf16 weight copy that the fused
+    AdamW + drift kernel writes in the same pass.  No drift is computed."""
+    import torch
+    params, weights = [], []
+    for layer in spec.layers:
+        n = sum(t.numel for t in layer.tensors)
+        p = torch.nn.Parameter(torch.randn(n, device=dev) * 0.02)
+        p.grad = torch.randn(n, device=dev)
+        params.append(p)
+        weights.append(torch.empty(n, dtype=torch.bfloat16, device=dev))
+    opt = torch.optim.AdamW(params, lr=ADAMW["lr"], betas=(ADAMW["beta1"], ADAMW["beta2"]), eps=ADAMW["eps"],
+                            weight_decay=ADAMW["weight_decay"], fused=True)
+    stream = torch.cuda.current_stream()
+    times = []
+    for i in range(steps + 2):
+        e = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        torch.cuda.synchronize()
+        e[0].record(stream)
+        opt.step()
+        e[1].record(stream)
+        with torch.no_grad():
+            for w, p in zip(weights, params):
+                w.copy_(p)
+        e[2].record(stream)
+        torch.cuda.synchronize()
+        if i >= 2:
+            times.append((e[0].elapsed_time(e[1]), e[1].elapsed_time(e[2])))
+    opt_ms = float(np.mean([a for a, _ in times]))
+    copy_ms = float(np.mean([b for _, b in times]))
+    P = spec.numel
+    log(f"[bench] torch fused AdamW {opt_ms:.2f} ms + bf16 weight copy {copy_ms:.2f} ms")
+    return {"adamw_ms": round(opt_ms, 3), "weight_copy_ms": round(copy_ms, 3),
+            "total_ms": round(opt_ms + copy_ms, 3),
+            "bytes_gb": round(P * (28 + 6) / 1e9, 2),
+            "note": "fp32 params and grads (28 B/param) + bf16 weight copy (6 B/param); no drift statistic"}
 
 
 if __name__ == "__main__":
