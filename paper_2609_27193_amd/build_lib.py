@@ -28,12 +28,29 @@ def hipcc() -> str:
     return os.path.join(rocm, "bin", "hipcc")
 
 
-def build(verbose: bool = False, out: str = LIB, defines=()) -> str:
+SANITIZED_LIB = os.path.join(HERE, "liblayercheck_hostsan.so")
+# AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (the
+# validation, tables, state machine and store); device code is unchanged.
+HOST_SANITIZER_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+                        "-Xarch_host", "-fno-sanitize-recover=undefined", "-shared-libsan", "-g"]
+
+
+def sanitizer_runtime() -> str:
+    """The clang AddressSanitizer runtime the sanitized build needs preloaded."""
+    import glob
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    hits = sorted(glob.glob(os.path.join(rocm, "lib", "llvm", "lib", "clang", "*", "lib", "linux",
+                                         "libclang_rt.asan-x86_64.so")))
+    return hits[-1] if hits else ""
+
+
+def build(verbose: bool = False, out: str = LIB, defines=(), sanitize: bool = False) -> str:
     """Compile the library to ``out``; ``defines`` are extra -D macros
-    (tile sizes LC_CHUNK_BYTES / LC_PIECE_BYTES for tuning builds)."""
+    (tile sizes LC_CHUNK_BYTES / LC_PIECE_BYTES for tuning builds);
+    ``sanitize`` adds the host-side sanitizers (for CPU tests only)."""
     tmp = out + ".tmp"
-    cmd = [hipcc(), *HIPCC_FLAGS, *[f"-D{d}" for d in defines], "-o", tmp,
-           *[os.path.join(CSRC, s) for s in SOURCES]]
+    cmd = [hipcc(), *HIPCC_FLAGS, *(HOST_SANITIZER_FLAGS if sanitize else []), *[f"-D{d}" for d in defines],
+           "-o", tmp, *[os.path.join(CSRC, s) for s in SOURCES]]
     if verbose:
         print(" ".join(cmd), flush=True)
     res = subprocess.run(cmd, capture_output=True, text=True)
@@ -75,3 +92,4 @@ def build_c_client(verbose: bool = False, lib: str = LIB) -> str:
 if __name__ == "__main__":
     print(build(verbose=True))
     print(build_c_client(verbose=True))
+    print(build(verbose=True, out=SANITIZED_LIB, sanitize=True))
