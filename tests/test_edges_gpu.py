@@ -165,3 +165,27 @@ def test_many_layers(mode):
         p.check_arrays()
     finally:
         p.close()
+
+
+def test_layer_of_64_segments_and_restore():
+    """A layer of 64 tensors (1..5000 elements: 64 blocks per array in its
+    record), a one-element layer and a plain layer, six steps, then a
+    composite restore from device versions."""
+    from tests.test_parity_gpu import _restore_and_compare
+    T = I.TensorSpec
+    rng = np.random.default_rng(64)
+    layers = (I.LayerSpec("block_0", tuple(T(f"t{k}", int(rng.integers(1, 5001)), "matrix") for k in range(64))),
+              I.LayerSpec("norm", (T("n", 1, "norm"),)),
+              I.LayerSpec("block_1", (T("w", 20000, "matrix"),)))
+    spec = I.ModelSpec(name="seg64", layers=layers, weight_dtype="bf16", has_master=True,
+                       scale_rule="loguniform_0.01_1", target_fraction=0.5, s_max=3)
+    p = Pair(spec, LC.LC_MODE_ACCUM, [0.02, 1e300, 0.02])
+    try:
+        assert len([s for s in p.lsegs if s.layer == 0]) == 64
+        p.pack(0, np.ones(p.N, np.uint8))
+        for t in range(1, 7):
+            p.step(t)
+        chosen = _restore_and_compare(p, 5, "device")
+        log(f"  restored from steps {chosen.tolist()}")
+    finally:
+        p.close()
