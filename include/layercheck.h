@@ -280,6 +280,18 @@ lc_status lc_store_plan(lc_store *s, int64_t t_fail, int64_t *chosen_step_out);
  * record sizes.  Returns after the restore has completed. */
 lc_status lc_store_restore(lc_store *s, lc_ctx *c, int64_t t_fail, int64_t *chosen_step_out);
 
+/* Storage reclamation: removes the versions that no reconstruction plan with
+ * t_fail >= t_keep can choose (Section 3.5), i.e. keeps every non-empty
+ * version after t_keep and, per layer, the newest version at or before t_keep
+ * holding it; plans for t_fail >= t_keep are unchanged.  t_keep = the newest
+ * stored step keeps exactly the latest record of every layer.  Waits for
+ * pending writes first.  The manifest is replaced atomically (temporary file,
+ * fsync, rename, directory fsync) before any version file is removed, so a
+ * crash leaves either the old history or the new one; files that no manifest
+ * line names are removed too.  `removed_out` (or NULL) receives the number of
+ * files removed. */
+lc_status lc_store_compact(lc_store *s, int64_t t_keep, uint32_t *removed_out);
+
 /* Waits for pending writes, stops the writer and frees the store. */
 lc_status lc_store_close(lc_store *s);
 

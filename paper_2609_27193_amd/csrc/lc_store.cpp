@@ -10,6 +10,7 @@
 // of writer threads writes each buffer as soon as its copy completes, so the
 // caller's stream is released as soon as the staging buffer has been read.
 // Versions are made durable in the order they were appended.
+#include <dirent.h>
 #include <fcntl.h>
 #include <sys/stat.h>
 #include <sys/types.h>
@@ -118,6 +119,20 @@ std::string mask_string(const std::vector<uint8_t>& m) {
   return s;
 }
 
+std::string manifest_line(const StoredVersion& v) {
+  return "LCV1 " + std::to_string(v.step) + " " + std::to_string(v.bytes) + " " + v.file + " " + mask_string(v.mask) +
+         "\n";
+}
+
+// Makes the directory's entries (new files, renames, removals) durable.
+bool fsync_dir(const std::string& dir) {
+  const int fd = open(dir.c_str(), O_RDONLY | O_DIRECTORY);
+  if (fd < 0) return false;
+  const bool ok = fsync(fd) == 0;
+  close(fd);
+  return ok;
+}
+
 }  // namespace
 
 struct lc_store {
@@ -151,16 +166,16 @@ struct lc_store {
 
 namespace {
 
-// Makes a completed version durable: fsync its file, then append and fsync
-// its manifest line.
+// Makes a completed version durable: fsync its file and the directory entry,
+// then append and fsync its manifest line.
 std::string finalise(lc_store* s, const StoredVersion& v) {
   std::string err;
   if (v.dfd >= 0) close(v.dfd);
   if (fsync(v.fd) != 0) err = std::string("fsync failed: ") + std::strerror(errno);
   close(v.fd);
+  if (err.empty() && !fsync_dir(s->dir)) err = std::string("directory fsync failed: ") + std::strerror(errno);
   if (!err.empty()) return err;
-  const std::string line = "LCV1 " + std::to_string(v.step) + " " + std::to_string(v.bytes) + " " + v.file + " " +
-                           mask_string(v.mask) + "\n";
+  const std::string line = manifest_line(v);
   const off_t end = lseek(s->manifest_fd, 0, SEEK_END);
   if (end < 0 ||
       !write_all(s->manifest_fd, reinterpret_cast<const uint8_t*>(line.data()), line.size(),
@@ -723,6 +738,75 @@ lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chos
   cleanup();
   if (st != LC_OK) return st;
   if (chosen_step_out) std::memcpy(chosen_step_out, steps.data(), s->N * sizeof(int64_t));
+  return LC_OK;
+}
+
+lc_status lc_store_compact(lc_store* s, int64_t t_keep, uint32_t* removed_out) {
+  if (removed_out) *removed_out = 0;
+  if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
+  lc_status st = wait_idle(s);
+  if (st != LC_OK) return st;
+  // needed: every non-empty version after t_keep, and per layer the newest
+  // version at or before t_keep holding it
+  const size_t n = s->durable.size();
+  std::vector<uint8_t> keep(n, 0);
+  for (size_t i = 0; i < n; ++i) {
+    const StoredVersion& v = s->durable[i];
+    if (v.step > t_keep)
+      for (uint32_t l = 0; l < s->N && !keep[i]; ++l) keep[i] = v.mask[l];
+  }
+  for (uint32_t l = 0; l < s->N; ++l) {
+    long best = -1;
+    for (size_t i = 0; i < n; ++i) {
+      const StoredVersion& v = s->durable[i];
+      if (v.step <= t_keep && v.mask[l] && (best < 0 || v.step > s->durable[best].step)) best = static_cast<long>(i);
+    }
+    if (best >= 0) keep[best] = 1;
+  }
+  std::vector<StoredVersion> kept;
+  std::vector<std::string> gone;
+  for (size_t i = 0; i < n; ++i) {
+    if (keep[i]) kept.push_back(s->durable[i]);
+    else gone.push_back(s->durable[i].file);
+  }
+  // files no manifest line names (a crash between a manifest rewrite and the
+  // removals, or a version that never became visible) go too: nothing is in
+  // flight once the store is idle
+  if (DIR* dp = opendir(s->dir.c_str())) {
+    std::vector<std::string> named;
+    for (const StoredVersion& v : s->durable) named.push_back(v.file);
+    while (dirent* e = readdir(dp)) {
+      const std::string f = e->d_name;
+      if (f.size() > 4 && f.compare(f.size() - 4, 4, ".lcr") == 0 &&
+          std::find(named.begin(), named.end(), f) == named.end())
+        gone.push_back(f);
+    }
+    closedir(dp);
+  }
+  if (gone.empty()) return LC_OK;
+  if (kept.size() != n) {
+    // the new manifest replaces the old one atomically: written to a temporary
+    // file, fsync'ed, renamed over it, then the directory fsync'ed
+    const std::string mpath = s->dir + "/manifest.lcm", tpath = s->dir + "/manifest.lcm.tmp";
+    const int fd = open(tpath.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
+    if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", tpath.c_str(), std::strerror(errno));
+    std::string text;
+    for (const StoredVersion& v : kept) text += manifest_line(v);
+    const bool ok = write_all(fd, reinterpret_cast<const uint8_t*>(text.data()), text.size(), 0) && fsync(fd) == 0;
+    close(fd);
+    if (!ok || rename(tpath.c_str(), mpath.c_str()) != 0 || !fsync_dir(s->dir))
+      return fail(LC_ERR_INVALID_ARG, "rewriting the manifest failed: %s", std::strerror(errno));
+    const int mfd = open(mpath.c_str(), O_RDWR);
+    if (mfd < 0) return fail(LC_ERR_INVALID_ARG, "cannot reopen %s: %s", mpath.c_str(), std::strerror(errno));
+    close(s->manifest_fd);
+    s->manifest_fd = mfd;
+    s->durable = kept;
+  }
+  uint32_t removed = 0;
+  for (const std::string& f : gone)
+    if (unlink((s->dir + "/" + f).c_str()) == 0) ++removed;
+  (void)fsync_dir(s->dir);
+  if (removed_out) *removed_out = removed;
   return LC_OK;
 }
 

@@ -25,7 +25,7 @@ LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
             "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_store_open", "lc_store_append", "lc_store_sync",
-            "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore", "lc_store_close",
+            "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore", "lc_store_compact", "lc_store_close",
             "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
 
 
@@ -98,6 +98,7 @@ def load_library(path: str = LIB_PATH):
             "lc_store_entry": (C.c_int, [C.c_void_p, C.c_uint32, P(C.c_int64), P(C.c_uint8), P(C.c_uint64)]),
             "lc_store_plan": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_int64)]),
             "lc_store_restore": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, P(C.c_int64)]),
+            "lc_store_compact": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint32)]),
             "lc_store_close": (C.c_int, [C.c_void_p]),
             "lc_read_state": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double), P(C.c_int64)]),
             "lc_record_bytes": (C.c_uint64, [C.c_void_p, C.c_uint32]),
@@ -263,6 +264,13 @@ class Store:
         _check(load_library().lc_store_restore(self.h, ctx, t_fail, out.ctypes.data_as(C.POINTER(C.c_int64))),
                "lc_store_restore")
         return out
+
+    def compact(self, t_keep: int) -> int:
+        """Removes versions no plan with t_fail >= t_keep can choose; returns
+        the number of files removed."""
+        n = C.c_uint32()
+        _check(load_library().lc_store_compact(self.h, t_keep, C.byref(n)), "lc_store_compact")
+        return n.value
 
     def close(self) -> None:
         if self.h is not None:

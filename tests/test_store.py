@@ -142,3 +142,60 @@ def test_large_host_payload_in_pieces(lib, tmp_path):
     files = sorted(f for f in os.listdir(d) if f.endswith(".lcr"))
     assert np.array_equal(np.fromfile(os.path.join(d, files[0]), np.uint8), payload)
     assert np.array_equal(np.fromfile(os.path.join(d, files[1]), np.uint8), part)
+
+
+@pytest.mark.parametrize("t_keep", [0, 3, 5, 8, 100])
+def test_compact_keeps_exactly_what_plans_can_choose(lib, tmp_path, t_keep):
+    """After lc_store_compact(t_keep) the store holds exactly the union, over
+    every t_fail >= t_keep, of the versions the oracle's plan chooses; those
+    plans are unchanged; the removed files are gone and the history survives
+    a reopen."""
+    orc, versions = oracle_history(steps=8)
+    d = str(tmp_path / "k")
+    st = LC.Store(d, orc.R)
+    for v in versions:
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    st.sync()
+    last = max(v["step"] for v in versions)
+    t_fails = range(t_keep, max(t_keep, last) + 2)  # plans for t_fail >= last all agree
+    chosen = set()
+    plans_before = {}
+    for t in t_fails:
+        try:
+            idx = O.plan_versions(versions, orc.N, t)
+        except O.OracleError:
+            continue
+        chosen.update(idx)
+        plans_before[t] = st.plan(t).tolist()
+    removed = st.compact(t_keep)
+    kept = [versions[i]["step"] for i in sorted(chosen)]
+    assert [e["step"] for e in st.entries()] == kept
+    assert removed == len(versions) - len(kept)
+    for t, plan in plans_before.items():
+        assert st.plan(t).tolist() == plan
+    st.close()
+    assert len([f for f in os.listdir(d) if f.endswith(".lcr")]) == len(kept)
+    st = LC.Store(d, orc.R)
+    assert [e["step"] for e in st.entries()] == kept
+    assert st.compact(t_keep) == 0  # nothing more to reclaim
+    st.close()
+
+
+def test_compact_crash_leftovers(lib, tmp_path):
+    """A crash during compaction leaves a stale temporary manifest or files the
+    manifest no longer names; the next open ignores them and the next
+    compaction removes the orphans."""
+    orc, versions = oracle_history(steps=4)
+    d = str(tmp_path / "c2")
+    st = LC.Store(d, orc.R)
+    for v in versions:
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    st.close()
+    open(os.path.join(d, "manifest.lcm.tmp"), "w").write("LCV1 garbage\n")
+    open(os.path.join(d, "v0000000999_s3.lcr"), "wb").write(b"\0" * 256)
+    st = LC.Store(d, orc.R)
+    assert [e["step"] for e in st.entries()] == [v["step"] for v in versions]
+    removed = st.compact(-1)  # keeps every non-empty version; removes the orphan
+    assert removed >= 1
+    assert "v0000000999_s3.lcr" not in os.listdir(d)
+    st.close()
