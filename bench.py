@@ -408,12 +408,19 @@ def main_store(args, spec):
         drained += r["bytes_written"]
         log(f"[bench] t={t}: {st['n_selected']} layers, {r['bytes_written'] / 1e9:.2f} GB: append {b - a:.3f} s, "
             f"staging free after {c - a:.3f} s, durable after {d - a:.3f} s")
+    t_fail = 5
+    stored_before = sum(e["payload_bytes"] for e in store.entries())
+    a = time.perf_counter()
+    removed = store.compact(t_fail)  # keep what recovery at t_fail or later can use
+    compact_s = time.perf_counter() - a
+    stored_after = sum(e["payload_bytes"] for e in store.entries())
+    log(f"[bench] compaction at t_keep={t_fail}: {stored_before / 1e9:.2f} GB -> {stored_after / 1e9:.2f} GB "
+        f"({removed} files removed) in {compact_s:.3f} s")
     # fail-stop: lose the live state, recover the composite from the store
     for tnsr in (state.weight, state.shadow, state.master, state.exp_avg, state.exp_avg_sq):
         if tnsr is not None:
             tnsr.zero_()
     torch.cuda.synchronize()
-    t_fail = 5
     a = time.perf_counter()
     chosen = store.restore(ctx, t_fail)
     restore_s = time.perf_counter() - a
@@ -428,6 +435,8 @@ def main_store(args, spec):
            "steps_append_call_s": round(call_s, 3),
            "steps_staging_release_gbs": round(drained / release_s / 1e9, 2),
            "steps_durable_gbs": round(drained / durable_s / 1e9, 3),
+           "stored_gb_before_compact": round(stored_before / 1e9, 3),
+           "stored_gb_after_compact": round(stored_after / 1e9, 3), "compact_s": round(compact_s, 3),
            "restore_gbs": round(total / restore_s / 1e9, 3), "restore_s": round(restore_s, 3),
            "restored_timestamps": sorted(set(int(x) for x in chosen))}
     print(json.dumps(out), flush=True)
