@@ -403,6 +403,138 @@ lc_status wait_idle(lc_store* s) {
   return LC_OK;
 }
 
+// Reads the chosen record of every layer and restores it (Section 3.5 steps
+// 2-3) as one pipeline: reader threads pull 64 MiB pieces of the records, in
+// layer order and across layer boundaries, into a pinned byte ring; as soon
+// as a layer's pieces are all in, its host-to-device copies are enqueued on
+// the context's stream, and its ring space is reused once an event after
+// those copies has completed.  The disk never waits for a batch boundary.
+lc_status restore_pipeline(lc_store* s, lc_ctx* c, const std::vector<size_t>& choice,
+                           const std::vector<uint64_t>& off, std::map<size_t, int>& fds) {
+  const uint32_t N = s->N;
+  constexpr uint64_t kPiece = 64ull << 20;
+  constexpr unsigned kReaders = 8;
+  const uint64_t max_rec = *std::max_element(s->R.begin(), s->R.end());
+  const uint64_t RB = std::max<uint64_t>(2 * max_rec, 1ull << 30);  // any record fits beside another
+  uint8_t* ring = nullptr;
+  {
+    void* p = nullptr;
+    const hipError_t e = hipHostMalloc(&p, RB, hipHostMallocDefault);
+    if (e != hipSuccess) return fail(LC_ERR_OOM, "pinned restore ring: %s", hipGetErrorString(e));
+    ring = static_cast<uint8_t*>(p);
+  }
+  std::vector<hipEvent_t> ev(N, nullptr);
+  struct Piece { int fd; uint64_t src; uint8_t* dst; uint64_t len; uint32_t layer; };
+  std::mutex mu;
+  std::condition_variable cv;
+  std::deque<Piece> queue;
+  std::vector<uint32_t> left(N, 0);  // pieces of each layer not yet read
+  bool stop = false, read_error = false;
+  std::vector<std::thread> readers;
+  for (unsigned r = 0; r < kReaders; ++r)
+    readers.emplace_back([&] {
+      for (;;) {
+        Piece pc;
+        {
+          std::unique_lock<std::mutex> lk(mu);
+          cv.wait(lk, [&] { return stop || !queue.empty(); });
+          if (queue.empty()) return;
+          pc = queue.front();
+          queue.pop_front();
+        }
+        const bool ok = read_all(pc.fd, pc.dst, pc.len, pc.src);
+        {
+          std::lock_guard<std::mutex> lk(mu);
+          if (!ok) read_error = true;
+          --left[pc.layer];
+        }
+        cv.notify_all();
+      }
+    });
+  struct Slot { uint64_t begin, end; uint32_t layer; };
+  std::deque<Slot> live;  // ring ranges in allocation order
+  uint64_t head = 0;
+  uint32_t next_alloc = 0, next_copy = 0;
+  lc_status st = LC_OK;
+  auto overlaps = [&](uint64_t a, uint64_t e) {
+    for (const Slot& sl : live)
+      if (a < sl.end && sl.begin < e) return true;
+    return false;
+  };
+  while (st == LC_OK && next_copy < N) {
+    // place and queue the reads of as many layers as the ring holds
+    bool progressed = false;
+    while (next_alloc < N) {
+      const uint64_t R = s->R[next_alloc];
+      const uint64_t a = head + R <= RB ? head : 0;
+      if (overlaps(a, a + R)) break;
+      live.push_back({a, a + R, next_alloc});
+      head = a + R;
+      {
+        std::lock_guard<std::mutex> lk(mu);
+        const int fd = fds[choice[next_alloc]];
+        uint32_t n = 0;
+        for (uint64_t o = 0; o < R; o += kPiece, ++n)
+          queue.push_back({fd, off[next_alloc] + o, ring + a + o, std::min<uint64_t>(kPiece, R - o), next_alloc});
+        left[next_alloc] = n;
+      }
+      cv.notify_all();
+      ++next_alloc;
+      progressed = true;
+    }
+    // the ring is full: reclaim the oldest range once its copies are done
+    if (next_alloc < N && !progressed && !live.empty() && live.front().layer < next_copy) {
+      const hipError_t e = hipEventSynchronize(ev[live.front().layer]);
+      if (e != hipSuccess) {
+        c->poisoned = true;
+        st = fail(LC_ERR_HIP, "restore copy failed: %s", hipGetErrorString(e));
+        break;
+      }
+      live.pop_front();
+      continue;
+    }
+    // enqueue the copies of the next layer once all its pieces are in
+    if (next_copy >= next_alloc) {  // cannot happen: an empty ring holds any record
+      st = fail(LC_ERR_INVALID_ARG, "internal: restore pipeline stalled at layer %u", next_copy);
+      break;
+    }
+    {
+      std::unique_lock<std::mutex> lk(mu);
+      cv.wait(lk, [&] { return read_error || left[next_copy] == 0; });
+      if (read_error) {
+        st = fail(LC_ERR_INVALID_ARG, "reading a stored record failed");
+        break;
+      }
+    }
+    const Slot* slot = nullptr;
+    for (const Slot& sl : live)
+      if (sl.layer == next_copy) slot = &sl;
+    st = restore_layer_from_host(c, next_copy, ring + slot->begin);
+    if (st != LC_OK) break;
+    hipError_t e = hipEventCreateWithFlags(&ev[next_copy], hipEventDisableTiming);
+    if (e == hipSuccess) e = hipEventRecord(ev[next_copy], c->stream);
+    if (e != hipSuccess) {
+      c->poisoned = true;
+      st = fail(LC_ERR_HIP, "event record failed: %s", hipGetErrorString(e));
+      break;
+    }
+    ++next_copy;
+  }
+  {
+    std::lock_guard<std::mutex> lk(mu);
+    stop = true;
+    queue.clear();
+  }
+  cv.notify_all();
+  for (auto& th : readers) th.join();
+  // the ring must outlive every copy that reads it
+  (void)hipStreamSynchronize(c->stream);
+  for (hipEvent_t e : ev)
+    if (e) (void)hipEventDestroy(e);
+  (void)hipHostFree(ring);
+  return st;
+}
+
 }  // namespace
 
 extern "C" {
@@ -651,91 +783,12 @@ lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chos
     }
     fds[i] = fd;
   }
-  // two pinned buffers: files are read into one while the GPU copies the other
-  const uint64_t max_rec = *std::max_element(s->R.begin(), s->R.end());
-  const uint64_t B = std::max<uint64_t>(max_rec, std::min<uint64_t>(s->slot_bytes * s->n_slots, 1ull << 30));
-  uint8_t* buf[2] = {nullptr, nullptr};
-  hipEvent_t done[2] = {nullptr, nullptr};
-  auto cleanup = [&]() {
-    for (int k = 0; k < 2; ++k) {
-      if (done[k]) (void)hipEventSynchronize(done[k]), (void)hipEventDestroy(done[k]);
-      if (buf[k]) (void)hipHostFree(buf[k]);
-    }
-    for (auto& kv : fds) close(kv.second);
-  };
-  for (int k = 0; k < 2; ++k) {
-    void* p = nullptr;
-    hipError_t e = hipHostMalloc(&p, B, hipHostMallocDefault);
-    if (e != hipSuccess) {
-      cleanup();
-      return fail(LC_ERR_OOM, "pinned restore buffer: %s", hipGetErrorString(e));
-    }
-    buf[k] = static_cast<uint8_t*>(p);
-    e = hipEventCreateWithFlags(&done[k], hipEventDisableTiming);
-    if (e != hipSuccess) {
-      cleanup();
-      return fail(LC_ERR_HIP, "event create failed: %s", hipGetErrorString(e));
-    }
-  }
-  bool used[2] = {false, false};
-  uint32_t l = 0;
-  int k = 0;
-  while (l < s->N) {
-    uint32_t end = l;
-    uint64_t fill = 0;
-    while (end < s->N && fill + s->R[end] <= B) fill += s->R[end++];
-    if (used[k] && hipEventSynchronize(done[k]) != hipSuccess) {
-      cleanup();
-      c->poisoned = true;
-      return fail(LC_ERR_HIP, "restore copy failed");
-    }
-    // read the batch with a few threads, 64 MiB at a time
-    struct Piece { int fd; uint64_t src; uint8_t* dst; uint64_t len; };
-    std::vector<Piece> pieces;
-    uint64_t pos = 0;
-    for (uint32_t j = l; j < end; ++j) {
-      for (uint64_t o = 0; o < s->R[j]; o += (64ull << 20)) {
-        const uint64_t len = std::min<uint64_t>(64ull << 20, s->R[j] - o);
-        pieces.push_back({fds[choice[j]], off[j] + o, buf[k] + pos + o, len});
-      }
-      pos += s->R[j];
-    }
-    std::atomic<size_t> next{0};
-    std::atomic<bool> ok{true};
-    const unsigned nt = std::min<size_t>(8, pieces.size());
-    std::vector<std::thread> readers;
-    for (unsigned r = 0; r < nt; ++r)
-      readers.emplace_back([&] {
-        for (size_t i; (i = next.fetch_add(1)) < pieces.size();)
-          if (!read_all(pieces[i].fd, pieces[i].dst, pieces[i].len, pieces[i].src)) ok = false;
-      });
-    for (auto& th : readers) th.join();
-    if (!ok) {
-      cleanup();
-      return fail(LC_ERR_INVALID_ARG, "reading a stored record failed");
-    }
-    pos = 0;
-    for (uint32_t j = l; j < end; ++j) {
-      st = restore_layer_from_host(c, j, buf[k] + pos);
-      if (st != LC_OK) {
-        cleanup();
-        return st;
-      }
-      pos += s->R[j];
-    }
-    if (hipEventRecord(done[k], c->stream) != hipSuccess) {
-      cleanup();
-      c->poisoned = true;
-      return fail(LC_ERR_HIP, "event record failed");
-    }
-    used[k] = true;
-    l = end;
-    k ^= 1;
-  }
+  st = restore_pipeline(s, c, choice, off, fds);
+  for (auto& kv : fds) close(kv.second);
+  if (st != LC_OK) return st;
   std::vector<int64_t> steps(s->N);
   for (uint32_t j = 0; j < s->N; ++j) steps[j] = s->durable[choice[j]].step;
   st = restore_finish(c, t_fail, steps);
-  cleanup();
   if (st != LC_OK) return st;
   if (chosen_step_out) std::memcpy(chosen_step_out, steps.data(), s->N * sizeof(int64_t));
   return LC_OK;

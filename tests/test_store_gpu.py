@@ -97,3 +97,67 @@ def test_store_rejects_other_layout(tmp_path):
         store.close()
     finally:
         p.close()
+
+
+def test_store_restore_pipeline_matches_device_restore(tmp_path):
+    """Records of about 300 MB (five 64 MiB read pieces each) whose total
+    exceeds the pinned restore ring, so the read pipeline wraps around it:
+    the composite restored from the store's files must equal, byte for byte,
+    the one the device restore (unpack kernel) builds from the same versions
+    held in device memory."""
+    import torch
+    from paper_2609_27193_amd import inputs as I
+    T = I.TensorSpec
+    n = 21_000_000
+    layers = tuple(I.LayerSpec(f"block_{l}", (T("w", n + 4097 * l, "matrix"),)) for l in range(6))
+    spec = I.ModelSpec(name="store-ring", layers=layers, weight_dtype="bf16", has_master=True,
+                       scale_rule="loguniform_0.01_1", target_fraction=0.4, s_max=3)
+    state = I.SyntheticState(spec, device="cuda")
+    stream = torch.cuda.current_stream().cuda_stream
+    segs = LC.segments_from_state(state)
+    lay = LC.LayoutDesc(segs, spec.n_layers, LC.LC_DT_BF16, True, LC.LC_MODE_ACCUM, [0.005] * spec.n_layers,
+                        spec.s_max, stream=stream)
+    _, R = LC.lc_query_layout(lay)
+    assert max(R) > (256 << 20) and sum(R) > max(2 * max(R), 1 << 30)
+    ctx = LC.lc_init_layout(lay)
+    store = LC.Store(str(tmp_path / "ring"), R)
+    versions = []
+    try:
+        def pack_append(t, mask):
+            nbytes = int(sum(R[l] for l in range(spec.n_layers) if mask[l]))
+            buf = torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+            if nbytes:
+                res = LC.lc_pack_selected(ctx, buf.data_ptr(), nbytes, 0)
+                assert res["done"] == 1
+            store.append(t, mask, buf.data_ptr() if nbytes else 0, nbytes, stream)
+            versions.append({"step": t, "mask": mask.copy(), "payload": buf.data_ptr() if nbytes else 0,
+                             "payload_bytes": nbytes, "buf": buf})
+
+        pack_append(0, np.ones(spec.n_layers, np.uint8))
+        for t in range(1, 4):
+            state.step(t)
+            LC.lc_score_layers(ctx, t)
+            mask, _ = LC.lc_select(ctx, t, 1.0, spec.n_layers)
+            pack_append(t, mask)
+        store.sync()
+        t_fail = 2
+        arrays = [a for a in (state.weight, state.shadow, state.master, state.exp_avg, state.exp_avg_sq)]
+
+        def wipe():
+            for a in arrays:
+                a.zero_()
+            torch.cuda.synchronize()
+
+        wipe()
+        chosen_store = store.restore(ctx, t_fail)
+        from_store = [a.clone() for a in arrays]
+        wipe()
+        chosen_dev = LC.lc_restore_composite(ctx, versions, t_fail, spec.n_layers)
+        torch.cuda.synchronize()
+        assert chosen_store.tolist() == chosen_dev.tolist()
+        log(f"  restored from steps {chosen_store.tolist()}; record set {sum(R) / 1e9:.2f} GB")
+        for a, b in zip(from_store, arrays):
+            assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+    finally:
+        store.close()
+        LC.lc_destroy(ctx)
