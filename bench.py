@@ -424,6 +424,11 @@ def main_store(args, spec):
     a = time.perf_counter()
     chosen = store.restore(ctx, t_fail)
     restore_s = time.perf_counter() - a
+    # again: the first restore's buffered reads left the records in the page
+    # cache, so this one measures the pipeline against the host link
+    a = time.perf_counter()
+    store.restore(ctx, t_fail)
+    restore_warm_s = time.perf_counter() - a
     store.close()
     LC.lc_destroy(ctx)
     out = {"metric": "persistence store: drain and composite-restore GB/s", "unit": "GB/s",
@@ -438,6 +443,7 @@ def main_store(args, spec):
            "stored_gb_before_compact": round(stored_before / 1e9, 3),
            "stored_gb_after_compact": round(stored_after / 1e9, 3), "compact_s": round(compact_s, 3),
            "restore_gbs": round(total / restore_s / 1e9, 3), "restore_s": round(restore_s, 3),
+           "restore_warm_gbs": round(total / restore_warm_s / 1e9, 3),
            "restored_timestamps": sorted(set(int(x) for x in chosen))}
     print(json.dumps(out), flush=True)
     shutil.rmtree(args.store_bench, ignore_errors=True)

@@ -92,5 +92,8 @@ namespace lc {
 // copies of one layer's record (device or host memory) into its arrays and
 // shadow; finish sets Delta = 0, t_l = steps and the call-order state.
 lc_status restore_layer_from_host(lc_ctx* c, uint32_t layer, const uint8_t* record);
+// The same for the bytes [rec_off, rec_off + len) of the layer's record,
+// held at `bytes` (host memory): only the parts of blocks inside the range.
+lc_status restore_range_from_host(lc_ctx* c, uint32_t layer, uint64_t rec_off, uint64_t len, const uint8_t* bytes);
 lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& steps);
 }  // namespace lc

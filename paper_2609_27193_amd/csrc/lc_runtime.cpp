@@ -266,6 +266,26 @@ lc_status restore_layer_from_host(lc_ctx* c, uint32_t l, const uint8_t* record) 
   return LC_OK;
 }
 
+lc_status restore_range_from_host(lc_ctx* c, uint32_t l, uint64_t rec_off, uint64_t len, const uint8_t* bytes) {
+  const HostLayout& L = c->L;
+  const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
+  uint32_t ub = 0;
+  for (uint32_t j = 0; j < l; ++j) ub += (L.layer_seg_begin[j + 1] - L.layer_seg_begin[j]) * per_seg;
+  const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * per_seg;
+  const uint64_t end = rec_off + len;
+  for (uint32_t k = 0; k < nu; ++k) {
+    const CopyUnit& u = L.units[ub + k];
+    const uint64_t a = std::max<uint64_t>(u.rec_off, rec_off), b = std::min<uint64_t>(u.rec_off + u.bytes, end);
+    if (a >= b) continue;  // this block (or its padding only) lies outside the range
+    void* dst = reinterpret_cast<void*>(u.arr + (a - u.rec_off));
+    LC_HIP(c, hipMemcpyAsync(dst, bytes + (a - rec_off), b - a, hipMemcpyHostToDevice, c->stream));
+    if (u.shadow)
+      LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.shadow + (a - u.rec_off)), dst, b - a,
+                               hipMemcpyDeviceToDevice, c->stream));
+  }
+  return LC_OK;
+}
+
 lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& steps) {
   const uint32_t N = c->L.N;
   std::vector<double> zeros(N, 0.0);

@@ -404,133 +404,103 @@ lc_status wait_idle(lc_store* s) {
 }
 
 // Reads the chosen record of every layer and restores it (Section 3.5 steps
-// 2-3) as one pipeline: reader threads pull 64 MiB pieces of the records, in
-// layer order and across layer boundaries, into a pinned byte ring; as soon
-// as a layer's pieces are all in, its host-to-device copies are enqueued on
-// the context's stream, and its ring space is reused once an event after
-// those copies has completed.  The disk never waits for a batch boundary.
+// 2-3) as one pipeline over fixed 64 MiB pieces of the records, in layer
+// order: reader threads fill a ring of pinned slots, each as soon as the
+// copies out of its previous piece have completed; the calling thread
+// enqueues each piece's host-to-device copies (the parts of the array blocks
+// the piece holds) as soon as it has been read, then records the slot's
+// event.  Neither the disk nor the host link waits for a layer boundary.
 lc_status restore_pipeline(lc_store* s, lc_ctx* c, const std::vector<size_t>& choice,
                            const std::vector<uint64_t>& off, std::map<size_t, int>& fds) {
-  const uint32_t N = s->N;
   constexpr uint64_t kPiece = 64ull << 20;
+  constexpr uint32_t kSlots = 32;  // 2 GiB of pinned read-ahead
   constexpr unsigned kReaders = 8;
-  const uint64_t max_rec = *std::max_element(s->R.begin(), s->R.end());
-  const uint64_t RB = std::max<uint64_t>(2 * max_rec, 1ull << 30);  // any record fits beside another
+  struct Piece { int fd; uint64_t src; uint32_t layer; uint64_t rec_off, len; };
+  std::vector<Piece> pieces;
+  for (uint32_t l = 0; l < s->N; ++l)
+    for (uint64_t o = 0; o < s->R[l]; o += kPiece)
+      pieces.push_back({fds[choice[l]], off[l] + o, l, o, std::min<uint64_t>(kPiece, s->R[l] - o)});
+  const size_t np = pieces.size();
   uint8_t* ring = nullptr;
   {
     void* p = nullptr;
-    const hipError_t e = hipHostMalloc(&p, RB, hipHostMallocDefault);
+    const hipError_t e = hipHostMalloc(&p, kSlots * kPiece, hipHostMallocDefault);
     if (e != hipSuccess) return fail(LC_ERR_OOM, "pinned restore ring: %s", hipGetErrorString(e));
     ring = static_cast<uint8_t*>(p);
   }
-  std::vector<hipEvent_t> ev(N, nullptr);
-  struct Piece { int fd; uint64_t src; uint8_t* dst; uint64_t len; uint32_t layer; };
+  std::vector<hipEvent_t> ev(kSlots, nullptr);
+  for (auto& e : ev)
+    if (hipEventCreateWithFlags(&e, hipEventDisableTiming) != hipSuccess) {
+      for (auto& x : ev)
+        if (x) (void)hipEventDestroy(x);
+      (void)hipHostFree(ring);
+      return fail(LC_ERR_HIP, "event create failed");
+    }
   std::mutex mu;
   std::condition_variable cv;
-  std::deque<Piece> queue;
-  std::vector<uint32_t> left(N, 0);  // pieces of each layer not yet read
-  bool stop = false, read_error = false;
+  std::vector<uint8_t> read_done(np, 0), issued(np, 0);
+  size_t next_piece = 0;
+  bool stop = false, failed = false;
   std::vector<std::thread> readers;
   for (unsigned r = 0; r < kReaders; ++r)
     readers.emplace_back([&] {
       for (;;) {
-        Piece pc;
+        size_t j;
         {
           std::unique_lock<std::mutex> lk(mu);
-          cv.wait(lk, [&] { return stop || !queue.empty(); });
-          if (queue.empty()) return;
-          pc = queue.front();
-          queue.pop_front();
+          if (stop || next_piece >= np) return;
+          j = next_piece++;
+          // the slot is free once the copies out of piece j - kSlots are done
+          if (j >= kSlots) cv.wait(lk, [&] { return stop || issued[j - kSlots]; });
+          if (stop) return;
         }
-        const bool ok = read_all(pc.fd, pc.dst, pc.len, pc.src);
+        bool ok = j < kSlots || hipEventSynchronize(ev[j % kSlots]) == hipSuccess;
+        const Piece& pc = pieces[j];
+        ok = ok && read_all(pc.fd, ring + (j % kSlots) * kPiece, pc.len, pc.src);
         {
           std::lock_guard<std::mutex> lk(mu);
-          if (!ok) read_error = true;
-          --left[pc.layer];
+          if (ok) read_done[j] = 1;
+          else failed = true;
         }
         cv.notify_all();
       }
     });
-  struct Slot { uint64_t begin, end; uint32_t layer; };
-  std::deque<Slot> live;  // ring ranges in allocation order
-  uint64_t head = 0;
-  uint32_t next_alloc = 0, next_copy = 0;
   lc_status st = LC_OK;
-  auto overlaps = [&](uint64_t a, uint64_t e) {
-    for (const Slot& sl : live)
-      if (a < sl.end && sl.begin < e) return true;
-    return false;
-  };
-  while (st == LC_OK && next_copy < N) {
-    // place and queue the reads of as many layers as the ring holds
-    bool progressed = false;
-    while (next_alloc < N) {
-      const uint64_t R = s->R[next_alloc];
-      const uint64_t a = head + R <= RB ? head : 0;
-      if (overlaps(a, a + R)) break;
-      live.push_back({a, a + R, next_alloc});
-      head = a + R;
-      {
-        std::lock_guard<std::mutex> lk(mu);
-        const int fd = fds[choice[next_alloc]];
-        uint32_t n = 0;
-        for (uint64_t o = 0; o < R; o += kPiece, ++n)
-          queue.push_back({fd, off[next_alloc] + o, ring + a + o, std::min<uint64_t>(kPiece, R - o), next_alloc});
-        left[next_alloc] = n;
-      }
-      cv.notify_all();
-      ++next_alloc;
-      progressed = true;
-    }
-    // the ring is full: reclaim the oldest range once its copies are done
-    if (next_alloc < N && !progressed && !live.empty() && live.front().layer < next_copy) {
-      const hipError_t e = hipEventSynchronize(ev[live.front().layer]);
-      if (e != hipSuccess) {
-        c->poisoned = true;
-        st = fail(LC_ERR_HIP, "restore copy failed: %s", hipGetErrorString(e));
-        break;
-      }
-      live.pop_front();
-      continue;
-    }
-    // enqueue the copies of the next layer once all its pieces are in
-    if (next_copy >= next_alloc) {  // cannot happen: an empty ring holds any record
-      st = fail(LC_ERR_INVALID_ARG, "internal: restore pipeline stalled at layer %u", next_copy);
-      break;
-    }
+  for (size_t i = 0; i < np && st == LC_OK; ++i) {
     {
       std::unique_lock<std::mutex> lk(mu);
-      cv.wait(lk, [&] { return read_error || left[next_copy] == 0; });
-      if (read_error) {
+      cv.wait(lk, [&] { return failed || read_done[i]; });
+      if (!read_done[i]) {
         st = fail(LC_ERR_INVALID_ARG, "reading a stored record failed");
         break;
       }
     }
-    const Slot* slot = nullptr;
-    for (const Slot& sl : live)
-      if (sl.layer == next_copy) slot = &sl;
-    st = restore_layer_from_host(c, next_copy, ring + slot->begin);
+    const Piece& pc = pieces[i];
+    st = restore_range_from_host(c, pc.layer, pc.rec_off, pc.len, ring + (i % kSlots) * kPiece);
     if (st != LC_OK) break;
-    hipError_t e = hipEventCreateWithFlags(&ev[next_copy], hipEventDisableTiming);
-    if (e == hipSuccess) e = hipEventRecord(ev[next_copy], c->stream);
-    if (e != hipSuccess) {
+    if (hipEventRecord(ev[i % kSlots], c->stream) != hipSuccess) {
       c->poisoned = true;
-      st = fail(LC_ERR_HIP, "event record failed: %s", hipGetErrorString(e));
+      st = fail(LC_ERR_HIP, "event record failed");
       break;
     }
-    ++next_copy;
+    {
+      std::lock_guard<std::mutex> lk(mu);
+      issued[i] = 1;
+    }
+    cv.notify_all();
   }
   {
     std::lock_guard<std::mutex> lk(mu);
     stop = true;
-    queue.clear();
   }
   cv.notify_all();
   for (auto& th : readers) th.join();
   // the ring must outlive every copy that reads it
-  (void)hipStreamSynchronize(c->stream);
-  for (hipEvent_t e : ev)
-    if (e) (void)hipEventDestroy(e);
+  if (hipStreamSynchronize(c->stream) != hipSuccess && st == LC_OK) {
+    c->poisoned = true;
+    st = fail(LC_ERR_HIP, "restore copies failed");
+  }
+  for (hipEvent_t e : ev) (void)hipEventDestroy(e);
   (void)hipHostFree(ring);
   return st;
 }
