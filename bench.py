@@ -22,6 +22,7 @@ import hashlib
 import json
 import math
 import os
+import subprocess
 import sys
 import time
 
@@ -52,6 +53,9 @@ def parse():
                     help="also run one plain 4 GiB device copy (counter calibration)")
     ap.add_argument("--adamw", action="store_true",
                     help="drive the state with the fused AdamW + drift step instead of the standalone score")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="run the HBM ceiling probe (read, copy, 2-read-1-write streams with the kernels' "
+                         "tile and block mapping) and print its JSON line")
     ap.add_argument("--torch-adamw-reference", action="store_true",
                     help="with --adamw: also time torch's fused AdamW (no drift) on the same parameter "
                          "shapes, plus the bf16 weight copy, as a reference point")
@@ -191,6 +195,16 @@ def main():
         print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1 "
                                    "(the decision step is per-rank, see the design notes on sharding)"}))
         sys.exit(2)
+    if args.ceilings:
+        # a child process of its own: this process has not touched the GPU yet
+        from paper_2609_27193_amd.build_lib import HBM_PROBE
+        if not os.path.exists(HBM_PROBE):
+            raise SystemExit("the HBM probe is built by __graft_entry__.build()")
+        r = subprocess.run([HBM_PROBE], capture_output=True, text=True, timeout=600)
+        if r.returncode != 0:
+            raise SystemExit(r.stderr)
+        print(r.stdout.strip(), flush=True)
+        return
     import torch
     from paper_2609_27193_amd import inputs as I
     from paper_2609_27193_amd import layercheck as LC

@@ -64,6 +64,24 @@ def build(verbose: bool = False, out: str = LIB, defines=(), sanitize: bool = Fa
     return out
 
 
+HBM_PROBE = os.path.join(HERE, "lc_hbm_probe")
+
+
+def build_hbm_probe(verbose: bool = False) -> str:
+    """Compile the stand-alone HBM ceiling probe (``bench.py --ceilings``)."""
+    cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17",
+           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
+           "-o", HBM_PROBE + ".tmp", os.path.join(CSRC, "hbm_probe.hip")]
+    if verbose:
+        print(" ".join(cmd), flush=True)
+    res = subprocess.run(cmd, capture_output=True, text=True)
+    if res.returncode != 0:
+        sys.stderr.write(res.stdout + res.stderr)
+        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+    os.replace(HBM_PROBE + ".tmp", HBM_PROBE)
+    return HBM_PROBE
+
+
 C_CLIENT_SRC = os.path.join(ROOT, "tests", "c_client", "lc_c_client.c")
 C_CLIENT = os.path.join(ROOT, "tests", "c_client", "lc_c_client")
 
@@ -93,3 +111,4 @@ if __name__ == "__main__":
     print(build(verbose=True))
     print(build_c_client(verbose=True))
     print(build(verbose=True, out=SANITIZED_LIB, sanitize=True))
+    print(build_hbm_probe(verbose=True))
