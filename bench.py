@@ -538,6 +538,8 @@ def main_restore(args, spec):
             best = wall if best is None else min(best, wall)
         return best, chosen
 
+    if args.copy_calibration:
+        copy_calibration(dev)
     dev_s, chosen = timed(versions)
     if with_host:
         host_s, chosen_h = timed(host)
