@@ -24,9 +24,10 @@ LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
-            "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_store_open", "lc_store_append", "lc_store_sync",
-            "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore", "lc_store_compact", "lc_store_close",
-            "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
+            "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_store_open", "lc_store_append",
+            "lc_store_sync", "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore",
+            "lc_store_compact", "lc_store_close", "lc_read_state", "lc_record_bytes", "lc_destroy",
+            "lc_last_error")
 
 
 class lc_segment(C.Structure):
