@@ -16,8 +16,14 @@ namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
-__device__ __forceinline__ u32x4 ld_nt(const u32x4* p) { return __builtin_nontemporal_load(p); }
-__device__ __forceinline__ void st_nt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, p); }
+// Every array the kernels stream is device (global) memory; accessing it
+// through global-address-space pointers gives global_load/global_store
+// instead of flat accesses (no aperture check, no LDS-counter coupling).
+typedef __attribute__((address_space(1))) u32x4 g_u32x4;
+__device__ __forceinline__ u32x4 ld_nt(const u32x4* p) {
+  return __builtin_nontemporal_load((const g_u32x4*)p);
+}
+__device__ __forceinline__ void st_nt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, (g_u32x4*)p); }
 
 // bf16 -> fp32 is exact: the bf16 bits are the top half of the fp32 bits.
 __device__ __forceinline__ float bf_lo(uint32_t x) { return __uint_as_float(x << 16); }
@@ -456,6 +462,9 @@ __global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables
 
 // ---- fused AdamW step + drift (Eq. 1-2 on the optimizer's parameters) -------
 typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(1))) u32x2 g_u32x2;
+__device__ __forceinline__ u32x2 ld_nt2(const u32x2* p) { return __builtin_nontemporal_load((const g_u32x2*)p); }
+__device__ __forceinline__ void st_nt2(u32x2* p, u32x2 v) { __builtin_nontemporal_store(v, (g_u32x2*)p); }
 
 __device__ __forceinline__ uint16_t bf16_rne(float f) {
   uint32_t u = __float_as_uint(f);
@@ -506,7 +515,7 @@ struct Group4 {
     if constexpr (MASTER) {
       p = ld_nt(reinterpret_cast<const u32x4*>(sg.master) + gi);
     } else if constexpr (WDT == 1) {
-      const u32x2 w = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(sg.w) + gi);
+      const u32x2 w = ld_nt2(reinterpret_cast<const u32x2*>(sg.w) + gi);
       p = u32x4{w[0] << 16, w[0] & 0xffff0000u, w[1] << 16, w[1] & 0xffff0000u};
     } else {
       p = ld_nt(reinterpret_cast<const u32x4*>(sg.w) + gi);
@@ -514,7 +523,7 @@ struct Group4 {
     m = ld_nt(reinterpret_cast<const u32x4*>(sg.m) + gi);
     v = ld_nt(reinterpret_cast<const u32x4*>(sg.v) + gi);
     if constexpr (GDT == 1) {
-      const u32x2 x = __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(gs.grad) + gi);
+      const u32x2 x = ld_nt2(reinterpret_cast<const u32x2*>(gs.grad) + gi);
       g[0] = __uint_as_float(x[0] << 16); g[1] = __uint_as_float(x[0] & 0xffff0000u);
       g[2] = __uint_as_float(x[1] << 16); g[3] = __uint_as_float(x[1] & 0xffff0000u);
     } else {
@@ -546,7 +555,7 @@ struct Group4 {
     if constexpr (WDT == 1) {
       const uint32_t lo = bf16_rne(__uint_as_float(pn[0])) | (static_cast<uint32_t>(bf16_rne(__uint_as_float(pn[1]))) << 16);
       const uint32_t hi = bf16_rne(__uint_as_float(pn[2])) | (static_cast<uint32_t>(bf16_rne(__uint_as_float(pn[3]))) << 16);
-      __builtin_nontemporal_store(u32x2{lo, hi}, reinterpret_cast<u32x2*>(sg.w) + gi);
+      st_nt2(reinterpret_cast<u32x2*>(sg.w) + gi, u32x2{lo, hi});
     } else {
       st_nt(reinterpret_cast<u32x4*>(sg.w) + gi, pn);
     }
