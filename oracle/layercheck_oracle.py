@@ -203,6 +203,24 @@ def adamw_update(p: np.ndarray, m: np.ndarray, v: np.ndarray, g: np.ndarray, sc:
     return p_new, m_new.astype(f), v_new.astype(f)
 
 
+# Section 4.7 notes the method applies to plain SGD, persisting the weights
+# without per-parameter optimizer state.  One SGD step with decoupled weight
+# decay, fp32, one rounding per operation:
+#   p_new = p * (1 - lr * wd) - lr * g      (the decay only for decayed groups)
+
+
+def sgd_scalars(lr: float, weight_decay: float) -> dict:
+    f = np.float32
+    return {"lr": f(lr), "decay": f(1.0 - lr * weight_decay)}
+
+
+def sgd_update(p: np.ndarray, g: np.ndarray, sc: dict, decayed: bool) -> np.ndarray:
+    """One SGD step on fp32 arrays; returns p_new."""
+    f = np.float32
+    p1 = (p * sc["decay"]).astype(f) if decayed else p.astype(f)
+    return (p1 - (sc["lr"] * g.astype(f)).astype(f)).astype(f)
+
+
 def bf16_round(x: np.ndarray) -> np.ndarray:
     """fp32 -> bf16 bits, round to nearest even (NaN kept as a quiet NaN)."""
     b = x.astype(np.float32).view(np.uint32).astype(np.uint64)
@@ -267,19 +285,17 @@ class LayerCheckOracle:
         self.unpacked = set(range(n_layers))
 
     # -- Section 3.4: AdamW step with the drift taken from the update --------
-    def adamw_step_score(self, step: int, grads, lr: float, beta1: float, beta2: float, eps: float,
-                         weight_decay: float, adam_t: int, decayed=None) -> None:
-        """``grads``: one fp32 array per segment (bf16 gradients widened
-        exactly); ``decayed``: per-segment weight-decay flags (the paper's
-        with/without weight-decay parameter groups, Section 3.4), all True
-        when None."""
+    def _optimizer_step(self, step: int, grads, decayed, update) -> None:
+        """Section 3.4: the optimizer updates every segment's parameters (the
+        fp32 master when present, else the weights widened to fp32); the
+        weights are written back (round to nearest even for bf16), and the
+        drift of each layer is Eq. 1 on its parameters before and after the
+        update, accumulated by Eq. 2.  ``update(segment, p_old, g, decayed)``
+        returns p_new and updates any optimizer state of the segment."""
         if step <= self.last_step:
             raise OracleError(LC_ERR_BAD_STATE, "decision steps must strictly increase")
         if self.mode != MODE_ACCUM:
             raise OracleError(LC_ERR_BAD_STATE, "the fused optimizer step accumulates (ACCUM mode)")
-        if not self.has_moments:
-            raise OracleError(LC_ERR_BAD_STATE, "AdamW needs the moment arrays")
-        sc = adamw_scalars(lr, beta1, beta2, eps, weight_decay, adam_t)
         segs = [s for g in self.by_layer for s in g]
         for i, (s, g) in enumerate(zip(segs, grads)):
             if s.master is not None:
@@ -287,9 +303,7 @@ class LayerCheckOracle:
             else:
                 p_old = widen(s.weight, self.dtype).astype(np.float32)
             dec = True if decayed is None else bool(decayed[i])
-            p_new, m_new, v_new = adamw_update(p_old, s.exp_avg, s.exp_avg_sq, g, sc, dec)
-            s.exp_avg[...] = m_new
-            s.exp_avg_sq[...] = v_new
+            p_new = update(s, p_old, g, dec)
             if s.master is not None:
                 s.master[...] = p_new
             s.weight[...] = bf16_round(p_new) if self.dtype == DT_BF16 else p_new
@@ -305,6 +319,31 @@ class LayerCheckOracle:
         self.scored_step = step
         self.unpacked = set()
         self.mask = None
+
+    def adamw_step_score(self, step: int, grads, lr: float, beta1: float, beta2: float, eps: float,
+                         weight_decay: float, adam_t: int, decayed=None) -> None:
+        """``grads``: one fp32 array per segment (bf16 gradients widened
+        exactly); ``decayed``: per-segment weight-decay flags (the paper's
+        with/without weight-decay parameter groups, Section 3.4), all True
+        when None."""
+        if step > self.last_step and self.mode == MODE_ACCUM and not self.has_moments:
+            raise OracleError(LC_ERR_BAD_STATE, "AdamW needs the moment arrays")
+        sc = adamw_scalars(lr, beta1, beta2, eps, weight_decay, adam_t)
+
+        def update(s, p_old, g, dec):
+            p_new, m_new, v_new = adamw_update(p_old, s.exp_avg, s.exp_avg_sq, g, sc, dec)
+            s.exp_avg[...] = m_new
+            s.exp_avg_sq[...] = v_new
+            return p_new
+
+        self._optimizer_step(step, grads, decayed, update)
+
+    # -- Section 4.7: SGD step with the drift taken from the update ----------
+    def sgd_step_score(self, step: int, grads, lr: float, weight_decay: float, decayed=None) -> None:
+        """As ``adamw_step_score`` for plain SGD; Adam moments, if the layout
+        has them, are left as they are."""
+        sc = sgd_scalars(lr, weight_decay)
+        self._optimizer_step(step, grads, decayed, lambda s, p_old, g, dec: sgd_update(p_old, g, sc, dec))
 
     # -- Eq. 1-2 -------------------------------------------------------------
     def score(self, step: int) -> None:

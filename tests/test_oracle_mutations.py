@@ -9,6 +9,7 @@ import pytest
 from oracle import layercheck_oracle as O
 from tests import oracle_pins as P
 from tests import test_oracle_adamw as A
+from tests import test_oracle_sgd as G
 from tests.test_bruteforce_tiny import run_bruteforce
 
 SRC = open(O.__file__).read()
@@ -54,8 +55,14 @@ MUTANTS = {
     "adamw_no_bias_correction": ('"c1": f(1.0 / (1.0 - beta1 ** t)), "c2": f(1.0 / (1.0 - beta2 ** t)),',
                                  '"c1": f(1.0), "c2": f(1.0),'),
     "adamw_coupled_decay": ("    g = g.astype(f)\n    m_new", "    g = (g.astype(f) + (1.0 - sc['decay']) / sc['lr'] * p).astype(f) if decayed else g.astype(f)\n    m_new"),
-    "adamw_decay_ignores_group": ("p1 = (p * sc[\"decay\"]).astype(f) if decayed else p.astype(f)",
-                                  "p1 = (p * sc[\"decay\"]).astype(f)"),
+    "adamw_decay_ignores_group": ("p1 = (p * sc[\"decay\"]).astype(f) if decayed else p.astype(f)\n    p_new =",
+                                  "p1 = (p * sc[\"decay\"]).astype(f)\n    p_new ="),
+    "sgd_decay_ignores_group": ("p1 = (p * sc[\"decay\"]).astype(f) if decayed else p.astype(f)\n    return (p1 -",
+                                "p1 = (p * sc[\"decay\"]).astype(f)\n    return (p1 -"),
+    "sgd_sign_flipped": ("return (p1 - (sc[\"lr\"] * g.astype(f)).astype(f)).astype(f)",
+                         "return (p1 + (sc[\"lr\"] * g.astype(f)).astype(f)).astype(f)"),
+    "sgd_decay_without_lr": ("return {\"lr\": f(lr), \"decay\": f(1.0 - lr * weight_decay)}",
+                          "return {\"lr\": f(lr), \"decay\": f(1.0 - weight_decay)}"),
     "adamw_eps_inside_sqrt": ("denom = (np.sqrt(v_hat).astype(f) + sc[\"eps\"]).astype(f)",
                               "denom = np.sqrt((v_hat + sc[\"eps\"]).astype(f)).astype(f)"),
     "adamw_drift_on_new_params": ("_, _, _, u = layer_update_score([s._p_new for s in g], [s._p_old for s in g], DT_F32, self.eps_w)",
@@ -92,7 +99,9 @@ def all_checks(M):
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
         yield lambda mode=mode: run_bruteforce(M, mode, O.DT_BF16, 0, steps=12)
     for chk in (A.test_first_step_is_lr_times_sign, A.test_decoupled_weight_decay_on_zero_gradient,
-                A.test_matches_torch_adamw_over_steps, A.test_fused_step_drift_is_eq1_on_the_parameters):
+                A.test_matches_torch_adamw_over_steps, A.test_fused_step_drift_is_eq1_on_the_parameters,
+                G.test_closed_form_exact, G.test_decoupled_weight_decay, G.test_matches_torch_sgd,
+                G.test_drift_is_eq1_on_the_parameters):
         yield lambda chk=chk: chk(M)
 
 
