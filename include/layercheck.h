@@ -226,6 +226,25 @@ lc_status lc_rebase(lc_ctx *c, int64_t step);
 lc_status lc_adamw_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,
                               const uint8_t *decay_mask, const lc_adamw_params *p);
 
+/* Hyper-parameters of one plain SGD step (decoupled weight decay). */
+typedef struct {
+  double lr;           /* learning rate of this step, >= 0                     */
+  double weight_decay; /* decoupled decay for segments flagged in decay_mask   */
+} lc_sgd_params;
+
+/* The same for plain SGD, to which Section 4.7 notes the method carries over
+ * (records then need no optimizer state: a layout without Adam moments).  For
+ * every element, in fp32 with one rounding per operation:
+ *   p_new = p * (1 - lr wd) - lr * g      (the decay only where decay_mask)
+ * where p is the fp32 master (or the weights themselves when there is no
+ * master); the master and the weights (round-to-nearest-even image of p_new)
+ * are written back; Adam moments, if the layout has them, are not touched.
+ * Eq. 1 on the parameters before and after the update, Eq. 2 into Delta_l.
+ * Arguments, call sequence and errors as lc_adamw_step_score, except that no
+ * moments are needed.  Asynchronous. */
+lc_status lc_sgd_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,
+                            const uint8_t *decay_mask, const lc_sgd_params *p);
+
 /* ---- Persistence store (Section 3.5 "Metadata-driven reconstruction") ------
  * A directory of version files plus an append-only manifest recording the
  * persistence history: per version its step, its layer mask and its payload

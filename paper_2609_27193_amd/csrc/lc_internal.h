@@ -1,5 +1,6 @@
 // Internal tables and kernel launchers of the LayerCheck HIP library.
-// Shared by the host runtime (lc_runtime.cpp) and the kernels (lc_kernels.hip).
+// Shared by the host runtime (lc_runtime.cpp) and the kernels (lc_kernels.hip,
+// lc_optim.hip).
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -60,12 +61,12 @@ struct CopyUnit {
   uint32_t pad;
 };
 
-// One segment as the fused optimizer kernel sees it (static part).
+// One segment as the optimizer kernels see it (static part).
 struct OptSeg {
   uint64_t w;            // weights (bf16 or fp32)
   uint64_t master;       // fp32 master, 0 when absent
-  uint64_t m;            // fp32 Adam first moment
-  uint64_t v;            // fp32 Adam second moment
+  uint64_t m;            // fp32 Adam first moment (AdamW only)
+  uint64_t v;            // fp32 Adam second moment (AdamW only)
   uint64_t numel;
   uint32_t chunk_begin;  // same chunks as the score kernel
   uint32_t vec_ok;       // master/m/v 16-B aligned and weights aligned to 4 elements
@@ -81,6 +82,11 @@ struct GradSeg {
 // fp32 scalars of one AdamW step, formed in fp64 on the host and rounded once.
 struct AdamScalars {
   float b1, omb1, b2, omb2, c1, c2, eps, lr, decay;
+};
+
+// fp32 scalars of one SGD step: lr and the decoupled decay factor 1 - lr wd.
+struct SgdScalars {
+  float lr, decay;
 };
 
 // Written by the select kernel, copied to pinned host memory, followed by the
@@ -124,7 +130,7 @@ struct DeviceTables {
   uint64_t* sel_rec_prefix;           // [N+1] record byte offsets by rank
   uint64_t* sel_piece_prefix;         // [N+1] piece offsets by rank
   SelectHeader* result;               // header + mask[N]
-  const OptSeg* opt_segs;              // [n_segments]
+  const OptSeg* opt_segs;             // [n_segments]
   const GradSeg* grad_segs;           // [n_segments], refreshed per optimizer call
   // restore scratch
   uint32_t* rank_layer;               // [N]
@@ -133,7 +139,10 @@ struct DeviceTables {
 };
 
 // Launchers: return hipGetLastError() of the launches.
+// launch_score: score kernel, then the finalize kernel (u and Delta).
 hipError_t launch_score(const DeviceTables& t, hipStream_t st);
+// Eq. 1-2 from the per-chunk partials alone (after an optimizer step).
+hipError_t launch_finalize(const DeviceTables& t, hipStream_t st);
 hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode,
                          hipStream_t st);
 hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last_rank,
@@ -141,7 +150,9 @@ hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last
                        void* staging, int refresh_shadow, hipStream_t st);
 hipError_t launch_unpack(const DeviceTables& t, uint32_t n_ranks, uint64_t n_pieces,
                          hipStream_t st);
+// Optimizer steps writing the per-chunk drift partials (lc_optim.hip).
 hipError_t launch_adamw(const DeviceTables& t, int grad_dtype, int has_master, const AdamScalars& sc,
                         hipStream_t st);
+hipError_t launch_sgd(const DeviceTables& t, int grad_dtype, int has_master, const SgdScalars& sc, hipStream_t st);
 
 }  // namespace lc

@@ -9,25 +9,10 @@
 //    fixed-order per-layer sum, so scores are bitwise reproducible;
 //  * wave64 reductions (DPP quad permutes, then cross-row shuffles), LDS for
 //    the cross-wave combine.
-#include "lc_internal.h"
+#include "lc_device.h"
 
 namespace lc {
 namespace {
-
-typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-
-// Every array the kernels stream is device (global) memory; accessing it
-// through global-address-space pointers gives global_load/global_store
-// instead of flat accesses (no aperture check, no LDS-counter coupling).
-typedef __attribute__((address_space(1))) u32x4 g_u32x4;
-__device__ __forceinline__ u32x4 ld_nt(const u32x4* p) {
-  return __builtin_nontemporal_load((const g_u32x4*)p);
-}
-__device__ __forceinline__ void st_nt(u32x4* p, u32x4 v) { __builtin_nontemporal_store(v, (g_u32x4*)p); }
-
-// bf16 -> fp32 is exact: the bf16 bits are the top half of the fp32 bits.
-__device__ __forceinline__ float bf_lo(uint32_t x) { return __uint_as_float(x << 16); }
-__device__ __forceinline__ float bf_hi(uint32_t x) { return __uint_as_float(x & 0xffff0000u); }
 
 // |W - S| and |S| of one 16-byte vector, summed pairwise in fp32.
 template <int DT>
@@ -76,77 +61,6 @@ __device__ __forceinline__ void elem_copy(const uint8_t* src, uint8_t* dst, uint
   }
 }
 
-__device__ __forceinline__ uint64_t round_up(uint64_t x, uint64_t a) { return (x + a - 1) / a * a; }
-
-// Work item x of a launch of G blocks.  Workgroups are dispatched round-robin
-// over the 8 XCDs; with LC_XCD_REMAP each XCD instead walks one contiguous
-// eighth of the items (a bijection on the first 8*floor(G/8) items, identity
-// on the rest), which keeps each XCD's in-flight accesses within a narrow
-// address window.
-__device__ __forceinline__ uint32_t remap_xcd(uint32_t x, uint32_t G) {
-#if LC_XCD_REMAP && LC_XCD_RUN > 0
-  // runs of LC_XCD_RUN consecutive items per XCD, the XCDs' runs interleaved
-  constexpr uint32_t R = 8u * LC_XCD_RUN;
-  const uint32_t full = G - G % R;
-  if (x >= full) return x;
-  const uint32_t xcd = x % 8u, k = x / 8u;
-  return (k / LC_XCD_RUN) * R + xcd * LC_XCD_RUN + k % LC_XCD_RUN;
-#elif LC_XCD_REMAP
-  const uint32_t full = G - G % 8u;
-  return x < full ? (x % 8u) * (full / 8u) + x / 8u : x;
-#else
-  (void)G;
-  return x;
-#endif
-}
-
-// ---- wave64 / block reductions of an fp64 pair, fixed order ------------------
-__device__ __forceinline__ double dpp_f64(double v, int ctrl_sel) {
-  int lo = __double2loint(v), hi = __double2hiint(v);
-  if (ctrl_sel == 0) {  // quad_perm [1,0,3,2]: partner = lane ^ 1
-    lo = __builtin_amdgcn_update_dpp(0, lo, 0xB1, 0xF, 0xF, false);
-    hi = __builtin_amdgcn_update_dpp(0, hi, 0xB1, 0xF, 0xF, false);
-  } else {              // quad_perm [2,3,0,1]: partner = lane ^ 2
-    lo = __builtin_amdgcn_update_dpp(0, lo, 0x4E, 0xF, 0xF, false);
-    hi = __builtin_amdgcn_update_dpp(0, hi, 0x4E, 0xF, 0xF, false);
-  }
-  return __hiloint2double(hi, lo);
-}
-
-__device__ __forceinline__ void wave_sum2(double& a, double& b) {
-  a += dpp_f64(a, 0);
-  b += dpp_f64(b, 0);
-  a += dpp_f64(a, 1);
-  b += dpp_f64(b, 1);
-#pragma unroll
-  for (int m = 4; m < 64; m <<= 1) {
-    a += __shfl_xor(a, m, 64);
-    b += __shfl_xor(b, m, 64);
-  }
-}
-
-// Sum of (a, b) over a block of NT threads; the result is valid in thread 0.
-template <int NT>
-__device__ __forceinline__ void block_sum2(double& a, double& b) {
-  __shared__ double sa[NT / 64], sb[NT / 64];
-  wave_sum2(a, b);
-  const int wave = threadIdx.x >> 6;
-  if ((threadIdx.x & 63) == 0) {
-    sa[wave] = a;
-    sb[wave] = b;
-  }
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    double x = sa[0], y = sb[0];
-#pragma unroll
-    for (int w = 1; w < NT / 64; ++w) {
-      x += sa[w];
-      y += sb[w];
-    }
-    a = x;
-    b = y;
-  }
-}
 
 // ---- score: one chunk per block and iteration ---------------------------------
 // Streams W and S of one chunk once; writes (sum|W-S|, sum|S|) in fp64.  In
@@ -460,192 +374,6 @@ __global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables
   }
 }
 
-// ---- fused AdamW step + drift (Eq. 1-2 on the optimizer's parameters) -------
-typedef unsigned int u32x2 __attribute__((ext_vector_type(2)));
-typedef __attribute__((address_space(1))) u32x2 g_u32x2;
-__device__ __forceinline__ u32x2 ld_nt2(const u32x2* p) { return __builtin_nontemporal_load((const g_u32x2*)p); }
-__device__ __forceinline__ void st_nt2(u32x2* p, u32x2 v) { __builtin_nontemporal_store(v, (g_u32x2*)p); }
-
-__device__ __forceinline__ uint16_t bf16_rne(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7FC0u;  // NaN stays a quiet NaN
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return static_cast<uint16_t>(u >> 16);
-}
-
-// One AdamW element update in fp32, one rounding per operation, fixed order.
-// The library is built with -ffp-contract=off (no fused multiply-adds), and
-// fp32 division and sqrtf compile to their correctly rounded sequences
-// (div_scale/div_fmas/div_fixup; v_sqrt with neighbour correction), so every
-// operation below is the IEEE round-to-nearest-even result.
-__device__ __forceinline__ float adamw_elem(float p, float& m, float& v, float g, const AdamScalars& sc,
-                                            bool decay) {
-  m = sc.b1 * m + sc.omb1 * g;
-  v = sc.b2 * v + sc.omb2 * (g * g);
-  const float mh = m * sc.c1;
-  const float vh = v * sc.c2;
-  const float den = sqrtf(vh) + sc.eps;
-  const float upd = mh / den;
-  const float p1 = decay ? p * sc.decay : p;
-  return p1 - sc.lr * upd;
-}
-
-template <int WDT>
-__device__ __forceinline__ float w_load(const uint8_t* w, uint64_t i) {
-  if constexpr (WDT == 1) return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(w)[i]) << 16);
-  else return reinterpret_cast<const float*>(w)[i];
-}
-template <int WDT>
-__device__ __forceinline__ void w_store(uint8_t* w, uint64_t i, float x) {
-  if constexpr (WDT == 1) reinterpret_cast<uint16_t*>(w)[i] = bf16_rne(x);
-  else reinterpret_cast<float*>(w)[i] = x;
-}
-template <int GDT>
-__device__ __forceinline__ float g_load(const uint8_t* g, uint64_t i) {
-  if constexpr (GDT == 1) return __uint_as_float(static_cast<uint32_t>(reinterpret_cast<const uint16_t*>(g)[i]) << 16);
-  else return reinterpret_cast<const float*>(g)[i];
-}
-
-// Four consecutive elements starting at element 4*gi (all arrays 4-element aligned).
-template <int WDT, int GDT, bool MASTER>
-struct Group4 {
-  u32x4 p, m, v;
-  float g[4];
-  __device__ __forceinline__ void load(const OptSeg& sg, const GradSeg& gs, uint64_t gi) {
-    if constexpr (MASTER) {
-      p = ld_nt(reinterpret_cast<const u32x4*>(sg.master) + gi);
-    } else if constexpr (WDT == 1) {
-      const u32x2 w = ld_nt2(reinterpret_cast<const u32x2*>(sg.w) + gi);
-      p = u32x4{w[0] << 16, w[0] & 0xffff0000u, w[1] << 16, w[1] & 0xffff0000u};
-    } else {
-      p = ld_nt(reinterpret_cast<const u32x4*>(sg.w) + gi);
-    }
-    m = ld_nt(reinterpret_cast<const u32x4*>(sg.m) + gi);
-    v = ld_nt(reinterpret_cast<const u32x4*>(sg.v) + gi);
-    if constexpr (GDT == 1) {
-      const u32x2 x = ld_nt2(reinterpret_cast<const u32x2*>(gs.grad) + gi);
-      g[0] = __uint_as_float(x[0] << 16); g[1] = __uint_as_float(x[0] & 0xffff0000u);
-      g[2] = __uint_as_float(x[1] << 16); g[3] = __uint_as_float(x[1] & 0xffff0000u);
-    } else {
-      const u32x4 x = ld_nt(reinterpret_cast<const u32x4*>(gs.grad) + gi);
-      for (int k = 0; k < 4; ++k) g[k] = __uint_as_float(x[k]);
-    }
-  }
-  // update in place; returns the drift terms (sum|p_new - p|, sum|p|) of the group
-  __device__ __forceinline__ void step_store(const OptSeg& sg, uint64_t gi, const AdamScalars& sc, bool decay,
-                                             float& da, float& db) {
-    float d[4], b[4];
-    u32x4 pn, mn, vn;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      const float po = __uint_as_float(p[k]);
-      float mm = __uint_as_float(m[k]), vv = __uint_as_float(v[k]);
-      const float x = adamw_elem(po, mm, vv, g[k], sc, decay);
-      pn[k] = __float_as_uint(x);
-      mn[k] = __float_as_uint(mm);
-      vn[k] = __float_as_uint(vv);
-      d[k] = fabsf(x - po);
-      b[k] = fabsf(po);
-    }
-    da = (d[0] + d[1]) + (d[2] + d[3]);
-    db = (b[0] + b[1]) + (b[2] + b[3]);
-    st_nt(reinterpret_cast<u32x4*>(sg.m) + gi, mn);
-    st_nt(reinterpret_cast<u32x4*>(sg.v) + gi, vn);
-    if constexpr (MASTER) st_nt(reinterpret_cast<u32x4*>(sg.master) + gi, pn);
-    if constexpr (WDT == 1) {
-      const uint32_t lo = bf16_rne(__uint_as_float(pn[0])) | (static_cast<uint32_t>(bf16_rne(__uint_as_float(pn[1]))) << 16);
-      const uint32_t hi = bf16_rne(__uint_as_float(pn[2])) | (static_cast<uint32_t>(bf16_rne(__uint_as_float(pn[3]))) << 16);
-      st_nt2(reinterpret_cast<u32x2*>(sg.w) + gi, u32x2{lo, hi});
-    } else {
-      st_nt(reinterpret_cast<u32x4*>(sg.w) + gi, pn);
-    }
-  }
-};
-
-template <int WDT, int GDT, bool MASTER>
-__device__ __forceinline__ void adamw_chunk(const DeviceTables& t, const AdamScalars& sc, uint32_t c) {
-  constexpr uint32_t WSZ = WDT == 1 ? 2 : 4;
-  constexpr uint32_t CE = kChunkBytes / WSZ;        // elements per chunk (the score chunks)
-  constexpr uint32_t GPT = CE / 4 / kScoreThreads;  // 4-element groups per thread in a full chunk
-  static_assert(GPT >= 1 && CE % (4 * kScoreThreads) == 0, "tiling");
-  const uint32_t tid = threadIdx.x;
-  const uint32_t si = t.chunk_seg[c];
-  const OptSeg sg = t.opt_segs[si];
-  const GradSeg gs = t.grad_segs[si];
-  const uint64_t e0 = static_cast<uint64_t>(c - sg.chunk_begin) * CE;
-  const uint64_t rem = sg.numel - e0;
-  const uint32_t n = rem < CE ? static_cast<uint32_t>(rem) : CE;
-  const bool decay = gs.decay != 0;
-  double a = 0.0, b = 0.0;
-  uint32_t scalar_from = 0;
-  if (sg.vec_ok && gs.vec_ok) {
-    const uint64_t g0 = e0 / 4;
-    const uint32_t ng = n / 4;
-    if (ng == GPT * kScoreThreads) {
-      Group4<WDT, GDT, MASTER> grp[GPT];
-#pragma unroll
-      for (uint32_t k = 0; k < GPT; ++k) grp[k].load(sg, gs, g0 + tid + k * kScoreThreads);
-#pragma unroll
-      for (uint32_t k = 0; k < GPT; ++k) {
-        float da, db;
-        grp[k].step_store(sg, g0 + tid + k * kScoreThreads, sc, decay, da, db);
-        a += static_cast<double>(da);
-        b += static_cast<double>(db);
-      }
-    } else {
-      for (uint32_t i = tid; i < ng; i += kScoreThreads) {
-        Group4<WDT, GDT, MASTER> grp;
-        grp.load(sg, gs, g0 + i);
-        float da, db;
-        grp.step_store(sg, g0 + i, sc, decay, da, db);
-        a += static_cast<double>(da);
-        b += static_cast<double>(db);
-      }
-    }
-    scalar_from = ng * 4;
-  }
-  const uint8_t* wb = reinterpret_cast<const uint8_t*>(sg.w);
-  for (uint32_t i = scalar_from + tid; i < n; i += kScoreThreads) {
-    const uint64_t e = e0 + i;
-    float* mp = reinterpret_cast<float*>(sg.m) + e;
-    float* vp = reinterpret_cast<float*>(sg.v) + e;
-    const float po = MASTER ? reinterpret_cast<const float*>(sg.master)[e] : w_load<WDT>(wb, e);
-    float mm = *mp, vv = *vp;
-    const float x = adamw_elem(po, mm, vv, g_load<GDT>(reinterpret_cast<const uint8_t*>(gs.grad), e), sc, decay);
-    *mp = mm;
-    *vp = vv;
-    if constexpr (MASTER) reinterpret_cast<float*>(sg.master)[e] = x;
-    w_store<WDT>(reinterpret_cast<uint8_t*>(sg.w), e, x);
-    a += static_cast<double>(fabsf(x - po));
-    b += static_cast<double>(fabsf(po));
-  }
-  block_sum2<kScoreThreads>(a, b);
-  if (tid == 0) t.partials[c] = make_double2(a, b);
-}
-
-template <int WDT, int GDT, bool MASTER, bool LOOP>
-__global__ __launch_bounds__(kScoreThreads) void adamw_kernel(const DeviceTables t, const AdamScalars sc) {
-  if constexpr (!LOOP) {
-    adamw_chunk<WDT, GDT, MASTER>(t, sc, remap_xcd(blockIdx.x, gridDim.x));
-  } else {
-    for (uint64_t base = 0; base < t.n_chunks; base += gridDim.x) {
-      const uint64_t left = t.n_chunks - base;
-      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
-      if (blockIdx.x >= span) return;
-      adamw_chunk<WDT, GDT, MASTER>(t, sc, static_cast<uint32_t>(base + remap_xcd(blockIdx.x, span)));
-      __syncthreads();
-    }
-  }
-}
-
-// Blocks per launch: one per work item up to the dispatch limit of 2^32
-// work-items per dimension; beyond it the kernels loop.
-__host__ inline uint32_t grid_for(uint64_t items, uint32_t threads) {
-  uint64_t cap = (0xFFFFFFFFull / threads) & ~7ull;
-  if (LC_MAX_GRID_BLOCKS > 0 && cap > LC_MAX_GRID_BLOCKS) cap = LC_MAX_GRID_BLOCKS;
-  return static_cast<uint32_t>(items < cap ? items : cap);
-}
-
 template <int DT, bool ACCUM>
 void launch_score_t(const DeviceTables& t, hipStream_t st) {
   const uint32_t g = grid_for(t.n_chunks, kScoreThreads);
@@ -681,6 +409,11 @@ hipError_t launch_score(const DeviceTables& t, hipStream_t st) {
   return hipGetLastError();
 }
 
+hipError_t launch_finalize(const DeviceTables& t, hipStream_t st) {
+  hipLaunchKernelGGL(finalize_kernel, dim3(t.n_layers), dim3(kFinalizeThreads), 0, st, t);
+  return hipGetLastError();
+}
+
 hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode,
                          hipStream_t st) {
   hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelectThreads), 0, st, t, step, lr_scale, base_mode);
@@ -693,29 +426,6 @@ hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last
   uint8_t* stg = static_cast<uint8_t*>(staging);
   if (refresh_shadow) launch_pack_t<true>(t, first_rank, last_rank, piece_base, n_pieces, rec_base, stg, st);
   else launch_pack_t<false>(t, first_rank, last_rank, piece_base, n_pieces, rec_base, stg, st);
-  return hipGetLastError();
-}
-
-template <int WDT, int GDT, bool MASTER>
-void launch_adamw_t(const DeviceTables& t, const AdamScalars& sc, hipStream_t st) {
-  const uint32_t g = grid_for(t.n_chunks, kScoreThreads);
-  if (g == t.n_chunks)
-    hipLaunchKernelGGL((adamw_kernel<WDT, GDT, MASTER, false>), dim3(g), dim3(kScoreThreads), 0, st, t, sc);
-  else
-    hipLaunchKernelGGL((adamw_kernel<WDT, GDT, MASTER, true>), dim3(g), dim3(kScoreThreads), 0, st, t, sc);
-}
-
-hipError_t launch_adamw(const DeviceTables& t, int grad_dtype, int has_master, const AdamScalars& sc,
-                        hipStream_t st) {
-  const bool gb = grad_dtype == 1;
-  if (t.dtype == 1) {
-    if (has_master) { if (gb) launch_adamw_t<1, 1, true>(t, sc, st); else launch_adamw_t<1, 2, true>(t, sc, st); }
-    else { if (gb) launch_adamw_t<1, 1, false>(t, sc, st); else launch_adamw_t<1, 2, false>(t, sc, st); }
-  } else {
-    if (has_master) { if (gb) launch_adamw_t<2, 1, true>(t, sc, st); else launch_adamw_t<2, 2, true>(t, sc, st); }
-    else { if (gb) launch_adamw_t<2, 1, false>(t, sc, st); else launch_adamw_t<2, 2, false>(t, sc, st); }
-  }
-  hipLaunchKernelGGL(finalize_kernel, dim3(t.n_layers), dim3(kFinalizeThreads), 0, st, t);
   return hipGetLastError();
 }
 

@@ -664,22 +664,19 @@ lc_status lc_rebase(lc_ctx* c, int64_t step) {
   return LC_OK;
 }
 
-lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
-                              const uint8_t* decay_mask, const lc_adamw_params* p) {
-  lc_status st = check_ctx(c);
-  if (st != LC_OK) return st;
-  if (!grads || !p) return fail(LC_ERR_INVALID_ARG, "grads and params must be non-NULL");
+}  // extern "C"
+
+namespace {
+
+// Shared by the optimizer steps: validation of the call and the gradient
+// table, its upload, and the call-order state afterwards (the caller
+// launches its kernel between the two halves).
+lc_status optimizer_begin(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
+                          const uint8_t* decay_mask) {
+  if (!grads) return fail(LC_ERR_INVALID_ARG, "grads must be non-NULL");
   if (grad_dtype != LC_DT_BF16 && grad_dtype != LC_DT_F32)
     return fail(LC_ERR_INVALID_ARG, "unknown gradient dtype %d", grad_dtype);
-  if (!(p->lr >= 0.0) || !std::isfinite(p->lr)) return fail(LC_ERR_INVALID_ARG, "lr must be finite and >= 0");
-  if (!(p->beta1 >= 0.0 && p->beta1 < 1.0) || !(p->beta2 >= 0.0 && p->beta2 < 1.0))
-    return fail(LC_ERR_INVALID_ARG, "betas must lie in [0, 1)");
-  if (!(p->eps > 0.0) || !std::isfinite(p->eps)) return fail(LC_ERR_INVALID_ARG, "eps must be finite and > 0");
-  if (!(p->weight_decay >= 0.0) || !std::isfinite(p->weight_decay))
-    return fail(LC_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
-  if (p->adam_step < 1) return fail(LC_ERR_INVALID_ARG, "adam_step must be >= 1");
   if (c->mode != LC_MODE_ACCUM) return fail(LC_ERR_BAD_STATE, "the fused optimizer step needs LC_MODE_ACCUM");
-  if (!c->L.has_moments) return fail(LC_ERR_BAD_STATE, "the layout has no Adam moments");
   if (step <= c->last_step)
     return fail(LC_ERR_BAD_STATE, "step %lld must exceed the previous step %lld", static_cast<long long>(step),
                 static_cast<long long>(c->last_step));
@@ -702,6 +699,40 @@ lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads,
   LC_HIP(c, hipMemcpyAsync(c->d_grad, c->h_grad, sizeof(GradSeg) * ns, hipMemcpyHostToDevice, c->stream));
   LC_HIP(c, hipEventRecord(c->grad_event, c->stream));
   c->grad_event_pending = true;
+  return LC_OK;
+}
+
+lc_status optimizer_end(lc_ctx* c, int64_t step) {
+  LC_HIP(c, launch_finalize(c->dt, c->stream));
+  c->last_step = step;
+  c->scored = true;
+  c->scored_step = step;
+  c->have_selection = false;
+  c->pending = false;
+  c->result_on_host = false;
+  c->shadow_valid = false;
+  return LC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
+                              const uint8_t* decay_mask, const lc_adamw_params* p) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (!p) return fail(LC_ERR_INVALID_ARG, "params must be non-NULL");
+  if (!(p->lr >= 0.0) || !std::isfinite(p->lr)) return fail(LC_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!(p->beta1 >= 0.0 && p->beta1 < 1.0) || !(p->beta2 >= 0.0 && p->beta2 < 1.0))
+    return fail(LC_ERR_INVALID_ARG, "betas must lie in [0, 1)");
+  if (!(p->eps > 0.0) || !std::isfinite(p->eps)) return fail(LC_ERR_INVALID_ARG, "eps must be finite and > 0");
+  if (!(p->weight_decay >= 0.0) || !std::isfinite(p->weight_decay))
+    return fail(LC_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  if (p->adam_step < 1) return fail(LC_ERR_INVALID_ARG, "adam_step must be >= 1");
+  if (!c->L.has_moments) return fail(LC_ERR_BAD_STATE, "the layout has no Adam moments");
+  st = optimizer_begin(c, step, grads, grad_dtype, decay_mask);
+  if (st != LC_OK) return st;
   const double t = static_cast<double>(p->adam_step);
   AdamScalars sc;
   sc.b1 = static_cast<float>(p->beta1);
@@ -714,14 +745,24 @@ lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads,
   sc.lr = static_cast<float>(p->lr);
   sc.decay = static_cast<float>(1.0 - p->lr * p->weight_decay);
   LC_HIP(c, launch_adamw(c->dt, grad_dtype, c->L.has_master ? 1 : 0, sc, c->stream));
-  c->last_step = step;
-  c->scored = true;
-  c->scored_step = step;
-  c->have_selection = false;
-  c->pending = false;
-  c->result_on_host = false;
-  c->shadow_valid = false;
-  return LC_OK;
+  return optimizer_end(c, step);
+}
+
+lc_status lc_sgd_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
+                            const uint8_t* decay_mask, const lc_sgd_params* p) {
+  lc_status st = check_ctx(c);
+  if (st != LC_OK) return st;
+  if (!p) return fail(LC_ERR_INVALID_ARG, "params must be non-NULL");
+  if (!(p->lr >= 0.0) || !std::isfinite(p->lr)) return fail(LC_ERR_INVALID_ARG, "lr must be finite and >= 0");
+  if (!(p->weight_decay >= 0.0) || !std::isfinite(p->weight_decay))
+    return fail(LC_ERR_INVALID_ARG, "weight_decay must be finite and >= 0");
+  st = optimizer_begin(c, step, grads, grad_dtype, decay_mask);
+  if (st != LC_OK) return st;
+  SgdScalars sc;
+  sc.lr = static_cast<float>(p->lr);
+  sc.decay = static_cast<float>(1.0 - p->lr * p->weight_decay);
+  LC_HIP(c, launch_sgd(c->dt, grad_dtype, c->L.has_master ? 1 : 0, sc, c->stream));
+  return optimizer_end(c, step);
 }
 
 lc_status lc_read_state(lc_ctx* c, double* u_out, double* delta_out, int64_t* t_last_out) {

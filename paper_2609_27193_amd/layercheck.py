@@ -24,10 +24,10 @@ LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
-            "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_store_open", "lc_store_append",
-            "lc_store_sync", "lc_store_count", "lc_store_entry", "lc_store_plan", "lc_store_restore",
-            "lc_store_compact", "lc_store_close", "lc_read_state", "lc_record_bytes", "lc_destroy",
-            "lc_last_error")
+            "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_sgd_step_score", "lc_store_open",
+            "lc_store_append", "lc_store_sync", "lc_store_count", "lc_store_entry", "lc_store_plan",
+            "lc_store_restore", "lc_store_compact", "lc_store_close", "lc_read_state", "lc_record_bytes",
+            "lc_destroy", "lc_last_error")
 
 
 class lc_segment(C.Structure):
@@ -64,6 +64,10 @@ class lc_adamw_params(C.Structure):
                 ("weight_decay", C.c_double), ("adam_step", C.c_int64)]
 
 
+class lc_sgd_params(C.Structure):
+    _fields_ = [("lr", C.c_double), ("weight_decay", C.c_double)]
+
+
 class LCError(RuntimeError):
     def __init__(self, code: int, func: str, msg: str):
         super().__init__(f"{func} failed with status {code}: {msg}")
@@ -91,6 +95,8 @@ def load_library(path: str = LIB_PATH):
             "lc_rebase": (C.c_int, [C.c_void_p, C.c_int64]),
             "lc_adamw_step_score": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_void_p), C.c_int32, P(C.c_uint8),
                                               P(lc_adamw_params)]),
+            "lc_sgd_step_score": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_void_p), C.c_int32, P(C.c_uint8),
+                                            P(lc_sgd_params)]),
             "lc_store_open": (C.c_int, [C.c_char_p, C.c_uint32, P(C.c_uint64), C.c_uint64, P(C.c_void_p)]),
             "lc_store_append": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint8), C.c_void_p, C.c_uint64,
                                           C.c_void_p]),
@@ -221,6 +227,18 @@ def lc_adamw_step_score(ctx, step: int, grads: Sequence[int], grad_dtype: int, l
         dm = dm_arr.ctypes.data_as(C.POINTER(C.c_uint8))
     prm = lc_adamw_params(lr, beta1, beta2, eps, weight_decay, adam_step)
     _check(load_library().lc_adamw_step_score(ctx, step, g, grad_dtype, dm, C.byref(prm)), "lc_adamw_step_score")
+
+
+def lc_sgd_step_score(ctx, step: int, grads: Sequence[int], grad_dtype: int, lr: float, weight_decay: float,
+                      decay_mask: Optional[Sequence[int]] = None) -> None:
+    """grads: one device address per segment, in layout order."""
+    g = (C.c_void_p * len(grads))(*[int(x) for x in grads])
+    dm = None
+    if decay_mask is not None:
+        dm_arr = np.ascontiguousarray(decay_mask, dtype=np.uint8)
+        dm = dm_arr.ctypes.data_as(C.POINTER(C.c_uint8))
+    prm = lc_sgd_params(lr, weight_decay)
+    _check(load_library().lc_sgd_step_score(ctx, step, g, grad_dtype, dm, C.byref(prm)), "lc_sgd_step_score")
 
 
 class Store:

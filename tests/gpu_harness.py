@@ -241,6 +241,29 @@ class Pair:
         self.pack(t, mask, capacity)
         return mask, st
 
+    def fused_sgd_step(self, t, lr=1e-3, wd=0.01, grad_dtype="bf16", lr_scale=1.0, capacity=None, decide=True):
+        """One SGD step with the drift taken from the update, on both sides,
+        then (with ``decide``) select and pack."""
+        torch = self.torch
+        gdt = torch.bfloat16 if grad_dtype == "bf16" else torch.float32
+        g = self.gen.gradients(t, gdt)
+        dg = g.to("cuda")
+        gf = g.float().numpy()
+        decay = self.gen.decay_mask()
+        ptrs = [dg[s.offset:s.offset + s.numel].data_ptr() for s in self.gen.segments]
+        LC.lc_sgd_step_score(self.ctx, t, ptrs, LC.LC_DT_BF16 if grad_dtype == "bf16" else LC.LC_DT_F32,
+                             lr, wd, decay)
+        self.orc.sgd_step_score(t, [gf[s.offset:s.offset + s.numel] for s in self.gen.segments], lr, wd, decay)
+        u, d, tl = LC.lc_read_state(self.ctx, self.N)
+        assert rel_ok(u, self.orc.u), (t, u, self.orc.u)
+        assert rel_ok(d, self.orc.delta), (t, d, self.orc.delta)
+        self.check_arrays()  # master and weights bit-exact, moments untouched
+        if not decide:
+            return None, None
+        mask, st = self.select(t, lr_scale, d, tl)
+        self.pack(t, mask, capacity)
+        return mask, st
+
     def step(self, t, lr_scale=1.0, capacity=None):
         self.advance(t)
         d, tl = self.score(t)

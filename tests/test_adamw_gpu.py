@@ -102,3 +102,52 @@ def test_layout_without_shadow():
         assert e.value.code == LC.LC_ERR_INVALID_ARG
     finally:
         p.close()
+
+
+SGD_CASES = [("8b-master-weights-only", reduced_8b, "bf16", False), ("qwen-nomaster", reduced_qwen, "bf16", True),
+             ("toy-f32-grads", I.toy_spec, "f32", False), ("odd-misaligned", lambda: odd_spec("bf16", True), "bf16", True)]
+
+
+@pytest.mark.parametrize("name,maker,gdt,moments", SGD_CASES, ids=[c[0] for c in SGD_CASES])
+def test_fused_sgd_steps(name, maker, gdt, moments):
+    """Plain SGD with the drift taken from its update (Section 4.7): the
+    parameters and weights bit-exact against the oracle, moments (when the
+    layout has them) untouched, then selection and records; the records of
+    a layout without moments hold the weights (and master) only."""
+    spec = maker()
+    p = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 0.02), moments=moments)
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        for t in range(1, 7):
+            mask, st = p.fused_sgd_step(t, lr=1e-2 if t < 4 else 5e-3, grad_dtype=gdt,
+                                        capacity=max(p.R) if t % 2 else None)
+            log(f"  {name} t={t}: selected {st['n_selected']}/{p.N}")
+    finally:
+        p.close()
+
+
+def test_fused_sgd_state_rules():
+    spec = reduced_8b()
+    q = Pair(spec, LC.LC_MODE_SNAPSHOT, k0_for(spec, 0.02))
+    try:
+        with pytest.raises(LC.LCError) as e:
+            LC.lc_sgd_step_score(q.ctx, 1, [s.weight for s in q.lsegs], LC.LC_DT_BF16, 1e-3, 0.0)
+        assert e.value.code == LC.LC_ERR_BAD_STATE  # the drift accumulates: ACCUM only
+    finally:
+        q.close()
+    p = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 0.02), moments=False)
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        for bad in (dict(lr=-1.0), dict(lr=float("inf")), dict(weight_decay=-0.1)):
+            args = dict(lr=1e-3, weight_decay=0.0)
+            args.update(bad)
+            with pytest.raises(LC.LCError) as e:
+                LC.lc_sgd_step_score(p.ctx, 1, [s.weight for s in p.lsegs], LC.LC_DT_BF16, **args)
+            assert e.value.code == LC.LC_ERR_INVALID_ARG
+        with pytest.raises(LC.LCError) as e:  # AdamW needs the moments this layout lacks
+            LC.lc_adamw_step_score(p.ctx, 1, [s.weight for s in p.lsegs], LC.LC_DT_BF16, 1e-3, 0.9, 0.95, 1e-8, 0.0, 1)
+        assert e.value.code == LC.LC_ERR_BAD_STATE
+        p.fused_sgd_step(1)  # the failed calls left the context usable
+        p.check_arrays()
+    finally:
+        p.close()
