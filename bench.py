@@ -53,6 +53,8 @@ def parse():
                     help="also run one plain 4 GiB device copy (counter calibration)")
     ap.add_argument("--adamw", action="store_true",
                     help="drive the state with the fused AdamW + drift step instead of the standalone score")
+    ap.add_argument("--sgd", action="store_true",
+                    help="drive the state with the fused SGD + drift step (weights-only records)")
     ap.add_argument("--ceilings", action="store_true",
                     help="run the HBM ceiling probe (read, copy, 2-read-1-write streams with the kernels' "
                          "tile and block mapping) and print its JSON line")
@@ -71,9 +73,17 @@ def parse():
     return ap.parse_args()
 
 
-def kernel_source_hash() -> str:
+# The sources each profiled kernel is compiled from: counter files taken on
+# other sources are not reported.
+KERNEL_SOURCES = {
+    "score_kernel": ("lc_device.h", "lc_internal.h", "lc_kernels.hip"),
+    "adamw_kernel": ("lc_device.h", "lc_internal.h", "lc_optim.hip"),
+}
+
+
+def kernel_source_hash(kernel: str = "score_kernel") -> str:
     h = hashlib.sha256()
-    for f in ("lc_kernels.hip", "lc_internal.h"):
+    for f in KERNEL_SOURCES[kernel]:
         h.update(open(os.path.join(ROOT, "paper_2609_27193_amd", "csrc", f), "rb").read())
     return h.hexdigest()[:16]
 
@@ -85,7 +95,7 @@ def measured_traffic(kernel: str, workload: str, mode: str):
     if not os.path.exists(path):
         return None
     d = json.load(open(path))
-    if d.get("kernel_source_hash") != kernel_source_hash():
+    if d.get("kernel_source_hash") != kernel_source_hash(kernel):
         return None
     return d.get("hbm_bytes_per_launch")
 
@@ -216,8 +226,8 @@ def main():
     if args.restore_bench:
         return main_restore(args, I.WORKLOADS[args.workload]())
     spec = I.WORKLOADS[args.workload]()
-    if args.adamw:
-        return main_adamw(args, spec)
+    if args.adamw or args.sgd:
+        return main_optim(args, spec, "sgd" if args.sgd else "adamw")
     s_max = spec.s_max
     steps = args.steps if args.steps is not None else 2 * s_max
     warmup = args.warmup if args.warmup is not None else s_max
@@ -580,16 +590,22 @@ def main_restore(args, spec):
 ADAMW = dict(lr=1e-5, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
 
 
-def main_adamw(args, spec):
-    """Optimizer-driven decision step: the fused AdamW + drift pass (one read
-    and write of the optimizer state, no shadow), then select and pack.  The
-    gradients of each step are generated untimed."""
+SGD = dict(lr=1e-4, weight_decay=0.1)
+
+
+def main_optim(args, spec, optimizer):
+    """Optimizer-driven decision step: the fused optimizer + drift pass (one
+    read and write of the optimizer state, no shadow), then select and pack.
+    AdamW records hold W, master, m and v; SGD keeps no moments, so its
+    records hold W and master only (Section 4.7).  The gradients of each step
+    are generated untimed."""
     import torch
     from paper_2609_27193_amd import inputs as I
     from paper_2609_27193_amd import layercheck as LC
 
     if args.mode != "accum":
-        raise SystemExit("--adamw accumulates (ACCUM mode)")
+        raise SystemExit("the optimizer-driven step accumulates (ACCUM mode)")
+    adamw = optimizer == "adamw"
     s_max = spec.s_max
     steps = args.steps if args.steps is not None else 2 * s_max
     warmup = args.warmup if args.warmup is not None else s_max
@@ -599,8 +615,10 @@ def main_adamw(args, spec):
     LC.load_library()
     state = I.SyntheticState(spec, device=dev, shadow=False)
     torch.cuda.synchronize()
-    log(f"[bench] {spec.name} (AdamW-driven, no shadow): state {state.nbytes() / 1e9:.2f} GB")
+    log(f"[bench] {spec.name} ({optimizer}-driven, no shadow): state {state.nbytes() / 1e9:.2f} GB")
     segs = LC.segments_from_state(state)
+    if not adamw:  # weights-only layout: the moments are not part of the state
+        segs = [LC.Segment(s.layer, s.numel, s.weight, None, s.master, None, None) for s in segs]
     dtype = LC.LC_DT_BF16 if spec.weight_dtype == "bf16" else LC.LC_DT_F32
     embed = np.array([l.name == "embed_tokens" for l in spec.layers])
     decay = state.decay_mask()
@@ -608,8 +626,11 @@ def main_adamw(args, spec):
 
     def fused(ctx, t, g):
         ptrs = [g[s.offset:s.offset + s.numel].data_ptr() for s in state.segments]
-        LC.lc_adamw_step_score(ctx, t, ptrs, LC.LC_DT_BF16, ADAMW["lr"], ADAMW["beta1"], ADAMW["beta2"],
-                               ADAMW["eps"], ADAMW["weight_decay"], adam_t, decay)
+        if adamw:
+            LC.lc_adamw_step_score(ctx, t, ptrs, LC.LC_DT_BF16, ADAMW["lr"], ADAMW["beta1"], ADAMW["beta2"],
+                                   ADAMW["eps"], ADAMW["weight_decay"], adam_t, decay)
+        else:
+            LC.lc_sgd_step_score(ctx, t, ptrs, LC.LC_DT_BF16, SGD["lr"], SGD["weight_decay"], decay)
 
     t = 0
     if args.k0 is None:
@@ -641,9 +662,12 @@ def main_adamw(args, spec):
     LC.lc_pack_selected(ctx, staging.data_ptr(), cap, 0)
     w, P = spec.weight_bytes, spec.numel
     n_chunks = sum(math.ceil(s.numel * w / CHUNK_BYTES) for s in state.segments)
-    # grad (bf16) read, master/m/v read+write, weights written (and read when they are the parameters)
-    opt_bytes = P * (2 + (8 if spec.has_master else 0) + 16 + (w if spec.has_master else 2 * w)) + 32 * n_chunks
-    opt_b = 4 * (3 if spec.has_master else 2)
+    # grad (bf16) read, master (and m, v for AdamW) read+written, weights written
+    # (and read when they are the parameters)
+    moments_b = 16 if adamw else 0
+    opt_bytes = P * (2 + (8 if spec.has_master else 0) + moments_b + (w if spec.has_master else 2 * w)) \
+        + 32 * n_chunks
+    opt_b = (4 if spec.has_master else 0) + (8 if adamw else 0)  # fp32 bytes per element in a record
     if args.copy_calibration:
         copy_calibration(dev)
     rows = []
@@ -674,7 +698,7 @@ def main_adamw(args, spec):
                "pack_ms": ev[2].elapsed_time(ev[3]), "n_sel": st["n_selected"], "pack_bytes": pack_bytes,
                "bytes": opt_bytes + pack_bytes}
         log(f"[bench] {'warm' if i < warmup else 'time'} t={t} sel {st['n_selected']:2d}/{spec.n_layers} "
-            f"step {row['step_ms']:.3f} ms (AdamW+drift {row['opt_ms']:.3f}, pack {row['pack_ms']:.3f}) "
+            f"step {row['step_ms']:.3f} ms ({optimizer}+drift {row['opt_ms']:.3f}, pack {row['pack_ms']:.3f}) "
             f"-> {row['bytes'] / row['step_ms'] / 1e6:.1f} GB/s")
         if i >= warmup:
             rows.append(row)
@@ -686,17 +710,18 @@ def main_adamw(args, spec):
         "metric": "GB/s of optimizer state updated+scored and packed per training step (% of HBM peak); ms/step",
         "value": round(tot_bytes / tot_ms / 1e6, 2), "unit": "GB/s", "n_gpus": 1, "steps": steps,
         "warmup": warmup, "ms_per_step": round(tot_ms / len(rows), 4), "higher_is_better": True,
-        "scaling": "weak", "vs_baseline": None, "dtype": "bf16 grads, f32 AdamW, f64 reduce", "data": "synthetic",
-        "config": {"workload": f"{spec.name}-shaped state, fused AdamW + drift, select, pack",
-                   "params": P, "layer_groups": spec.n_layers, "s_max": s_max, "adamw": ADAMW,
+        "scaling": "weak", "vs_baseline": None, "dtype": f"bf16 grads, f32 {optimizer}, f64 reduce",
+        "data": "synthetic",
+        "config": {"workload": f"{spec.name}-shaped state, fused {optimizer} + drift, select, pack",
+                   "params": P, "layer_groups": spec.n_layers, "s_max": s_max, optimizer: ADAMW if adamw else SGD,
                    "selected_fraction": round(float(np.mean([r["n_sel"] for r in rows])) / spec.n_layers, 4),
                    "k0_base": k0_base, "opt_bytes_per_step_gb": round(opt_bytes / 1e9, 3)},
-        "roofline": {"bound": "hbm", "kernel": "adamw_kernel (+finalize)",
+        "roofline": {"bound": "hbm", "kernel": f"optim_kernel<{optimizer}> (+finalize)",
                      "achieved": round(opt_bytes / opt_ms / 1e6, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(opt_bytes / opt_ms / 1e6 / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("adamw_kernel", args.workload, "accum")},
+                     "traffic": measured_traffic("adamw_kernel", args.workload, "accum") if adamw else None},
     }
-    if args.torch_adamw_reference:
+    if args.torch_adamw_reference and adamw:
         del state, staging
         torch.cuda.empty_cache()
         out["torch_fused_adamw_reference"] = torch_adamw_reference(spec, dev)
