@@ -301,12 +301,14 @@ def test_fullsize_qwen14b_composite_restore_six_versions():
 
 
 @pytest.mark.timeout(900)
-def test_fullsize_8b_fused_adamw_sampled():
-    """The fused AdamW + drift step on the full Llama-3-8B-shaped state, in
-    the launch configuration `bench.py --adamw` times: sampled layers (one
-    transformer block, the final norm) bit-exact against the oracle's AdamW
-    on host copies, their u within the band, and the Eq. 2 arithmetic of
-    every layer bit for bit, over two steps."""
+@pytest.mark.parametrize("optimizer", ["adamw", "sgd"])
+def test_fullsize_8b_fused_optimizer_sampled(optimizer):
+    """The fused optimizer + drift step (AdamW, or SGD of Section 4.7) on the
+    full Llama-3-8B-shaped state, in the launch configuration `bench.py
+    --adamw` / `--sgd` times: sampled layers (one transformer block, the final
+    norm) bit-exact against the oracle's update on host copies, their u
+    within the band, and the Eq. 2 arithmetic of every layer bit for bit,
+    over two steps."""
     import torch
     spec = I.llama3_8b_spec()
     N = spec.n_layers
@@ -317,25 +319,33 @@ def test_fullsize_8b_fused_adamw_sampled():
         decay = run.state.decay_mask()
         segs = run.state.segments
         hp = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.1)
+        arrays = ("weight", "master", "exp_avg", "exp_avg_sq")
         for t in (1, 2):
             g = run.state.gradients(t)
-            before = {l: run.host_layer(l, ("weight", "master", "exp_avg", "exp_avg_sq")) for l in sampled}
+            before = {l: run.host_layer(l, arrays) for l in sampled}
             grads = {l: [g[s.offset:s.offset + s.numel].float().cpu().numpy() for s in run.layer_segments(l)]
                      for l in sampled}
             _, d_prev, _ = LC.lc_read_state(run.ctx, N)
-            LC.lc_adamw_step_score(run.ctx, t, [g[s.offset:s.offset + s.numel].data_ptr() for s in segs],
-                                   LC.LC_DT_BF16, hp["lr"], hp["beta1"], hp["beta2"], hp["eps"],
-                                   hp["weight_decay"], t, decay)
+            ptrs = [g[s.offset:s.offset + s.numel].data_ptr() for s in segs]
+            if optimizer == "adamw":
+                LC.lc_adamw_step_score(run.ctx, t, ptrs, LC.LC_DT_BF16, hp["lr"], hp["beta1"], hp["beta2"],
+                                       hp["eps"], hp["weight_decay"], t, decay)
+                sc = O.adamw_scalars(hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["weight_decay"], t)
+            else:
+                LC.lc_sgd_step_score(run.ctx, t, ptrs, LC.LC_DT_BF16, hp["lr"], hp["weight_decay"], decay)
+                sc = O.sgd_scalars(hp["lr"], hp["weight_decay"])
             u, d, _ = LC.lc_read_state(run.ctx, N)
             assert np.array_equal(d, d_prev + u)  # Eq. 2, every layer
-            sc = O.adamw_scalars(hp["lr"], hp["beta1"], hp["beta2"], hp["eps"], hp["weight_decay"], t)
-            after = {l: run.host_layer(l, ("weight", "master", "exp_avg", "exp_avg_sq")) for l in sampled}
+            after = {l: run.host_layer(l, arrays) for l in sampled}
             for l in sampled:
                 p_old, p_new = [], []
                 for k, s in enumerate(run.layer_segments(l)):
                     b, a = before[l][k], after[l][k]
-                    pn, mn, vn = O.adamw_update(b["master"], b["exp_avg"], b["exp_avg_sq"], grads[l][k], sc,
-                                                bool(decay[segs.index(s)]))
+                    dec = bool(decay[segs.index(s)])
+                    if optimizer == "adamw":
+                        pn, mn, vn = O.adamw_update(b["master"], b["exp_avg"], b["exp_avg_sq"], grads[l][k], sc, dec)
+                    else:  # SGD leaves the moments as they were
+                        pn, mn, vn = O.sgd_update(b["master"], grads[l][k], sc, dec), b["exp_avg"], b["exp_avg_sq"]
                     assert np.array_equal(a["master"].view(np.uint32), pn.view(np.uint32)), (t, l, k, "master")
                     assert np.array_equal(a["exp_avg"].view(np.uint32), mn.view(np.uint32)), (t, l, k, "m")
                     assert np.array_equal(a["exp_avg_sq"].view(np.uint32), vn.view(np.uint32)), (t, l, k, "v")
@@ -344,7 +354,7 @@ def test_fullsize_8b_fused_adamw_sampled():
                     p_new.append(pn)
                 uo = O.layer_update_score(p_new, p_old, O.DT_F32, 1e-8)[3]
                 assert abs(u[l] - uo) <= REL * uo, (t, l, u[l], uo)
-                log(f"  t={t} {names[l]}: u = {u[l]:.6e} (oracle {uo:.6e})")
+                log(f"  {optimizer} t={t} {names[l]}: u = {u[l]:.6e} (oracle {uo:.6e})")
             LC.lc_select(run.ctx, t, 1.0, N)
             del g
             torch.cuda.synchronize()
