@@ -296,6 +296,18 @@ class Store:
             h, self.h = self.h, None
             _check(load_library().lc_store_close(h), "lc_store_close")
 
+    def __enter__(self):
+        return self
+
+    def __exit__(self, *exc) -> None:
+        self.close()
+
+    def __del__(self):
+        # a store dropped without close() still finishes its writes
+        if getattr(self, "h", None) is not None and _LIB is not None:
+            _LIB.lc_store_close(self.h)
+            self.h = None
+
 
 def lc_read_state(ctx, n_layers: int):
     u = np.zeros(n_layers, dtype=np.float64)

@@ -199,3 +199,14 @@ def test_compact_crash_leftovers(lib, tmp_path):
     assert removed >= 1
     assert "v0000000999_s3.lcr" not in os.listdir(d)
     st.close()
+
+
+def test_store_context_manager(lib, tmp_path):
+    orc, versions = oracle_history(steps=2)
+    d = str(tmp_path / "cm")
+    with LC.Store(d, orc.R) as st:
+        v = versions[0]
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data, len(v["payload"]))
+    assert st.h is None
+    with LC.Store(d, orc.R) as st:
+        assert [e["step"] for e in st.entries()] == [0]
