@@ -222,7 +222,7 @@ lc_status lc_rebase(lc_ctx *c, int64_t step);
  * Requires LC_MODE_ACCUM and `step` greater than every earlier step; follows
  * the same call sequence as lc_score_layers (select and pack next).  The
  * shadow is left as it was, so lc_score_layers is refused afterwards until a
- * restore re-synchronises it.  Asynchronous. */
+ * restore or lc_rebase re-synchronises it.  Asynchronous. */
 lc_status lc_adamw_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,
                               const uint8_t *decay_mask, const lc_adamw_params *p);
 

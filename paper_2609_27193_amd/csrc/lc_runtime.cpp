@@ -457,8 +457,9 @@ lc_status lc_score_layers(lc_ctx* c, int64_t step) {
                 static_cast<long long>(c->last_step));
   if (!c->shadow_valid)
     return fail(LC_ERR_BAD_STATE, c->L.has_shadow
-                                      ? "the shadow is stale after lc_adamw_step_score; restore to re-synchronise it"
-                                      : "the layout has no shadow copies; use lc_adamw_step_score");
+                                      ? "the shadow is stale after a fused optimizer step; a restore or "
+                                        "lc_rebase re-synchronises it"
+                                      : "the layout has no shadow copies; use a fused optimizer step");
   if (c->mode == LC_MODE_SNAPSHOT && c->pending) {
     if (!c->result_on_host) {
       st = fetch_result(c);
