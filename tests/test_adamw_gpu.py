@@ -53,12 +53,16 @@ def test_fused_step_state_rules():
         with pytest.raises(LC.LCError) as e:
             LC.lc_adamw_step_score(p.ctx, 1, [1] * len(p.lsegs), LC.LC_DT_BF16, 1e-3, 0.9, 0.95, 1e-8, 0, 1)
         assert e.value.code == LC.LC_ERR_BAD_STATE  # step not increasing
+        # a full base checkpoint re-synchronises the shadow: the standalone score works again
+        p.rebase(1)
+        p.pack(1, np.ones(p.N, np.uint8))
+        p.step(2)
         for bad in (dict(beta1=1.0), dict(eps=0.0), dict(lr=-1.0), dict(weight_decay=float("nan")),
                     dict(adam_step=0)):
             args = dict(lr=1e-3, beta1=0.9, beta2=0.95, eps=1e-8, weight_decay=0.0, adam_step=2)
             args.update(bad)
             with pytest.raises(LC.LCError) as e:
-                LC.lc_adamw_step_score(p.ctx, 2, [s.weight for s in p.lsegs], LC.LC_DT_BF16, **args)
+                LC.lc_adamw_step_score(p.ctx, 3, [s.weight for s in p.lsegs], LC.LC_DT_BF16, **args)
             assert e.value.code == LC.LC_ERR_INVALID_ARG
         p.check_arrays()
     finally:
