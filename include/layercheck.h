@@ -278,7 +278,9 @@ lc_status lc_store_open(const char *dir, uint32_t n_layers, const uint64_t *reco
 lc_status lc_store_append(lc_store *s, int64_t step, const uint8_t *mask, const void *payload,
                           uint64_t payload_bytes, void *stream);
 
-/* Waits until every appended version is durable and visible. */
+/* Waits until every appended version is durable and visible.  After an I/O
+ * failure of the writers (a full disk, say) the failed version is dropped and
+ * this and every later append return LC_ERR_BAD_STATE with the error. */
 lc_status lc_store_sync(lc_store *s);
 
 /* Visible versions, in manifest order. */

@@ -348,20 +348,46 @@ lc_status parse_manifest(lc_store* s) {
   return LC_OK;
 }
 
+// Releases the drain ring and its stream (nothing may be in flight on them).
+void release_gpu(lc_store* s) {
+  for (uint8_t* p : s->slots) (void)hipHostFree(p);
+  for (hipEvent_t e : s->slot_events) (void)hipEventDestroy(e);
+  if (s->caller_ready) (void)hipEventDestroy(s->caller_ready);
+  if (s->copies_done) (void)hipEventDestroy(s->copies_done);
+  if (s->copy_stream) (void)hipStreamDestroy(s->copy_stream);
+  s->slots.clear();
+  s->slot_events.clear();
+  s->slot_free.clear();
+  s->caller_ready = s->copies_done = nullptr;
+  s->copy_stream = nullptr;
+  s->gpu_ready = false;
+}
+
+// The drain ring and its stream, set up on the first device append; a failed
+// set-up releases what it created, so a later append can try again.
 lc_status ensure_gpu(lc_store* s) {
   if (s->gpu_ready) return LC_OK;
   hipError_t e = hipStreamCreateWithFlags(&s->copy_stream, hipStreamNonBlocking);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&s->caller_ready, hipEventDisableTiming);
   if (e == hipSuccess) e = hipEventCreateWithFlags(&s->copies_done, hipEventDisableTiming);
-  if (e != hipSuccess) return fail(LC_ERR_HIP, "store stream setup failed: %s", hipGetErrorString(e));
+  if (e != hipSuccess) {
+    release_gpu(s);
+    return fail(LC_ERR_HIP, "store stream setup failed: %s", hipGetErrorString(e));
+  }
   for (uint32_t k = 0; k < s->n_slots; ++k) {
     void* p = nullptr;
     e = hipHostMalloc(&p, s->slot_bytes, hipHostMallocDefault);
-    if (e != hipSuccess) return fail(LC_ERR_OOM, "pinned drain buffer: %s", hipGetErrorString(e));
+    if (e != hipSuccess) {
+      release_gpu(s);
+      return fail(LC_ERR_OOM, "pinned drain buffer: %s", hipGetErrorString(e));
+    }
     s->slots.push_back(static_cast<uint8_t*>(p));
-    hipEvent_t ev;
+    hipEvent_t ev = nullptr;
     e = hipEventCreateWithFlags(&ev, hipEventDisableTiming);
-    if (e != hipSuccess) return fail(LC_ERR_HIP, "event create failed: %s", hipGetErrorString(e));
+    if (e != hipSuccess) {
+      release_gpu(s);
+      return fail(LC_ERR_HIP, "event create failed: %s", hipGetErrorString(e));
+    }
     s->slot_events.push_back(ev);
     s->slot_free.push_back(1);
   }
@@ -399,7 +425,7 @@ lc_status wait_idle(lc_store* s) {
   s->cv.wait(lk, [&] { return s->outstanding == 0 && s->next_final == s->writing.size(); });
   s->writing.clear();
   s->next_final = 0;
-  if (!s->writer_error.empty()) return fail(LC_ERR_INVALID_ARG, "store: %s", s->writer_error.c_str());
+  if (!s->writer_error.empty()) return fail(LC_ERR_BAD_STATE, "store failed: %s", s->writer_error.c_str());
   return LC_OK;
 }
 
@@ -845,11 +871,7 @@ lc_status lc_store_close(lc_store* s) {
     if (w.joinable()) w.join();
   if (s->gpu_ready) {
     (void)hipStreamSynchronize(s->copy_stream);
-    for (uint8_t* p : s->slots) (void)hipHostFree(p);
-    for (hipEvent_t e : s->slot_events) (void)hipEventDestroy(e);
-    (void)hipEventDestroy(s->caller_ready);
-    (void)hipEventDestroy(s->copies_done);
-    (void)hipStreamDestroy(s->copy_stream);
+    release_gpu(s);
   }
   if (s->manifest_fd >= 0) close(s->manifest_fd);
   delete s;
