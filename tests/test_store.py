@@ -210,3 +210,42 @@ def test_store_context_manager(lib, tmp_path):
     assert st.h is None
     with LC.Store(d, orc.R) as st:
         assert [e["step"] for e in st.entries()] == [0]
+
+
+def test_write_failure_drops_the_version(lib, tmp_path):
+    """An I/O failure in the writers (here the file-size limit of a child
+    process, so a write fails with EFBIG) drops the version being written,
+    fails the call with LC_ERR_BAD_STATE and every later append too; the
+    manifest never names the failed version, and the earlier history stays
+    restorable after reopening."""
+    import subprocess
+    import sys
+    d = str(tmp_path / "efbig")
+    child = f"""
+import resource, signal, sys
+import numpy as np
+sys.path.insert(0, {os.path.dirname(os.path.dirname(os.path.abspath(__file__)))!r})
+from paper_2609_27193_amd import layercheck as LC
+signal.signal(signal.SIGXFSZ, signal.SIG_IGN)
+R = [256 * 1024, 4 * 1024 * 1024]
+st = LC.Store({d!r}, R)
+small = np.arange(R[0], dtype=np.uint8)
+st.append(0, np.array([1, 0], np.uint8), small.ctypes.data, small.nbytes)   # fits under the limit
+resource.setrlimit(resource.RLIMIT_FSIZE, (1024 * 1024, 1024 * 1024))
+big = np.ones(R[1], dtype=np.uint8)
+codes = []
+for step in (1, 2):
+    try:
+        st.append(step, np.array([0, 1], np.uint8), big.ctypes.data, big.nbytes)
+        codes.append(0)
+    except LC.LCError as e:
+        codes.append(e.code)
+print(codes)
+"""
+    r = subprocess.run([sys.executable, "-c", child], capture_output=True, text=True, timeout=120)
+    assert r.returncode == 0, r.stderr
+    assert r.stdout.strip() == f"[{LC.LC_ERR_BAD_STATE}, {LC.LC_ERR_BAD_STATE}]", r.stdout
+    st = LC.Store(d, [256 * 1024, 4 * 1024 * 1024])
+    assert [e["step"] for e in st.entries()] == [0]
+    assert "LCV1 1 " not in open(os.path.join(d, "manifest.lcm")).read()
+    st.close()
