@@ -29,6 +29,10 @@ def hipcc() -> str:
 
 
 SANITIZED_LIB = os.path.join(HERE, "liblayercheck_hostsan.so")
+# Test build: every grid capped at 40 blocks, so each kernel runs the looped
+# form it uses beyond the 2^32 work-item dispatch limit.
+GRID_CAPPED_LIB = os.path.join(HERE, "liblayercheck_gridcap.so")
+GRID_CAP_DEFINES = ("LC_MAX_GRID_BLOCKS=40",)
 # AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (the
 # validation, tables, state machine and store); device code is unchanged.
 HOST_SANITIZER_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
@@ -111,4 +115,5 @@ if __name__ == "__main__":
     print(build(verbose=True))
     print(build_c_client(verbose=True))
     print(build(verbose=True, out=SANITIZED_LIB, sanitize=True))
+    print(build(verbose=True, out=GRID_CAPPED_LIB, defines=GRID_CAP_DEFINES))
     print(build_hbm_probe(verbose=True))
