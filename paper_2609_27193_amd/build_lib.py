@@ -111,9 +111,20 @@ def build_c_client(verbose: bool = False, lib: str = LIB) -> str:
     return C_CLIENT
 
 
+def build_all(verbose: bool = False) -> None:
+    """Everything the tests, smoke check and benchmark use: the library, then
+    (in parallel) the plain-C client linked against it, the host-sanitized
+    and grid-capped test builds, and the HBM probe."""
+    from concurrent.futures import ThreadPoolExecutor
+    build(verbose=verbose)
+    jobs = [lambda: build_c_client(verbose=verbose),
+            lambda: build(verbose=verbose, out=SANITIZED_LIB, sanitize=True),
+            lambda: build(verbose=verbose, out=GRID_CAPPED_LIB, defines=GRID_CAP_DEFINES),
+            lambda: build_hbm_probe(verbose=verbose)]
+    with ThreadPoolExecutor(max_workers=len(jobs)) as pool:
+        for f in [pool.submit(j) for j in jobs]:
+            f.result()
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
-    print(build_c_client(verbose=True))
-    print(build(verbose=True, out=SANITIZED_LIB, sanitize=True))
-    print(build(verbose=True, out=GRID_CAPPED_LIB, defines=GRID_CAP_DEFINES))
-    print(build_hbm_probe(verbose=True))
+    build_all(verbose=True)
