@@ -313,6 +313,15 @@ lc_status lc_store_restore(lc_store *s, lc_ctx *c, int64_t t_fail, int64_t *chos
  * files removed. */
 lc_status lc_store_compact(lc_store *s, int64_t t_keep, uint32_t *removed_out);
 
+/* Recovery timeline: after a restore at t_fail, training continues from
+ * t_fail + 1 and versions persisted after t_fail belong to the abandoned run.
+ * Removes every visible version with a step greater than `step` (the
+ * manifest is rewritten atomically first, as for lc_store_compact) so the
+ * resumed run can append its own versions of those steps.  Waits for pending
+ * writes first.  `removed_out` (or NULL) receives the number of files
+ * removed. */
+lc_status lc_store_discard_after(lc_store *s, int64_t step, uint32_t *removed_out);
+
 /* Waits for pending writes, stops the writer and frees the store. */
 lc_status lc_store_close(lc_store *s);
 

@@ -429,6 +429,55 @@ lc_status wait_idle(lc_store* s) {
   return LC_OK;
 }
 
+// Keeps the visible versions flagged in `keep` and removes the rest, plus any
+// version file no manifest line names (a crash between a manifest rewrite and
+// the removals, or a version that never became visible: nothing is in flight
+// once the store is idle).  The new manifest replaces the old one atomically
+// (temporary file, fsync, rename, directory fsync) before any file goes.
+lc_status keep_only(lc_store* s, const std::vector<uint8_t>& keep, uint32_t* removed_out) {
+  const size_t n = s->durable.size();
+  std::vector<StoredVersion> kept;
+  std::vector<std::string> gone;
+  for (size_t i = 0; i < n; ++i) {
+    if (keep[i]) kept.push_back(s->durable[i]);
+    else gone.push_back(s->durable[i].file);
+  }
+  if (DIR* dp = opendir(s->dir.c_str())) {
+    std::vector<std::string> named;
+    for (const StoredVersion& v : s->durable) named.push_back(v.file);
+    while (dirent* e = readdir(dp)) {
+      const std::string f = e->d_name;
+      if (f.size() > 4 && f.compare(f.size() - 4, 4, ".lcr") == 0 &&
+          std::find(named.begin(), named.end(), f) == named.end())
+        gone.push_back(f);
+    }
+    closedir(dp);
+  }
+  if (gone.empty()) return LC_OK;
+  if (kept.size() != n) {
+    const std::string mpath = s->dir + "/manifest.lcm", tpath = s->dir + "/manifest.lcm.tmp";
+    const int fd = open(tpath.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
+    if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", tpath.c_str(), std::strerror(errno));
+    std::string text;
+    for (const StoredVersion& v : kept) text += manifest_line(v);
+    const bool ok = write_all(fd, reinterpret_cast<const uint8_t*>(text.data()), text.size(), 0) && fsync(fd) == 0;
+    close(fd);
+    if (!ok || rename(tpath.c_str(), mpath.c_str()) != 0 || !fsync_dir(s->dir))
+      return fail(LC_ERR_INVALID_ARG, "rewriting the manifest failed: %s", std::strerror(errno));
+    const int mfd = open(mpath.c_str(), O_RDWR);
+    if (mfd < 0) return fail(LC_ERR_INVALID_ARG, "cannot reopen %s: %s", mpath.c_str(), std::strerror(errno));
+    close(s->manifest_fd);
+    s->manifest_fd = mfd;
+    s->durable = kept;
+  }
+  uint32_t removed = 0;
+  for (const std::string& f : gone)
+    if (unlink((s->dir + "/" + f).c_str()) == 0) ++removed;
+  (void)fsync_dir(s->dir);
+  if (removed_out) *removed_out = removed;
+  return LC_OK;
+}
+
 // Reads the chosen record of every layer and restores it (Section 3.5 steps
 // 2-3) as one pipeline over fixed 64 MiB pieces of the records, in layer
 // order: reader threads fill a ring of pinned slots, each as soon as the
@@ -812,51 +861,17 @@ lc_status lc_store_compact(lc_store* s, int64_t t_keep, uint32_t* removed_out) {
     }
     if (best >= 0) keep[best] = 1;
   }
-  std::vector<StoredVersion> kept;
-  std::vector<std::string> gone;
-  for (size_t i = 0; i < n; ++i) {
-    if (keep[i]) kept.push_back(s->durable[i]);
-    else gone.push_back(s->durable[i].file);
-  }
-  // files no manifest line names (a crash between a manifest rewrite and the
-  // removals, or a version that never became visible) go too: nothing is in
-  // flight once the store is idle
-  if (DIR* dp = opendir(s->dir.c_str())) {
-    std::vector<std::string> named;
-    for (const StoredVersion& v : s->durable) named.push_back(v.file);
-    while (dirent* e = readdir(dp)) {
-      const std::string f = e->d_name;
-      if (f.size() > 4 && f.compare(f.size() - 4, 4, ".lcr") == 0 &&
-          std::find(named.begin(), named.end(), f) == named.end())
-        gone.push_back(f);
-    }
-    closedir(dp);
-  }
-  if (gone.empty()) return LC_OK;
-  if (kept.size() != n) {
-    // the new manifest replaces the old one atomically: written to a temporary
-    // file, fsync'ed, renamed over it, then the directory fsync'ed
-    const std::string mpath = s->dir + "/manifest.lcm", tpath = s->dir + "/manifest.lcm.tmp";
-    const int fd = open(tpath.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
-    if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", tpath.c_str(), std::strerror(errno));
-    std::string text;
-    for (const StoredVersion& v : kept) text += manifest_line(v);
-    const bool ok = write_all(fd, reinterpret_cast<const uint8_t*>(text.data()), text.size(), 0) && fsync(fd) == 0;
-    close(fd);
-    if (!ok || rename(tpath.c_str(), mpath.c_str()) != 0 || !fsync_dir(s->dir))
-      return fail(LC_ERR_INVALID_ARG, "rewriting the manifest failed: %s", std::strerror(errno));
-    const int mfd = open(mpath.c_str(), O_RDWR);
-    if (mfd < 0) return fail(LC_ERR_INVALID_ARG, "cannot reopen %s: %s", mpath.c_str(), std::strerror(errno));
-    close(s->manifest_fd);
-    s->manifest_fd = mfd;
-    s->durable = kept;
-  }
-  uint32_t removed = 0;
-  for (const std::string& f : gone)
-    if (unlink((s->dir + "/" + f).c_str()) == 0) ++removed;
-  (void)fsync_dir(s->dir);
-  if (removed_out) *removed_out = removed;
-  return LC_OK;
+  return keep_only(s, keep, removed_out);
+}
+
+lc_status lc_store_discard_after(lc_store* s, int64_t step, uint32_t* removed_out) {
+  if (removed_out) *removed_out = 0;
+  if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
+  lc_status st = wait_idle(s);
+  if (st != LC_OK) return st;
+  std::vector<uint8_t> keep(s->durable.size(), 0);
+  for (size_t i = 0; i < keep.size(); ++i) keep[i] = s->durable[i].step <= step;
+  return keep_only(s, keep, removed_out);
 }
 
 lc_status lc_store_close(lc_store* s) {

@@ -26,8 +26,8 @@ LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
             "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_sgd_step_score", "lc_store_open",
             "lc_store_append", "lc_store_sync", "lc_store_count", "lc_store_entry", "lc_store_plan",
-            "lc_store_restore", "lc_store_compact", "lc_store_close", "lc_read_state", "lc_record_bytes",
-            "lc_destroy", "lc_last_error")
+            "lc_store_restore", "lc_store_compact", "lc_store_discard_after", "lc_store_close", "lc_read_state",
+            "lc_record_bytes", "lc_destroy", "lc_last_error")
 
 
 class lc_segment(C.Structure):
@@ -106,6 +106,7 @@ def load_library(path: str = LIB_PATH):
             "lc_store_plan": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_int64)]),
             "lc_store_restore": (C.c_int, [C.c_void_p, C.c_void_p, C.c_int64, P(C.c_int64)]),
             "lc_store_compact": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint32)]),
+            "lc_store_discard_after": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint32)]),
             "lc_store_close": (C.c_int, [C.c_void_p]),
             "lc_read_state": (C.c_int, [C.c_void_p, P(C.c_double), P(C.c_double), P(C.c_int64)]),
             "lc_record_bytes": (C.c_uint64, [C.c_void_p, C.c_uint32]),
@@ -289,6 +290,13 @@ class Store:
         the number of files removed."""
         n = C.c_uint32()
         _check(load_library().lc_store_compact(self.h, t_keep, C.byref(n)), "lc_store_compact")
+        return n.value
+
+    def discard_after(self, step: int) -> int:
+        """Removes the versions newer than ``step`` (an abandoned timeline);
+        returns the number of files removed."""
+        n = C.c_uint32()
+        _check(load_library().lc_store_discard_after(self.h, step, C.byref(n)), "lc_store_discard_after")
         return n.value
 
     def close(self) -> None:

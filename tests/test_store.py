@@ -249,3 +249,31 @@ print(codes)
     assert [e["step"] for e in st.entries()] == [0]
     assert "LCV1 1 " not in open(os.path.join(d, "manifest.lcm")).read()
     st.close()
+
+
+def test_discard_after_for_a_resumed_run(lib, tmp_path):
+    """After a restore at t_fail the versions newer than t_fail belong to the
+    abandoned run: discarding them lets the resumed run append its own
+    versions of those steps (a layer may be stored once per step), and plans
+    then mix the old history up to t_fail with the new one."""
+    orc, versions = oracle_history(steps=6)
+    d = str(tmp_path / "tl")
+    st = LC.Store(d, orc.R)
+    for v in versions:
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    st.sync()
+    t_fail = 3
+    new = [v for v in versions if v["step"] > t_fail and v["mask"].any()][0]
+    with pytest.raises(LC.LCError):  # the abandoned run already stored these layers at this step
+        st.append(new["step"], new["mask"], new["payload"].ctypes.data, len(new["payload"]))
+    removed = st.discard_after(t_fail)
+    assert removed == len([v for v in versions if v["step"] > t_fail])
+    assert [e["step"] for e in st.entries()] == [v["step"] for v in versions if v["step"] <= t_fail]
+    st.append(new["step"], new["mask"], new["payload"].ctypes.data, len(new["payload"]))
+    st.close()
+    st = LC.Store(d, orc.R)
+    timeline = [v for v in versions if v["step"] <= t_fail] + [new]
+    assert [e["step"] for e in st.entries()] == [v["step"] for v in timeline]
+    for t in range(0, 8):
+        assert st.plan(t).tolist() == [timeline[i]["step"] for i in O.plan_versions(timeline, orc.N, t)]
+    st.close()

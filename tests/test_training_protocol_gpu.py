@@ -10,7 +10,9 @@ the oracle at every step.
   (Section 3.3), the pack of the selected layers and its drain into the store
   with no host synchronisation before the next step.
 * A fail-stop at t_fail, the composite recovery from the store (Section 3.5),
-  and training resumed from the recovered state.
+  training resumed from the recovered state (the abandoned run's newer
+  versions discarded from the store), and a second fail-stop recovered from
+  a history that mixes both runs.
 
 Optimizer state, weights and records are bit-exact against the oracle; the
 scores agree within the harness tolerance."""
@@ -101,11 +103,35 @@ def test_warmup_schedule_store_failure_recovery(tmp_path, maker):
         assert min(chosen) >= t_fail - (spec.s_max - 1)  # the staleness bound holds at recovery
         p.check_arrays()
         log(f"  recovered at {t_fail} from steps {sorted(set(chosen.tolist()))}")
-        # training resumes from the recovered state
+        # training resumes from the recovered state; the abandoned run's newer
+        # versions leave the store, and the resumed run persists its own
         p.adopt_restored()
+        removed = store.discard_after(t_fail)
+        stored = [v for v in stored if v["step"] <= t_fail]
+        assert removed >= 1 and [e["step"] for e in store.entries()] == [v["step"] for v in stored]
         for t in range(t_fail + 1, t_fail + 3):
             lr = lr_at(t, warm, total)
-            p.fused_step(t, adam_t=t, lr=lr, lr_scale=lr / LR_PEAK)
+            mask, st = p.fused_step(t, adam_t=t, lr=lr, lr_scale=lr / LR_PEAK)
+            assert st["max_age"] <= spec.s_max - 1
+            drain(t, mask)
+        store.sync()
+        # a second fail-stop: the composite mixes the first run's records up
+        # to its t_fail with the resumed run's
+        t_fail2 = t_fail + 2
+        for a in (p.dW, p.dS, p.dm, p.dv) + ((p.dM,) if p.dM is not None else ()):
+            a.fill_(0)
+        for a in (p.hW, p.hS, p.hm, p.hv) + ((p.hM,) if p.hM is not None else ()):
+            a[...] = 0
+        torch.cuda.synchronize()
+        chosen = store.restore(p.ctx, t_fail2)
+        assert chosen.tolist() == p.orc.restore(stored, t_fail2).tolist()
+        assert min(chosen) >= t_fail2 - (spec.s_max - 1)
+        assert min(chosen) <= t_fail < max(chosen), chosen  # records of both runs
+        p.check_arrays()
+        log(f"  second recovery at {t_fail2} from steps {sorted(set(chosen.tolist()))}")
+        p.adopt_restored()
+        lr = lr_at(t_fail2 + 1, warm, total)
+        p.fused_step(t_fail2 + 1, adam_t=t_fail2 + 1, lr=lr, lr_scale=lr / LR_PEAK)
     finally:
         store.close()
         p.close()
