@@ -23,6 +23,9 @@ What it computes, in the paper's notation:
 * Section 3.4 warm-up: no selective persistence during the warm-up window,
   then a full base checkpoint, after which every layer counts as persisted
   at the base step (``rebase``).
+* Section 3.4 / 4.1 / 4.7: the drift taken from the optimizer's own update,
+  for AdamW (``adamw_step_score``) and for plain SGD (``sgd_step_score``),
+  in fp32 with one rounding per operation (the optimizer's precision).
 * Section 3.1 / Eq. 8 recovery: each layer takes its newest persisted record
   with step <= t_fail; the base full checkpoint is simply a version holding
   every layer.
