@@ -461,6 +461,8 @@ def main_store(args, spec):
            "host_link_gbs": round(link_gbs, 2),
            "drain_base_gbs": round(total / t_base / 1e9, 3),
            "steps_gb": round(drained / 1e9, 3),
+           # what full checkpoints at the same six steps would have written (Table 1's comparison)
+           "full_checkpoints_gb": round(6 * total / 1e9, 3),
            "steps_append_call_s": round(call_s, 3),
            "steps_staging_release_gbs": round(drained / release_s / 1e9, 2),
            "steps_durable_gbs": round(drained / durable_s / 1e9, 3),
