@@ -251,7 +251,8 @@ lc_status lc_sgd_step_score(lc_ctx *c, int64_t step, const void *const *grads, i
  * (records in the lc_pack_selected format).  A version is visible once its
  * file is complete and fsync'ed and its manifest line ("LCV1 <step> <bytes>
  * <file> <mask as 0/1 characters>") is written and fsync'ed; on open, torn or
- * inconsistent lines and files of the wrong size are ignored.  A store is
+ * inconsistent lines, files of the wrong size and names other than a plain
+ * "v*.lcr" file of the directory itself are ignored.  A store is
  * used from one thread; it owns a small pool of writer threads, and versions
  * become visible in the order they were appended. */
 typedef struct lc_store lc_store;

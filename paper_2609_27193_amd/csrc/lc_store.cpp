@@ -327,6 +327,13 @@ lc_status parse_manifest(lc_store* s) {
     v.step = step;
     v.bytes = bytes;
     v.file = file;
+    // only a plain name of this store's own version files: a damaged line must
+    // never lead a restore or a removal outside the directory
+    if (v.file.find('/') != std::string::npos || v.file.size() < 5 ||
+        v.file.compare(v.file.size() - 4, 4, ".lcr") != 0 || v.file[0] != 'v') {
+      ++s->skipped;
+      continue;
+    }
     v.mask.resize(s->N);
     uint64_t need = 0;
     bool ok = true;

@@ -99,10 +99,14 @@ def test_crash_consistency(lib, tmp_path):
     with open(os.path.join(d, victim), "r+b") as f:
         f.truncate(os.path.getsize(os.path.join(d, victim)) - 256)
     # (2) a garbage line, (3) a line for a file that does not exist,
-    # (4) a torn last line, (5) an orphan version file with no line
+    # (4) a line naming a file outside the directory (right size, right mask),
+    # (5) a torn last line, (6) an orphan version file with no line
+    outside = str(tmp_path / "v_outside.lcr")
+    open(outside, "wb").write(b"\0" * orc.R[0])
     with open(os.path.join(d, "manifest.lcm"), "a") as f:
         f.write("not a manifest line\n")
         f.write("LCV1 9 256 v9999999999_s9.lcr " + "1" + "0" * (orc.N - 1) + "\n")
+        f.write(f"LCV1 11 {orc.R[0]} ../v_outside.lcr " + "1" + "0" * (orc.N - 1) + "\n")
         f.write("LCV1 10 25")
     open(os.path.join(d, "v0000000777_s12.lcr"), "wb").write(b"\0" * 512)
     st = LC.Store(d, orc.R)
@@ -119,7 +123,10 @@ def test_crash_consistency(lib, tmp_path):
     st.close()
     st = LC.Store(d, orc.R)
     assert st.entries()[-1]["step"] == 20
+    # reclaiming space never reaches outside the store's directory
+    st.compact(20)
     st.close()
+    assert os.path.getsize(outside) == orc.R[0]
 
 
 def test_large_host_payload_in_pieces(lib, tmp_path):
