@@ -63,7 +63,8 @@ typedef struct lc_ctx lc_ctx; /* opaque, library-owned */
 /* One contiguous piece of one tensor of one layer.  All arrays hold `numel`
  * elements; weight and shadow have the layout's weight dtype, the others are
  * fp32.  Pointers must be naturally aligned (2 B for bf16, 4 B for fp32);
- * 16-byte alignment selects the vectorised fast path. */
+ * 16-byte alignment selects the vectorised fast path.  No two arrays of a
+ * layout (over all its segments) may overlap in memory: LC_ERR_INVALID_ARG. */
 typedef struct {
   uint32_t layer;     /* layer group id in [0, n_layers)                      */
   uint32_t reserved;  /* must be 0                                            */

@@ -3,6 +3,7 @@
 // interface declared in include/layercheck.h.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -83,6 +84,31 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
   }
   if (prev != static_cast<int64_t>(N) - 1)
     return fail(LC_ERR_INVALID_ARG, "layer %lld has no segment", static_cast<long long>(prev + 1));
+  // The library writes every array (the shadow on each score, all of them on
+  // a restore or an optimizer step), so no two may share a byte.
+  {
+    struct Span { uint64_t b, e; uint32_t seg; };
+    std::vector<Span> spans;
+    spans.reserve(5ull * d->n_segments);
+    for (uint32_t i = 0; i < d->n_segments; ++i) {
+      const lc_segment& s = L.segs[i];
+      const void* arr[5] = {s.weight, s.shadow, s.master, s.exp_avg, s.exp_avg_sq};
+      for (int a = 0; a < 5; ++a)
+        if (arr[a]) {
+          const uint64_t b = reinterpret_cast<uint64_t>(arr[a]);
+          spans.push_back({b, b + s.numel * (a < 2 ? L.esz : 4u), i});
+        }
+    }
+    std::sort(spans.begin(), spans.end(), [](const Span& x, const Span& y) { return x.b < y.b; });
+    uint64_t reach = 0;
+    uint32_t reach_seg = 0;
+    for (const Span& sp : spans) {
+      if (sp.b < reach)
+        return fail(LC_ERR_INVALID_ARG, "segments %u and %u: arrays overlap in memory", reach_seg, sp.seg);
+      reach = sp.e;
+      reach_seg = sp.seg;
+    }
+  }
   L.layer_seg_begin[N] = d->n_segments;
   L.total_numel = 0;
   for (uint32_t l = 0; l < N; ++l) L.total_numel += L.numel[l];

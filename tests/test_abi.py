@@ -120,6 +120,19 @@ def test_validation_errors(lib):
     bad = fake_segments([[4], [4]])
     bad[1].layer = 5
     _expect(I, lambda: q(segs=bad))
+    # no two arrays may share a byte, within a segment or across segments
+    for a, b, shift in [(0, 0, 0), (1, 0, 0), (1, 0, 4), (0, 0, -4)]:
+        bad = fake_segments([[4], [4]])
+        bad[a].exp_avg_sq = bad[b].exp_avg + shift       # v on (or straddling) another segment's m
+        _expect(I, lambda: q(segs=bad))
+        assert "overlap" in lib.lc_last_error().decode()
+    bad = fake_segments([[4], [4]])
+    bad[1].master = bad[0].weight + 4                   # fp32 master over the tail of a bf16 weight
+    _expect(I, lambda: q(segs=bad))
+    # arrays that touch without overlapping are fine
+    a = FAKE
+    tight = [LC.Segment(0, 4, a, a + 8, a + 16, a + 32, a + 48), LC.Segment(1, 4, a + 64, a + 72, a + 80, a + 96, a + 112)]
+    q(segs=tight)
     big = fake_segments([[1 << 40]])
     _expect(I, lambda: q(segs=big, n=1, k0=[1e-3], s_max=1 << 30))  # staleness numerator overflow
     with pytest.raises(ValueError):
