@@ -384,9 +384,15 @@ def main_store(args, spec):
     k0 = [(args.k0 or 0.03) * (10.0 if l.name == "embed_tokens" else 1.0) for l in spec.layers]
     layout = LC.LayoutDesc(segs, spec.n_layers, dtype, spec.has_master, LC.LC_MODE_ACCUM, k0, spec.s_max,
                            stream=stream.cuda_stream)
-    _, rec = LC.lc_query_layout(layout)
+    numel, rec = LC.lc_query_layout(layout)
     total = sum(rec)
     staging = torch.empty(total, dtype=torch.uint8, device=dev)
+    w, opt_b = spec.weight_bytes, 4 * (3 if spec.has_master else 2)
+
+    def step_bytes(mask, packed):
+        """Algorithmic bytes of one ACCUM decision step: score 3wP, then the
+        selected state read and the records written."""
+        return 3 * w * spec.numel + sum(n for n, m in zip(numel, mask) if m) * (w + opt_b) + packed
     ctx = LC.lc_init_layout(layout)
     ring = 4 << 30
     # host-link ceiling: one plain device-to-pinned copy of the ring's size
@@ -413,12 +419,18 @@ def main_store(args, spec):
     log(f"[bench] base version {total / 1e9:.2f} GB: append returned after {t_append:.2f} s, durable after "
         f"{t_base:.2f} s -> {total / t_base / 1e9:.2f} GB/s")
     drained, release_s, durable_s, call_s = 0, 0.0, 0.0, 0.0
+    alone_ms, alone_bytes = [], 0
     for t in range(1, 7):
         state.step(t)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
         LC.lc_score_layers(ctx, t)
         mask, st = LC.lc_select(ctx, t, 1.0, spec.n_layers)
         r = LC.lc_pack_selected(ctx, staging.data_ptr(), total, 0)
+        e1.record(stream)
         torch.cuda.synchronize()
+        alone_ms.append(e0.elapsed_time(e1))
+        alone_bytes += step_bytes(mask, r["bytes_written"])
         a = time.perf_counter()
         store.append(t, mask, staging.data_ptr(), r["bytes_written"], stream.cuda_stream)
         b = time.perf_counter()
@@ -432,6 +444,49 @@ def main_store(args, spec):
         drained += r["bytes_written"]
         log(f"[bench] t={t}: {st['n_selected']} layers, {r['bytes_written'] / 1e9:.2f} GB: append {b - a:.3f} s, "
             f"staging free after {c - a:.3f} s, durable after {d - a:.3f} s")
+    # Overlapped drain: two staging buffers and lc_store_append_async.  The
+    # caller's stream waits only for the copies out of the buffer it is about
+    # to pack again, so each decision step runs while the previous step's
+    # payload is still being copied out; its GPU time is compared with the
+    # same step above, where nothing was in flight.
+    od = args.store_bench.rstrip("/") + "_overlapped"
+    shutil.rmtree(od, ignore_errors=True)
+    ostore = LC.Store(od, rec, buffer_bytes=ring)
+    stagings = [staging, torch.empty(total, dtype=torch.uint8, device=dev)]
+    reuse = [torch.cuda.Event() for _ in stagings]
+    for ev in reuse:
+        ev.record(stream)  # creates the underlying event
+    o_bytes, o_step_bytes, overlap_ms, o_call_s, marks = 0, 0, [], 0.0, []
+    a = time.perf_counter()
+    for t in range(7, 13):
+        state.step(t)
+        k = t % 2
+        stream.wait_event(reuse[k])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        LC.lc_score_layers(ctx, t)
+        mask, st = LC.lc_select(ctx, t, 1.0, spec.n_layers)
+        r = LC.lc_pack_selected(ctx, stagings[k].data_ptr(), total, 0)
+        e1.record(stream)
+        b = time.perf_counter()
+        ostore.append_async(t, mask, stagings[k].data_ptr(), r["bytes_written"], stream.cuda_stream,
+                            reuse[k].cuda_event)
+        o_call_s += time.perf_counter() - b
+        marks.append((e0, e1))
+        o_bytes += r["bytes_written"]
+        o_step_bytes += step_bytes(mask, r["bytes_written"])
+    torch.cuda.synchronize()
+    ostore.sync()
+    o_total_s = time.perf_counter() - a
+    overlap_ms = [x.elapsed_time(y) for x, y in marks]
+    ostore.close()
+    shutil.rmtree(od, ignore_errors=True)
+    del stagings[1]
+    alone_gbs = alone_bytes / sum(alone_ms) / 1e6
+    overlap_gbs = o_step_bytes / sum(overlap_ms) / 1e6
+    log(f"[bench] overlapped drain: decision steps at {overlap_gbs:.0f} GB/s with the previous payload in flight "
+        f"vs {alone_gbs:.0f} GB/s alone ({np.mean(overlap_ms):.2f} / {np.mean(alone_ms):.2f} ms per step); "
+        f"append calls {o_call_s:.3f} s in total; {o_bytes / 1e9:.2f} GB durable after {o_total_s:.2f} s")
     t_fail = 5
     stored_before = sum(e["payload_bytes"] for e in store.entries())
     a = time.perf_counter()
@@ -466,6 +521,13 @@ def main_store(args, spec):
            "steps_append_call_s": round(call_s, 3),
            "steps_staging_release_gbs": round(drained / release_s / 1e9, 2),
            "steps_durable_gbs": round(drained / durable_s / 1e9, 3),
+           # the caller's stream held per step by the drain: the device-to-host copies
+           # with lc_store_append, none with lc_store_append_async
+           "steps_stream_held_ms": round(release_s / 6 * 1e3, 2),
+           "decision_step_gbs_alone": round(alone_gbs, 1),
+           "decision_step_gbs_overlapped": round(overlap_gbs, 1),
+           "overlapped_append_call_s": round(o_call_s, 3),
+           "overlapped_durable_gbs": round(o_bytes / o_total_s / 1e9, 3),
            "stored_gb_before_compact": round(stored_before / 1e9, 3),
            "stored_gb_after_compact": round(stored_after / 1e9, 3), "compact_s": round(compact_s, 3),
            "restore_gbs": round(total / restore_s / 1e9, 3), "restore_s": round(restore_s, 3),

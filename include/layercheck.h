@@ -280,6 +280,21 @@ lc_status lc_store_open(const char *dir, uint32_t n_layers, const uint64_t *reco
 lc_status lc_store_append(lc_store *s, int64_t step, const uint8_t *mask, const void *payload,
                           uint64_t payload_bytes, void *stream);
 
+/* The same append, overlapped with the caller's next steps (the staging drain
+ * of Section 3.5 runs beside training instead of in its stream): `stream`
+ * does NOT wait for the copies out of a device payload.  Instead the store
+ * records `reuse_event` (a hipEvent_t the caller created; required for a
+ * device payload) on its own stream behind the last copy, and the caller must
+ * order any later write to the payload after it (hipStreamWaitEvent, or
+ * hipEventSynchronize) -- typically by alternating between two staging
+ * buffers and waiting on the event of the one about to be packed again.  The
+ * event is re-recorded by every call that is given it.  For a host payload
+ * (written before the call returns) the event, if given, is recorded on
+ * `stream`.  The call still blocks while the pinned ring is full.  Errors as
+ * lc_store_append; after an error return nothing reads the payload any more. */
+lc_status lc_store_append_async(lc_store *s, int64_t step, const uint8_t *mask, const void *payload,
+                                uint64_t payload_bytes, void *stream, void *reuse_event);
+
 /* Waits until every appended version is durable and visible.  After an I/O
  * failure of the writers (a full disk, say) the failed version is dropped and
  * this and every later append return LC_ERR_BAD_STATE with the error. */

@@ -629,8 +629,15 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
   return LC_OK;
 }
 
-lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const void* payload, uint64_t bytes,
-                          void* stream) {
+}  // extern "C"
+
+namespace {
+
+// Both appends.  caller_waits: `stream` waits for the copies out of a device
+// payload (lc_store_append); otherwise `reuse_event` is recorded behind them
+// on the store's stream and `stream` runs on (lc_store_append_async).
+lc_status append_impl(lc_store* s, int64_t step, const uint8_t* mask, const void* payload, uint64_t bytes,
+                      void* stream, bool caller_waits, void* reuse_event) {
   if (!s || !mask) return fail(LC_ERR_INVALID_ARG, "store and mask must be non-NULL");
   StoredVersion v;
   v.step = step;
@@ -661,6 +668,8 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
     if (e == hipSuccess && attr.type == hipMemoryTypeDevice) device = true;
     else (void)hipGetLastError();
   }
+  if (device && !caller_waits && !reuse_event)
+    return fail(LC_ERR_INVALID_ARG, "a device payload needs reuse_event");
   char name[96];
   snprintf(name, sizeof(name), "v%010llu_s%lld.lcr", static_cast<unsigned long long>(s->seq++),
            static_cast<long long>(step));
@@ -699,7 +708,14 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
       } while (off < bytes);
     }
     s->cv.notify_all();
-    return wait_idle(s);
+    lc_status st = wait_idle(s);
+    if (st == LC_OK && !caller_waits && reuse_event) {
+      // the payload was written before this call returns: the event only
+      // has to follow the caller's work
+      const hipError_t e = hipEventRecord(static_cast<hipEvent_t>(reuse_event), static_cast<hipStream_t>(stream));
+      if (e != hipSuccess) return fail(LC_ERR_HIP, "event record failed: %s", hipGetErrorString(e));
+    }
+    return st;
   }
   lc_status st = ensure_gpu(s);
   if (st != LC_OK) {
@@ -729,6 +745,7 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
         const std::string why = s->writer_error;
         lk.unlock();
         abandon(s, vi, bytes - off, why.c_str());
+        (void)hipStreamSynchronize(s->copy_stream);  // nothing reads the payload after an error return
         return fail(LC_ERR_BAD_STATE, "store: %s", why.c_str());
       }
       for (uint32_t k = 0; k < s->n_slots; ++k)
@@ -746,6 +763,7 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
         s->slot_free[slot] = 1;  // nothing was queued on it
       }
       abandon(s, vi, bytes - off, "drain copy failed");
+      (void)hipStreamSynchronize(s->copy_stream);  // nothing reads the payload after an error return
       return fail(LC_ERR_HIP, "drain copy failed: %s", hipGetErrorString(e));
     }
     WriteJob job;
@@ -763,11 +781,32 @@ lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const 
     }
     s->cv.notify_all();
   }
-  // the caller's later work (the next pack into the same staging) waits for the copies
-  e = hipEventRecord(s->copies_done, s->copy_stream);
-  if (e == hipSuccess) e = hipStreamWaitEvent(cs, s->copies_done, 0);
-  if (e != hipSuccess) return fail(LC_ERR_HIP, "stream ordering failed: %s", hipGetErrorString(e));
+  if (caller_waits) {
+    // the caller's later work (the next pack into the same staging) waits for the copies
+    e = hipEventRecord(s->copies_done, s->copy_stream);
+    if (e == hipSuccess) e = hipStreamWaitEvent(cs, s->copies_done, 0);
+  } else {
+    e = hipEventRecord(static_cast<hipEvent_t>(reuse_event), s->copy_stream);
+  }
+  if (e != hipSuccess) {
+    (void)hipStreamSynchronize(s->copy_stream);
+    return fail(LC_ERR_HIP, "stream ordering failed: %s", hipGetErrorString(e));
+  }
   return LC_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const void* payload, uint64_t bytes,
+                          void* stream) {
+  return append_impl(s, step, mask, payload, bytes, stream, true, nullptr);
+}
+
+lc_status lc_store_append_async(lc_store* s, int64_t step, const uint8_t* mask, const void* payload,
+                                uint64_t bytes, void* stream, void* reuse_event) {
+  return append_impl(s, step, mask, payload, bytes, stream, false, reuse_event);
 }
 
 lc_status lc_store_sync(lc_store* s) {

@@ -25,9 +25,9 @@ LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
 EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
             "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_sgd_step_score", "lc_store_open",
-            "lc_store_append", "lc_store_sync", "lc_store_count", "lc_store_entry", "lc_store_plan",
-            "lc_store_restore", "lc_store_compact", "lc_store_discard_after", "lc_store_close", "lc_read_state",
-            "lc_record_bytes", "lc_destroy", "lc_last_error")
+            "lc_store_append", "lc_store_append_async", "lc_store_sync", "lc_store_count", "lc_store_entry",
+            "lc_store_plan", "lc_store_restore", "lc_store_compact", "lc_store_discard_after", "lc_store_close",
+            "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
 
 
 class lc_segment(C.Structure):
@@ -100,6 +100,8 @@ def load_library(path: str = LIB_PATH):
             "lc_store_open": (C.c_int, [C.c_char_p, C.c_uint32, P(C.c_uint64), C.c_uint64, P(C.c_void_p)]),
             "lc_store_append": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint8), C.c_void_p, C.c_uint64,
                                           C.c_void_p]),
+            "lc_store_append_async": (C.c_int, [C.c_void_p, C.c_int64, P(C.c_uint8), C.c_void_p, C.c_uint64,
+                                                C.c_void_p, C.c_void_p]),
             "lc_store_sync": (C.c_int, [C.c_void_p]),
             "lc_store_count": (C.c_int, [C.c_void_p, P(C.c_uint32)]),
             "lc_store_entry": (C.c_int, [C.c_void_p, C.c_uint32, P(C.c_int64), P(C.c_uint8), P(C.c_uint64)]),
@@ -257,6 +259,16 @@ class Store:
         m = np.ascontiguousarray(mask, dtype=np.uint8)
         _check(load_library().lc_store_append(self.h, step, m.ctypes.data_as(C.POINTER(C.c_uint8)), payload or None,
                                               payload_bytes, stream or None), "lc_store_append")
+
+    def append_async(self, step: int, mask, payload: int, payload_bytes: int, stream: int = 0,
+                     reuse_event: int = 0) -> None:
+        """lc_store_append_async: ``stream`` runs on; ``reuse_event`` (a raw
+        hipEvent_t, e.g. ``torch.cuda.Event().cuda_event`` once created) marks
+        when the payload may be overwritten."""
+        m = np.ascontiguousarray(mask, dtype=np.uint8)
+        _check(load_library().lc_store_append_async(self.h, step, m.ctypes.data_as(C.POINTER(C.c_uint8)),
+                                                    payload or None, payload_bytes, stream or None,
+                                                    reuse_event or None), "lc_store_append_async")
 
     def sync(self) -> None:
         _check(load_library().lc_store_sync(self.h), "lc_store_sync")

@@ -80,6 +80,13 @@ def test_append_validation(lib, tmp_path):
     st.append(5, m1, p1.ctypes.data, len(p1))
     st.append(5, m2, p2.ctypes.data, len(p2))
     assert st.plan(5).tolist() == [5, 0, 5, 0, 0]
+    # the overlapped append takes host payloads the same way (no event needed:
+    # the bytes are written before it returns), with the same validation
+    st.append_async(6, m1, p1.ctypes.data, len(p1))
+    with pytest.raises(LC.LCError):
+        st.append_async(6, m1, p1.ctypes.data, len(p1))
+    st.sync()
+    assert st.plan(6).tolist() == [6, 0, 5, 0, 0]
     st.close()
     with pytest.raises(LC.LCError):
         LC.Store(str(tmp_path / "bad"), [100, 256])  # record sizes are 256-byte multiples

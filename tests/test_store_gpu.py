@@ -3,8 +3,10 @@ recovery from it (Section 3.5), against the oracle.
 
 One staging buffer is reused every step with no synchronisation between
 lc_store_append and the next lc_pack_selected: the drain's copies must be
-stream-ordered before the next pack overwrites the buffer.  Small drain
-buffers force many chunks through the pinned ring."""
+stream-ordered before the next pack overwrites the buffer.  The overlapped
+variant alternates two staging buffers with lc_store_append_async, and the
+caller's stream waits only on the reuse event of the buffer it packs next.
+Small drain buffers force many chunks through the pinned ring."""
 import os
 
 import numpy as np
@@ -26,26 +28,39 @@ def _gpu():
     LC.load_library()
 
 
-@pytest.mark.parametrize("maker,mode,buf", [(reduced_8b, LC.LC_MODE_ACCUM, 1 << 20),
-                                            (reduced_qwen, LC.LC_MODE_SNAPSHOT, 3 << 20)],
-                         ids=["8b-accum", "qwen-snapshot"])
-def test_drain_and_restore_from_store(tmp_path, maker, mode, buf):
+@pytest.mark.parametrize("maker,mode,buf,overlapped", [(reduced_8b, LC.LC_MODE_ACCUM, 1 << 20, False),
+                                                       (reduced_qwen, LC.LC_MODE_SNAPSHOT, 3 << 20, False),
+                                                       (reduced_8b, LC.LC_MODE_ACCUM, 4 << 20, True),
+                                                       (reduced_qwen, LC.LC_MODE_SNAPSHOT, 64 << 20, True)],
+                         ids=["8b-accum", "qwen-snapshot", "8b-accum-overlapped", "qwen-snapshot-overlapped"])
+def test_drain_and_restore_from_store(tmp_path, maker, mode, buf, overlapped):
     import torch
     spec = maker()
     p = Pair(spec, mode, k0_for(spec, 0.01))
     d = str(tmp_path / "store")
     store = LC.Store(d, p.R, buffer_bytes=buf)
     try:
-        stream = torch.cuda.current_stream().cuda_stream
+        cur = torch.cuda.current_stream()
+        stream = cur.cuda_stream
         cap = sum(p.R)
-        staging = torch.empty(cap, dtype=torch.uint8, device="cuda")
+        stagings = [torch.empty(cap, dtype=torch.uint8, device="cuda") for _ in range(2 if overlapped else 1)]
+        events = [torch.cuda.Event() for _ in stagings]
+        for ev in events:
+            ev.record(cur)  # creates the underlying event
         expected = []
 
         def pack_and_drain(t, mask):
+            k = t % len(stagings)
+            staging = stagings[k]
+            if overlapped:
+                cur.wait_event(events[k])  # the copies out of this buffer's previous payload are done
             res = LC.lc_pack_selected(p.ctx, staging.data_ptr(), cap, 0)
             pay_o, res_o = p.orc.pack(0, cap)
             assert res == res_o
-            store.append(t, mask, staging.data_ptr(), res["bytes_written"], stream)  # no sync afterwards
+            if overlapped:
+                store.append_async(t, mask, staging.data_ptr(), res["bytes_written"], stream, events[k].cuda_event)
+            else:
+                store.append(t, mask, staging.data_ptr(), res["bytes_written"], stream)  # no sync afterwards
             expected.append({"step": t, "mask": mask.copy(), "payload": pay_o})
 
         pack_and_drain(0, np.ones(p.N, np.uint8))
@@ -81,6 +96,25 @@ def test_drain_and_restore_from_store(tmp_path, maker, mode, buf):
         p.adopt_restored()
         for t in range(t_fail + 1, t_fail + 3):
             p.step(t)
+    finally:
+        store.close()
+        p.close()
+
+
+def test_async_append_needs_an_event_for_device_payloads(tmp_path):
+    import torch
+    spec = reduced_8b()
+    p = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 0.01))
+    store = LC.Store(str(tmp_path / "s"), p.R)
+    try:
+        staging = torch.empty(sum(p.R), dtype=torch.uint8, device="cuda")
+        res = LC.lc_pack_selected(p.ctx, staging.data_ptr(), staging.numel(), 0)
+        with pytest.raises(LC.LCError) as e:
+            store.append_async(0, np.ones(p.N, np.uint8), staging.data_ptr(), res["bytes_written"],
+                               torch.cuda.current_stream().cuda_stream, 0)
+        assert e.value.code == LC.LC_ERR_INVALID_ARG
+        store.sync()
+        assert store.entries() == []  # refused before anything was written
     finally:
         store.close()
         p.close()
