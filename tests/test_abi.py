@@ -156,3 +156,16 @@ def test_invalid_init_enqueues_nothing(lib):
     bad = fake_segments([[4], [4]])
     bad[0].numel = 0
     _expect(LC.LC_ERR_INVALID_ARG, lambda: LC.lc_init_layout(desc(bad, 2)))
+
+
+def test_missing_library_fails_loudly(tmp_path):
+    """No fallback: without the built library the binding refuses to run."""
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    code = ("from paper_2609_27193_amd import layercheck as LC\n"
+            "try:\n    LC.load_library()\nexcept RuntimeError as e:\n    print('refused:', e)\n")
+    env = dict(os.environ, LAYERCHECK_LIB=str(tmp_path / "absent.so"), PYTHONPATH=root)
+    out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
+    assert out.returncode == 0, out.stderr
+    assert "refused:" in out.stdout and "not built" in out.stdout
