@@ -78,6 +78,7 @@ def parse():
 KERNEL_SOURCES = {
     "score_kernel": ("lc_device.h", "lc_internal.h", "lc_kernels.hip"),
     "adamw_kernel": ("lc_device.h", "lc_internal.h", "lc_optim.hip"),
+    "sgd_kernel": ("lc_device.h", "lc_internal.h", "lc_optim.hip"),
 }
 
 
@@ -688,8 +689,12 @@ def main_optim(args, spec, optimizer):
     decay = state.decay_mask()
     adam_t = 0
 
-    def fused(ctx, t, g):
-        ptrs = [g[s.offset:s.offset + s.numel].data_ptr() for s in state.segments]
+    def grad_ptrs(g):
+        """One device address per segment (the layout's order) into the flat gradient."""
+        base, esz = g.data_ptr(), g.element_size()
+        return [base + s.offset * esz for s in state.segments]
+
+    def fused(ctx, t, ptrs):
         if adamw:
             LC.lc_adamw_step_score(ctx, t, ptrs, LC.LC_DT_BF16, ADAMW["lr"], ADAMW["beta1"], ADAMW["beta2"],
                                    ADAMW["eps"], ADAMW["weight_decay"], adam_t, decay)
@@ -706,7 +711,7 @@ def main_optim(args, spec, optimizer):
             t += 1
             adam_t += 1
             g = state.gradients(t)
-            fused(ctx, t, g)
+            fused(ctx, t, grad_ptrs(g))
             LC.lc_select(ctx, t, 1.0)
             u_hist.append(LC.lc_read_state(ctx, spec.n_layers)[0])
             del g
@@ -739,10 +744,11 @@ def main_optim(args, spec, optimizer):
         t += 1
         adam_t += 1
         g = state.gradients(t)
+        ptrs = grad_ptrs(g)
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
         ev[0].record(stream)
-        fused(ctx, t, g)
+        fused(ctx, t, ptrs)
         ev[1].record(stream)
         mask, st = LC.lc_select(ctx, t, 1.0, spec.n_layers)
         ev[2].record(stream)
@@ -783,7 +789,7 @@ def main_optim(args, spec, optimizer):
         "roofline": {"bound": "hbm", "kernel": f"optim_kernel<{optimizer}> (+finalize)",
                      "achieved": round(opt_bytes / opt_ms / 1e6, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(opt_bytes / opt_ms / 1e6 / HBM_PEAK_GBS, 4),
-                     "traffic": measured_traffic("adamw_kernel", args.workload, "accum") if adamw else None},
+                     "traffic": measured_traffic(f"{optimizer}_kernel", args.workload, "accum")},
     }
     if args.torch_adamw_reference and adamw:
         del state, staging

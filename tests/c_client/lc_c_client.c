@@ -4,9 +4,12 @@
  * step of a recorded trajectory (score, select, pack into a fresh device
  * version buffer), then loses the live state and rebuilds it with the
  * composite restore, writing everything the library returned to a file that
- * the test compares with the oracle.
+ * the test compares with the oracle.  Every version is also appended to a
+ * persistence store with the overlapped append (a reuse event, the stream
+ * never waits), and the composite rebuilt from the store must equal the one
+ * rebuilt from the device versions byte for byte.
  *
- *   lc_c_client <input file> <output file>
+ *   lc_c_client <input file> <output file> <store directory>
  *
  * Input (little endian):
  *   "LCC1", u32 n_layers, u32 n_segments, u32 weight_dtype, u32 has_master,
@@ -105,8 +108,15 @@ static version_t pack_version(lc_ctx *c, int64_t step, const uint8_t *mask, uint
   return v;
 }
 
+/* Copies the live arrays to fresh host buffers. */
+static uint8_t *snapshot(const uint8_t *d, size_t n) {
+  uint8_t *h = (uint8_t *)xmalloc(n);
+  HIP(hipMemcpy(h, d, n, hipMemcpyDeviceToHost));
+  return h;
+}
+
 int main(int argc, char **argv) {
-  if (argc != 3) die("usage: lc_c_client <input> <output>");
+  if (argc != 4) die("usage: lc_c_client <input> <output> <store directory>");
   FILE *in = fopen(argv[1], "rb");
   if (!in) die("cannot open the input");
   out_f = fopen(argv[2], "wb");
@@ -205,10 +215,16 @@ int main(int argc, char **argv) {
   for (uint32_t l = 0; l < N; ++l)
     if (lc_record_bytes(c, l) != rec[l]) die("lc_record_bytes disagrees with lc_query_layout");
 
+  lc_store *store = NULL;
+  LC(lc_store_open(argv[3], N, rec, 8u << 20, &store));
+  hipEvent_t reuse;
+  HIP(hipEventCreateWithFlags(&reuse, hipEventDisableTiming));
+
   version_t *versions = (version_t *)xmalloc(sizeof(version_t) * (n_steps + 1));
   uint8_t *mask = (uint8_t *)xmalloc(N);
   memset(mask, 1, N);
   versions[0] = pack_version(c, t_base, mask, N, rec);
+  LC(lc_store_append_async(store, t_base, mask, versions[0].payload, versions[0].bytes, stream, reuse));
 
   double *u = (double *)xmalloc(8 * N), *delta = (double *)xmalloc(8 * N);
   int64_t *t_last = (int64_t *)xmalloc(8 * N);
@@ -229,6 +245,7 @@ int main(int argc, char **argv) {
     wr(&st.max_age, 8);
     wr(&st.weighted_age, 8);
     versions[k] = pack_version(c, t, mask, N, rec);
+    LC(lc_store_append_async(store, t, mask, versions[k].payload, versions[k].bytes, stream, reuse));
   }
 
   /* fail-stop: the live state is lost, then rebuilt from the versions */
@@ -250,19 +267,43 @@ int main(int argc, char **argv) {
   LC(lc_read_state(c, NULL, NULL, t_last));
   wr(chosen, 8 * N);
   wr(t_last, 8 * N);
+  uint8_t *rW = snapshot(dW, total * esz), *rS = snapshot(dS, total * esz);
+  uint8_t *rM = has_master ? snapshot(dM, total * 4) : NULL;
+  uint8_t *rm = snapshot(dm, total * 4), *rv = snapshot(dv, total * 4);
+  wr(rW, total * esz);
+  wr(rS, total * esz);
+  if (has_master) wr(rM, total * 4);
+  wr(rm, total * 4);
+  wr(rv, total * 4);
+
+  /* the same recovery from the store's files */
+  LC(lc_store_sync(store));
+  uint32_t n_stored = 0;
+  LC(lc_store_count(store, &n_stored));
+  if (n_stored != n_steps + 1) die("the store should hold every appended version");
+  int64_t *planned = (int64_t *)xmalloc(8 * N);
+  LC(lc_store_plan(store, t_fail, planned));
+  if (memcmp(planned, chosen, 8 * N)) die("the store's plan differs from the composite restore's");
+  HIP(hipMemset(dW, 0, total * esz));
+  HIP(hipMemset(dS, 0, total * esz));
+  if (has_master) HIP(hipMemset(dM, 0, total * 4));
+  HIP(hipMemset(dm, 0, total * 4));
+  HIP(hipMemset(dv, 0, total * 4));
+  HIP(hipDeviceSynchronize());
+  LC(lc_store_restore(store, c, t_fail, planned));
   uint8_t *h = (uint8_t *)xmalloc(total * 4);
-  HIP(hipMemcpy(h, dW, total * esz, hipMemcpyDeviceToHost));
-  wr(h, total * esz);
-  HIP(hipMemcpy(h, dS, total * esz, hipMemcpyDeviceToHost));
-  wr(h, total * esz);
-  if (has_master) {
-    HIP(hipMemcpy(h, dM, total * 4, hipMemcpyDeviceToHost));
-    wr(h, total * 4);
-  }
-  HIP(hipMemcpy(h, dm, total * 4, hipMemcpyDeviceToHost));
-  wr(h, total * 4);
-  HIP(hipMemcpy(h, dv, total * 4, hipMemcpyDeviceToHost));
-  wr(h, total * 4);
+#define SAME(dev, ref, n, what)                                   \
+  do {                                                            \
+    HIP(hipMemcpy(h, dev, n, hipMemcpyDeviceToHost));             \
+    if (memcmp(h, ref, n)) die("restore from the store: " what);  \
+  } while (0)
+  SAME(dW, rW, total * esz, "weights differ");
+  SAME(dS, rS, total * esz, "shadow differs");
+  if (has_master) SAME(dM, rM, total * 4, "master differs");
+  SAME(dm, rm, total * 4, "m differs");
+  SAME(dv, rv, total * 4, "v differs");
+  LC(lc_store_close(store));
+  HIP(hipEventDestroy(reuse));
 
   /* an error path through the interface: a restore before any version */
   if (lc_restore_composite(c, lv, n_steps + 1, t_base - 1, NULL) != LC_ERR_NO_VERSION)

@@ -6,7 +6,10 @@ step's weights, master and moments) to a file; the client allocates the
 arrays with hipMalloc (all segments of an array back to back in one
 allocation, so odd-sized tensors leave later segments misaligned), runs
 score, select and pack at every step into device version buffers, then
-loses the live state and restores the composite at t_fail.  Scores are
+loses the live state and restores the composite at t_fail; every version
+also goes through a persistence store (overlapped appends with a reuse
+event), and the client checks that the composite rebuilt from the store's
+files equals the device one byte for byte.  Scores are
 compared within the harness tolerance, masks, stats, payloads and restored
 arrays exactly (a layer whose accumulator sits inside the tolerance band of
 its threshold takes the client's decision on the oracle side)."""
@@ -92,7 +95,8 @@ def test_c_client_against_oracle(tmp_path, name, maker, mode):
             f.write(m.tobytes())
             f.write(v.tobytes())
     log(f"{name}: running the C client on {spec.numel} elements, {N} layers")
-    r = subprocess.run([C_CLIENT, str(fin), str(fout)], capture_output=True, text=True, timeout=120)
+    r = subprocess.run([C_CLIENT, str(fin), str(fout), str(tmp_path / "store")], capture_output=True, text=True,
+                       timeout=120)
     assert r.returncode == 0, r.stderr
     rd = Reader(open(fout, "rb").read())
 
