@@ -3,8 +3,9 @@
 // Every kernel here is HBM-bound streaming work or a tiny O(N) step; nothing
 // is a dense contraction, so there is no MFMA.  Design rules:
 //  * 16-byte (dwordx4) coalesced loads/stores, several in flight per lane;
-//    non-temporal hints because every byte is touched once per step and the
-//    per-step stream (tens of GB) dwarfs the 256 MB Infinity Cache;
+//    non-temporal, device-scope cache policy because every byte is touched
+//    once per step and the per-step stream (tens of GB) dwarfs the 256 MB
+//    Infinity Cache; full chunks and pieces go through buffer resources;
 //  * reductions use no floating-point atomics: one fp64 pair per chunk, then a
 //    fixed-order per-layer sum, so scores are bitwise reproducible;
 //  * wave64 reductions (DPP quad permutes, then cross-row shuffles), LDS for
@@ -85,17 +86,16 @@ __device__ __forceinline__ void score_chunk(const DeviceTables& t, uint32_t c) {
   double a = 0.0, b = 0.0;
   uint32_t scalar_from = 0;
   if (sg.vec_ok) {
-    const u32x4* wv = reinterpret_cast<const u32x4*>(wb);
-    u32x4* sv = reinterpret_cast<u32x4*>(sbp);
     if (n == CE) {
+      const tile_t tw = make_tile(wb, kChunkBytes), ts = make_tile(sbp, kChunkBytes);
 #pragma unroll
       for (uint32_t r = 0; r < VPT / U; ++r) {
         u32x4 w[U], s[U];
 #pragma unroll
         for (uint32_t k = 0; k < U; ++k) {
-          const uint32_t i = tid + (r * U + k) * kScoreThreads;
-          w[k] = ld_nt(wv + i);
-          s[k] = ld_nt(sv + i);
+          const uint32_t off = (tid + (r * U + k) * kScoreThreads) * 16u;
+          w[k] = ld_tile(tw, off);
+          s[k] = ld_tile(ts, off);
         }
 #pragma unroll
         for (uint32_t k = 0; k < U; ++k) {
@@ -103,11 +103,13 @@ __device__ __forceinline__ void score_chunk(const DeviceTables& t, uint32_t c) {
           vec_terms<DT>(w[k], s[k], da, db);
           a += static_cast<double>(da);
           b += static_cast<double>(db);
-          if constexpr (ACCUM) st_nt(sv + tid + (r * U + k) * kScoreThreads, w[k]);
+          if constexpr (ACCUM) st_tile(ts, (tid + (r * U + k) * kScoreThreads) * 16u, w[k]);
         }
       }
       scalar_from = n;
     } else {
+      const u32x4* wv = reinterpret_cast<const u32x4*>(wb);
+      u32x4* sv = reinterpret_cast<u32x4*>(sbp);
       const uint32_t nv = n / EPV;
       for (uint32_t i = tid; i < nv; i += kScoreThreads) {
         const u32x4 w = ld_nt(wv + i);
@@ -255,22 +257,24 @@ __device__ __forceinline__ void copy_piece(const uint8_t* __restrict__ src, uint
   const uint32_t tid = threadIdx.x;
   uint32_t done = 0;
   if (vec) {
-    const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
-    u32x4* d4 = reinterpret_cast<u32x4*>(dst);
-    u32x4* e4 = reinterpret_cast<u32x4*>(dst2);
     if (len == kPieceBytes) {
       constexpr uint32_t V = kPieceBytes / 16 / kCopyThreads;
+      const tile_t ts = make_tile(src, kPieceBytes), td = make_tile(dst, kPieceBytes);
       u32x4 v[V];
 #pragma unroll
-      for (uint32_t k = 0; k < V; ++k) v[k] = ld_nt(s4 + tid + k * kCopyThreads);
+      for (uint32_t k = 0; k < V; ++k) v[k] = ld_tile(ts, (tid + k * kCopyThreads) * 16u);
 #pragma unroll
-      for (uint32_t k = 0; k < V; ++k) st_nt(d4 + tid + k * kCopyThreads, v[k]);
+      for (uint32_t k = 0; k < V; ++k) st_tile(td, (tid + k * kCopyThreads) * 16u, v[k]);
       if (dst2) {
+        const tile_t te = make_tile(dst2, kPieceBytes);
 #pragma unroll
-        for (uint32_t k = 0; k < V; ++k) st_nt(e4 + tid + k * kCopyThreads, v[k]);
+        for (uint32_t k = 0; k < V; ++k) st_tile(te, (tid + k * kCopyThreads) * 16u, v[k]);
       }
       return;
     }
+    const u32x4* s4 = reinterpret_cast<const u32x4*>(src);
+    u32x4* d4 = reinterpret_cast<u32x4*>(dst);
+    u32x4* e4 = reinterpret_cast<u32x4*>(dst2);
     const uint32_t nv = len / 16;
     for (uint32_t i = tid; i < nv; i += kCopyThreads) {
       const u32x4 x = ld_nt(s4 + i);

@@ -4,7 +4,8 @@
 // over to.  One pass over the optimizer state per step; per chunk of the
 // score layout the kernel updates the parameters and writes the Eq. 1
 // partial sums of |p_new - p| and |p|, which the finalize kernel turns into
-// u and Delta.  Streaming rules as in lc_kernels.hip.
+// u and Delta.  Streaming rules as in lc_kernels.hip (full chunks through
+// buffer resources, ragged ones through global pointers).
 #include "lc_device.h"
 
 namespace lc {
@@ -61,40 +62,63 @@ __device__ __forceinline__ float sgd_elem(float p, float g, const SgdScalars& sc
   return p1 - sc.lr * g;
 }
 
-// Four consecutive elements starting at element 4*gi (all arrays 4-element
-// aligned).  AdamW also streams m and v; SGD touches only the parameters.
+// The tiles of one full chunk: the parameters (the fp32 master, else the
+// weights), the weights, the gradient and, for AdamW, the moments.
+struct ChunkTiles {
+  tile_t p, w, g, m, v;
+};
+
+__device__ __forceinline__ u32x4 widen_bf16x4(u32x2 x) {
+  return u32x4{x[0] << 16, x[0] & 0xffff0000u, x[1] << 16, x[1] & 0xffff0000u};
+}
+__device__ __forceinline__ u32x2 narrow_bf16x4(u32x4 p) {
+  return u32x2{bf16_rne(__uint_as_float(p[0])) | (static_cast<uint32_t>(bf16_rne(__uint_as_float(p[1]))) << 16),
+               bf16_rne(__uint_as_float(p[2])) | (static_cast<uint32_t>(bf16_rne(__uint_as_float(p[3]))) << 16)};
+}
+
+// Four consecutive elements (every array 4-element aligned): loaded through
+// global pointers (group gi of the segment, ragged chunks) or through the
+// chunk's tiles (group j of a full chunk), updated in place, stored the same
+// way.  AdamW also streams m and v; SGD touches only the parameters.
 template <int OPT, int WDT, int GDT, bool MASTER>
 struct Group4 {
-  u32x4 p, m, v;
+  u32x4 p, m, v;  // parameters as fp32 bits, moments
   float g[4];
+
+  __device__ __forceinline__ void set_grad(u32x2 x) {
+    g[0] = __uint_as_float(x[0] << 16); g[1] = __uint_as_float(x[0] & 0xffff0000u);
+    g[2] = __uint_as_float(x[1] << 16); g[3] = __uint_as_float(x[1] & 0xffff0000u);
+  }
+  __device__ __forceinline__ void set_grad(u32x4 x) {
+    for (int k = 0; k < 4; ++k) g[k] = __uint_as_float(x[k]);
+  }
   __device__ __forceinline__ void load(const OptSeg& sg, const GradSeg& gs, uint64_t gi) {
-    if constexpr (MASTER) {
-      p = ld_nt(reinterpret_cast<const u32x4*>(sg.master) + gi);
-    } else if constexpr (WDT == 1) {
-      const u32x2 w = ld_nt2(reinterpret_cast<const u32x2*>(sg.w) + gi);
-      p = u32x4{w[0] << 16, w[0] & 0xffff0000u, w[1] << 16, w[1] & 0xffff0000u};
-    } else {
-      p = ld_nt(reinterpret_cast<const u32x4*>(sg.w) + gi);
-    }
+    if constexpr (MASTER) p = ld_nt(reinterpret_cast<const u32x4*>(sg.master) + gi);
+    else if constexpr (WDT == 1) p = widen_bf16x4(ld_nt2(reinterpret_cast<const u32x2*>(sg.w) + gi));
+    else p = ld_nt(reinterpret_cast<const u32x4*>(sg.w) + gi);
     if constexpr (OPT == kAdamW) {
       m = ld_nt(reinterpret_cast<const u32x4*>(sg.m) + gi);
       v = ld_nt(reinterpret_cast<const u32x4*>(sg.v) + gi);
     }
-    if constexpr (GDT == 1) {
-      const u32x2 x = ld_nt2(reinterpret_cast<const u32x2*>(gs.grad) + gi);
-      g[0] = __uint_as_float(x[0] << 16); g[1] = __uint_as_float(x[0] & 0xffff0000u);
-      g[2] = __uint_as_float(x[1] << 16); g[3] = __uint_as_float(x[1] & 0xffff0000u);
-    } else {
-      const u32x4 x = ld_nt(reinterpret_cast<const u32x4*>(gs.grad) + gi);
-      for (int k = 0; k < 4; ++k) g[k] = __uint_as_float(x[k]);
-    }
+    if constexpr (GDT == 1) set_grad(ld_nt2(reinterpret_cast<const u32x2*>(gs.grad) + gi));
+    else set_grad(ld_nt(reinterpret_cast<const u32x4*>(gs.grad) + gi));
   }
-  // update in place; returns the drift terms (sum|p_new - p|, sum|p|) of the group
+  __device__ __forceinline__ void load(const ChunkTiles& t, uint32_t j) {
+    if constexpr (MASTER) p = ld_tile(t.p, j * 16u);
+    else if constexpr (WDT == 1) p = widen_bf16x4(ld_tile2(t.p, j * 8u));
+    else p = ld_tile(t.p, j * 16u);
+    if constexpr (OPT == kAdamW) {
+      m = ld_tile(t.m, j * 16u);
+      v = ld_tile(t.v, j * 16u);
+    }
+    if constexpr (GDT == 1) set_grad(ld_tile2(t.g, j * 8u));
+    else set_grad(ld_tile(t.g, j * 16u));
+  }
+  // One optimizer step of the four elements in place; returns the drift terms
+  // (sum|p_new - p|, sum|p|) of the group.
   template <typename SC>
-  __device__ __forceinline__ void step_store(const OptSeg& sg, uint64_t gi, const SC& sc, bool decay, float& da,
-                                             float& db) {
+  __device__ __forceinline__ void update(const SC& sc, bool decay, float& da, float& db) {
     float d[4], b[4];
-    u32x4 pn, mn, vn;
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const float po = __uint_as_float(p[k]);
@@ -102,31 +126,35 @@ struct Group4 {
       if constexpr (OPT == kAdamW) {
         float mm = __uint_as_float(m[k]), vv = __uint_as_float(v[k]);
         x = adamw_elem(po, mm, vv, g[k], sc, decay);
-        mn[k] = __float_as_uint(mm);
-        vn[k] = __float_as_uint(vv);
+        m[k] = __float_as_uint(mm);
+        v[k] = __float_as_uint(vv);
       } else {
         x = sgd_elem(po, g[k], sc, decay);
       }
-      pn[k] = __float_as_uint(x);
+      p[k] = __float_as_uint(x);
       d[k] = fabsf(x - po);
       b[k] = fabsf(po);
     }
     da = (d[0] + d[1]) + (d[2] + d[3]);
     db = (b[0] + b[1]) + (b[2] + b[3]);
+  }
+  __device__ __forceinline__ void store(const OptSeg& sg, uint64_t gi) const {
     if constexpr (OPT == kAdamW) {
-      st_nt(reinterpret_cast<u32x4*>(sg.m) + gi, mn);
-      st_nt(reinterpret_cast<u32x4*>(sg.v) + gi, vn);
+      st_nt(reinterpret_cast<u32x4*>(sg.m) + gi, m);
+      st_nt(reinterpret_cast<u32x4*>(sg.v) + gi, v);
     }
-    if constexpr (MASTER) st_nt(reinterpret_cast<u32x4*>(sg.master) + gi, pn);
-    if constexpr (WDT == 1) {
-      const uint32_t lo = bf16_rne(__uint_as_float(pn[0])) |
-                          (static_cast<uint32_t>(bf16_rne(__uint_as_float(pn[1]))) << 16);
-      const uint32_t hi = bf16_rne(__uint_as_float(pn[2])) |
-                          (static_cast<uint32_t>(bf16_rne(__uint_as_float(pn[3]))) << 16);
-      st_nt2(reinterpret_cast<u32x2*>(sg.w) + gi, u32x2{lo, hi});
-    } else {
-      st_nt(reinterpret_cast<u32x4*>(sg.w) + gi, pn);
+    if constexpr (MASTER) st_nt(reinterpret_cast<u32x4*>(sg.master) + gi, p);
+    if constexpr (WDT == 1) st_nt2(reinterpret_cast<u32x2*>(sg.w) + gi, narrow_bf16x4(p));
+    else st_nt(reinterpret_cast<u32x4*>(sg.w) + gi, p);
+  }
+  __device__ __forceinline__ void store(const ChunkTiles& t, uint32_t j) const {
+    if constexpr (OPT == kAdamW) {
+      st_tile(t.m, j * 16u, m);
+      st_tile(t.v, j * 16u, v);
     }
+    if constexpr (MASTER) st_tile(t.p, j * 16u, p);
+    if constexpr (WDT == 1) st_tile2(t.w, j * 8u, narrow_bf16x4(p));
+    else st_tile(t.w, j * 16u, p);
   }
 };
 
@@ -150,13 +178,24 @@ __device__ __forceinline__ void optim_chunk(const DeviceTables& t, const SC& sc,
     const uint64_t g0 = e0 / 4;
     const uint32_t ng = n / 4;
     if (ng == GPT * kScoreThreads) {
+      constexpr uint32_t GSZ = GDT == 1 ? 2 : 4;
+      ChunkTiles tl;
+      tl.w = make_tile(reinterpret_cast<const uint8_t*>(sg.w) + e0 * WSZ, CE * WSZ);
+      tl.p = MASTER ? make_tile(reinterpret_cast<const float*>(sg.master) + e0, CE * 4) : tl.w;
+      tl.g = make_tile(reinterpret_cast<const uint8_t*>(gs.grad) + e0 * GSZ, CE * GSZ);
+      tl.m = tl.v = tl.p;
+      if constexpr (OPT == kAdamW) {
+        tl.m = make_tile(reinterpret_cast<const float*>(sg.m) + e0, CE * 4);
+        tl.v = make_tile(reinterpret_cast<const float*>(sg.v) + e0, CE * 4);
+      }
       Group4<OPT, WDT, GDT, MASTER> grp[GPT];
 #pragma unroll
-      for (uint32_t k = 0; k < GPT; ++k) grp[k].load(sg, gs, g0 + tid + k * kScoreThreads);
+      for (uint32_t k = 0; k < GPT; ++k) grp[k].load(tl, tid + k * kScoreThreads);
 #pragma unroll
       for (uint32_t k = 0; k < GPT; ++k) {
         float da, db;
-        grp[k].step_store(sg, g0 + tid + k * kScoreThreads, sc, decay, da, db);
+        grp[k].update(sc, decay, da, db);
+        grp[k].store(tl, tid + k * kScoreThreads);
         a += static_cast<double>(da);
         b += static_cast<double>(db);
       }
@@ -165,7 +204,8 @@ __device__ __forceinline__ void optim_chunk(const DeviceTables& t, const SC& sc,
         Group4<OPT, WDT, GDT, MASTER> grp;
         grp.load(sg, gs, g0 + i);
         float da, db;
-        grp.step_store(sg, g0 + i, sc, decay, da, db);
+        grp.update(sc, decay, da, db);
+        grp.store(sg, g0 + i);
         a += static_cast<double>(da);
         b += static_cast<double>(db);
       }
