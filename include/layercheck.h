@@ -312,10 +312,12 @@ lc_status lc_store_entry(lc_store *s, uint32_t i, int64_t *step_out, uint8_t *ma
 lc_status lc_store_plan(lc_store *s, int64_t t_fail, int64_t *chosen_step_out);
 
 /* Composite recovery from the store (Section 3.5 steps 2-3): reads only the
- * chosen record of every layer (double-buffered pinned reads, several reader
- * threads) and restores it into the context's arrays exactly as
- * lc_restore_composite does.  The context's layout must match the store's
- * record sizes.  Returns after the restore has completed. */
+ * chosen record of every layer and restores it into the context's arrays
+ * exactly as lc_restore_composite does.  The records stream in 64 MiB pieces
+ * through a 2 GiB pinned ring (allocated for the call) that eight reader
+ * threads fill while the host-to-device copies of earlier pieces run.  The
+ * context's layout must match the store's record sizes.  Returns after the
+ * restore has completed on the device. */
 lc_status lc_store_restore(lc_store *s, lc_ctx *c, int64_t t_fail, int64_t *chosen_step_out);
 
 /* Storage reclamation: removes the versions that no reconstruction plan with
