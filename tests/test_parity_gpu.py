@@ -136,6 +136,29 @@ def test_restore_composite_then_continue(where):
         p.close()
 
 
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_rebase_mid_run_then_restore(mode):
+    """A full base checkpoint in the middle of a run (Section 3.4's base,
+    taken again after an unscored stretch): Delta and t_l reset, the shadow
+    re-synchronised and every layer packed, both sides alike; the decisions
+    after it agree, and a composite restore never reaches back past it."""
+    spec = reduced_8b()
+    p = Pair(spec, mode, k0_for(spec, 0.01))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        run_steps(p, range(1, 4))
+        p.advance(4)  # the weights move with no decision at step 4
+        p.pack(4, p.rebase(4))
+        run_steps(p, range(5, 9))
+        chosen = _restore_and_compare(p, 7, "device")
+        log(f"  restored from steps {sorted(set(chosen.tolist()))}")
+        assert min(chosen.tolist()) >= 4
+        p.adopt_restored()
+        run_steps(p, range(8, 10))
+    finally:
+        p.close()
+
+
 def _mean_scores(spec, steps):
     """Per-layer mean of u over the first ``steps`` steps of the synthetic
     trajectory, from an oracle-only dry run (no selection by drift)."""
