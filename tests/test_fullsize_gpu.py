@@ -15,9 +15,10 @@ and properties that hold at any size cover the rest:
   through capacity-limited multi-call packs where the state leaves no room
   for worst-case staging;
 * Qwen2.5-14B: composite recovery from six versions at steps 0..5 (base in
-  pageable host memory, partial versions on the device) with t_fail = 4, the
-  plan against the oracle's, sampled layers against their persisted truth,
-  and a restore -> re-pack round trip of every layer.
+  pageable host memory, partial versions on the device) with t_fail = 4,
+  mixing five timestamps, the plan against the oracle's, sampled layers
+  against their persisted truth, and a restore -> re-pack round trip of
+  every layer.
 """
 import numpy as np
 import pytest
@@ -199,24 +200,21 @@ def test_fullsize_decision_steps(name, mode, k0):
 
 @pytest.mark.timeout(900)
 def test_fullsize_qwen14b_composite_restore_six_versions():
-    """Qwen2.5-14B-shaped state (bf16 W, fp32 m/v, no master, S_max = 6).
-    Per-layer thresholds make layers cross at different steps so the
-    composite mixes several timestamps."""
+    """Qwen2.5-14B-shaped state (bf16 W, fp32 m/v, no master, S_max = 6):
+    the base at step 0 and the selections of steps 1-5, recovered at
+    t_fail = 4, so the step-5 version must be ignored.  Four blocks get a
+    threshold far below any drift; one of them changes at every step, the
+    other three only at step 3, 2 or 1 respectively (their weights are put
+    back after every other step, which also scores them exactly zero), so the
+    composite mixes five timestamps: 4, 3, 2, 1 and the base for every other
+    layer, whose threshold only the staleness guard (at step 6) would meet."""
     import torch
     spec = I.qwen25_14b_spec()
     N = spec.n_layers
-    # measure one step of scores to place the thresholds, then regenerate step 0
-    probe = FullRun(spec, LC.LC_MODE_ACCUM, [float("inf")] * N, staging_cap=1 << 30)
-    probe.state.step(1)
-    LC.lc_score_layers(probe.ctx, 1)
-    u1 = LC.lc_read_state(probe.ctx, N)[0]
-    probe.close()
-    del probe
-    torch.cuda.empty_cache()
-    fast = [l for l in range(N) if u1[l] > 0.5 * max(u1)]
-    k0 = [1e9] * N  # slow layers only by the guard (at t = 6, after t_fail)
-    for i, l in enumerate(fast):
-        k0[l] = u1[l] * (2 + i % 4) * 0.97  # crosses after about 2..5 steps
+    moving = {1: None, 2: 3, 3: 2, 4: 1}  # layer -> the only step it changes at (None: every step)
+    k0 = [1e9] * N
+    for l in moving:
+        k0[l] = 1e-12
     run = FullRun(spec, LC.LC_MODE_ACCUM, k0, staging_cap=1 << 30)
     try:
         total = sum(run.R)
@@ -236,12 +234,26 @@ def test_fullsize_qwen14b_composite_restore_six_versions():
         del chunk
         torch.cuda.empty_cache()
         versions = [{"step": 0, "mask": np.ones(N, np.uint8), "buf": base_host}]
-        sampled = sorted(set([0, N - 1, N - 2] + fast[:3] + [l for l in range(1, N - 2) if l not in fast][:2]))
+        sampled = sorted(set([0, N - 1, N - 2, 5, N // 2] + list(moving)))
         truth = {(l, 0): run.host_layer(l, ("weight", "exp_avg", "exp_avg_sq")) for l in sampled}
         for t in range(1, 6):
+            held = {}
+            for l, only in moving.items():
+                if only is not None and only != t:
+                    a, b = run.state.layer_range(l)
+                    held[l] = run.state.weight[a:b].clone()
             run.state.step(t)
+            for l, w in held.items():  # this layer does not move at step t
+                a, b = run.state.layer_range(l)
+                run.state.weight[a:b].copy_(w)
+            del held
             LC.lc_score_layers(run.ctx, t)
+            u = LC.lc_read_state(run.ctx, N)[0]
+            for l, only in moving.items():
+                assert (u[l] == 0.0) == (only is not None and only != t), (t, l, u[l])
             mask, st = LC.lc_select(run.ctx, t, 1.0, N)
+            assert sorted(np.flatnonzero(mask).tolist()) == sorted(
+                l for l, only in moving.items() if only is None or only == t), (t, mask)
             dev = torch.empty(max(st["payload_bytes"], 256), dtype=torch.uint8, device="cuda")
             if st["payload_bytes"]:
                 res = LC.lc_pack_selected(run.ctx, dev.data_ptr(), st["payload_bytes"], 0)
@@ -256,7 +268,8 @@ def test_fullsize_qwen14b_composite_restore_six_versions():
         expect = [versions[i]["step"] for i in expect_idx]
         stamps = sorted(set(expect))
         log(f"  composite timestamps for t_fail={t_fail}: {stamps}")
-        assert len(stamps) >= 3
+        assert stamps == [0, 1, 2, 3, 4]
+        assert [expect[l] for l in moving] == [4, 3, 2, 1]
         # fail-stop: live state lost
         for a in (run.state.weight, run.state.shadow, run.state.exp_avg, run.state.exp_avg_sq):
             a.zero_()
