@@ -91,6 +91,7 @@ class Pair:
         assert self.R == self.orc.R
         self.near_excluded = 0
         self.resyncs = 0
+        self.max_pack_calls = 0  # most lc_pack_selected calls one pack needed
         self.versions_dev = []  # (step, mask, device tensor)
         self.versions_host = []  # (step, mask, numpy payload from the oracle)
 
@@ -161,9 +162,10 @@ class Pair:
         staging = self.torch.empty(max(total, 1), dtype=self.torch.uint8, device="cuda")
         cap = total if capacity is None else capacity
         parts_g, parts_o = [], []
-        rank = 0
+        rank, calls = 0, 0
         while True:
             res = LC.lc_pack_selected(self.ctx, staging.data_ptr(), cap, rank)
+            calls += 1
             pay_o, res_o = self.orc.pack(rank, cap)
             assert res == res_o, (res, res_o)
             self.torch.cuda.synchronize()
@@ -174,6 +176,7 @@ class Pair:
             if res["done"]:
                 break
             rank = res["next_rank"]
+        self.max_pack_calls = max(self.max_pack_calls, calls)
         payload = np.concatenate(parts_o) if parts_o else np.zeros(0, np.uint8)
         assert len(payload) == total
         if keep_versions:

@@ -40,27 +40,41 @@ def reduced_13b():
     return I.scaled_spec(I.llama2_13b_spec(), hidden=320, ffn=864, n_blocks=4, vocab=640, n_q=5, n_kv=5)
 
 
-def run_steps(p, steps, lr=lambda t: 1.0, capacity=None):
+def run_steps(p, steps, lr=lambda t: 1.0, capacity=None, stats=None):
     fracs = []
     for t in steps:
         mask, st = p.step(t, lr(t), capacity(t) if capacity else None)
         fracs.append(mask.mean())
+        if stats is not None:
+            stats.append(st)
         log(f"  step {t}: selected {st['n_selected']}/{p.N} forced {st['n_forced']} "
             f"payload {st['payload_bytes']} max_age {st['max_age']} w_age {st['weighted_age']:.3f}")
     return fracs
 
 
+def assert_both_rules_fired(stats):
+    """Some layer was persisted by its accumulated drift (Eq. 3) and some only
+    by the staleness guard (Section 3.3) during the run."""
+    assert any(st["n_selected"] > st["n_forced"] for st in stats), stats
+    assert any(st["n_forced"] > 0 for st in stats), stats
+
+
 @pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
 def test_toy_ten_steps(mode):
-    """The toy decoder (fp32 weights, 3.67M params, S_max = 4) for 10 steps."""
+    """The toy decoder (fp32 weights, 3.67M params, S_max = 4) for 10 steps;
+    K0 = 0.02 persists about a quarter of the layers per step, by drift on
+    some steps and by the staleness guard on others."""
     spec = I.toy_spec()
     log(f"toy mode={mode}")
-    p = Pair(spec, mode, k0_for(spec, 0.08))
+    p = Pair(spec, mode, k0_for(spec, 0.02))
     try:
         p.pack(0, np.ones(p.N, np.uint8))  # base version
-        fracs = run_steps(p, range(1, 11))
+        stats = []
+        fracs = run_steps(p, range(1, 11), stats=stats)
         log(f"  mean selected fraction {np.mean(fracs):.3f}; near-threshold excluded {p.near_excluded}, "
             f"resyncs {p.resyncs}")
+        assert 0.15 <= np.mean(fracs) <= 0.35
+        assert_both_rules_fired(stats)
         p.check_arrays()
     finally:
         p.close()
@@ -78,7 +92,10 @@ def test_reduced_bf16(maker, mode):
     try:
         p.pack(0, np.ones(p.N, np.uint8))
         cap = lambda t: (max(p.R) + 4096) if t % 3 == 0 else None  # several pack calls on some steps
-        run_steps(p, range(1, 13), lr=lambda t: 1.0 if t < 6 else 0.5, capacity=cap)
+        stats = []
+        run_steps(p, range(1, 13), lr=lambda t: 1.0 if t < 6 else 0.5, capacity=cap, stats=stats)
+        assert_both_rules_fired(stats)
+        assert p.max_pack_calls > 1
         p.check_arrays()
     finally:
         p.close()
