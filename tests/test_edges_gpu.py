@@ -10,6 +10,7 @@ from paper_2609_27193_amd import inputs as I
 from paper_2609_27193_amd import layercheck as LC
 from tests.conftest import gpu_available
 from tests.gpu_harness import Pair, log
+from tests.test_parity_gpu import assert_both_rules_fired
 
 pytestmark = pytest.mark.gpu
 
@@ -38,13 +39,13 @@ def odd_spec(weight_dtype, has_master, s_max=3):
                                                ("f32", False, LC.LC_MODE_ACCUM), ("f32", True, LC.LC_MODE_SNAPSHOT)])
 def test_odd_sizes_misaligned(dtype, master, mode):
     spec = odd_spec(dtype, master)
-    p = Pair(spec, mode, [0.05] * spec.n_layers)
+    p = Pair(spec, mode, [0.02] * spec.n_layers)  # both the threshold and the guard fire
     try:
         aligned = [seg.weight % 16 == 0 for seg in p.lsegs]
         assert not all(aligned), "layout should contain misaligned segments"
         p.pack(0, np.ones(p.N, np.uint8), capacity=max(p.R))
-        for t in range(1, 8):
-            p.step(t, capacity=max(p.R) if t % 2 else None)
+        stats = [p.step(t, capacity=max(p.R) if t % 2 else None)[1] for t in range(1, 8)]
+        assert_both_rules_fired(stats)
         p.check_arrays()
     finally:
         p.close()
