@@ -203,7 +203,7 @@ def cpu_baseline(state, spec, mode_name, n_layers=3):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build measures one GPU only; --gpus must be 1 "
+        print(json.dumps({"error": "the benchmark measures one GPU only; --gpus must be 1 "
                                    "(the decision step is per-rank, see the design notes on sharding)"}))
         sys.exit(2)
     if args.ceilings:
