@@ -218,7 +218,7 @@ def test_fullsize_qwen14b_composite_restore_six_versions():
     run = FullRun(spec, LC.LC_MODE_ACCUM, k0, staging_cap=1 << 30)
     try:
         total = sum(run.R)
-        # 148 GB cannot be page-locked on this host; the base lives in pageable
+        # 148 GB is more than the page-locking limit allows; the base lives in pageable
         # memory, which the library restores through staged host copies
         log(f"  base version {total / 1e9:.1f} GB -> pageable host memory")
         base_host = torch.empty(total, dtype=torch.uint8)
