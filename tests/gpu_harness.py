@@ -30,13 +30,17 @@ def log(*a):
 
 
 def rel_ok(g, o):
+    """Within REL relative; a zero, an infinity or a NaN (Eq. 1 with eps_w = 0
+    on an all-zero layer is 0/0) must appear on both sides."""
     g = np.asarray(g, dtype=np.float64)
     o = np.asarray(o, dtype=np.float64)
+    if np.any(np.isnan(g) != np.isnan(o)):
+        return False
     zero = (o == 0) | (g == 0)
     if np.any(zero & (g != o)):
         return False
     both_inf = np.isinf(o) & np.isinf(g) & (np.sign(o) == np.sign(g))
-    nz = ~zero & ~both_inf
+    nz = ~zero & ~both_inf & ~np.isnan(o)
     return bool(np.all(np.abs(g[nz] - o[nz]) <= REL * np.abs(o[nz])))
 
 

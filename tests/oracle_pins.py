@@ -222,6 +222,31 @@ def check_k0_extremes(cls):
         orc.pack(0, 1 << 40)
 
 
+def check_zero_layer(cls, mode=O.MODE_ACCUM):
+    # A layer that is all zeros and stays zero.  With eps_w = 0, Eq. 1 is 0/0
+    # for it: u and Delta are NaN, the drift rule (Delta >= K) never holds for
+    # it, and the staleness guard still persists it every S_max steps.  With
+    # eps_w > 0 the same layer scores exactly 0.  The other layer moves every
+    # step and persists by drift every step.
+    for eps in (0.0, 1e-8):
+        segs = [_seg(0, np.zeros(4, np.float32), np.zeros(4, np.float32), O.DT_F32),
+                _seg(1, np.full(4, 0.5, np.float32), np.full(4, 0.5, np.float32), O.DT_F32)]
+        orc = cls(segs, 2, O.DT_F32, True, mode, [1e-30, 1e-30], s_max=3, eps_w=eps)
+        orc.pack(0, 1 << 30)
+        for t in range(1, 8):
+            segs[1].weight[...] = 0.5 + t * 2.0 ** -8
+            orc.score(t)
+            if eps == 0.0:
+                assert np.isnan(orc.u[0]) and np.isnan(orc.delta[0]), (t, orc.u[0])
+            else:
+                assert orc.u[0] == 0.0 and orc.delta[0] == 0.0
+            assert orc.u[1] > 0
+            mask, st = orc.select(t, 1.0)
+            assert list(mask) == [int(t % 3 == 0), 1], (eps, t, mask)
+            assert st["n_forced"] == int(t % 3 == 0)
+            orc.pack(0, 1 << 30)
+
+
 def check_rebase(cls, mode=O.MODE_ACCUM):
     # Section 3.4: a full base checkpoint at the end of the warm-up window.
     # (1) It resets Delta and t_l: u(1) = 2^-7 exactly, then the rebase at

@@ -65,6 +65,48 @@ def test_single_layer_smax_one():
         p.close()
 
 
+def test_all_zero_layer_with_eps_zero():
+    """A layer whose weights are zero and stay zero while the others move.
+    With eps_w = 0, Eq. 1 is 0/0 for it from the second step on: both sides
+    give NaN, its accumulator stays NaN, the drift rule never fires for it and
+    the staleness guard still persists it every S_max steps."""
+    from tests.test_parity_gpu import reduced_8b
+    spec = reduced_8b()
+    z = 1  # block_0
+    p = Pair(spec, LC.LC_MODE_ACCUM, [1e-30] * spec.n_layers, eps_w=0.0)
+    try:
+        a, b = p.gen.layer_range(z)
+
+        def zero():
+            p.dW[a:b].zero_()
+            p.hW[a:b] = 0
+            if p.dM is not None:
+                p.dM[a:b].zero_()
+                p.hM[a:b] = 0
+            p.torch.cuda.synchronize()
+
+        zero()  # the shadow still holds the initial weights: u = 1 at step 1
+        p.pack(0, np.ones(p.N, np.uint8))
+        for t in range(1, 2 * spec.s_max + 2):
+            p.advance(t)
+            zero()
+            d, tl = p.score(t)
+            u = LC.lc_read_state(p.ctx, p.N)[0]
+            if t == 1:
+                assert u[z] == 1.0
+            else:
+                assert np.isnan(u[z]) and np.isnan(d[z])
+            mask, st = p.select(t, 1.0, d, tl)
+            due = (t - 1) % spec.s_max == 0
+            assert mask[z] == 1 if due else mask[z] == 0, (t, mask)
+            if due and t > 1:  # z's accumulator is NaN: only the guard can have selected it
+                assert st["n_forced"] >= 1
+            p.pack(t, mask)
+        p.check_arrays()
+    finally:
+        p.close()
+
+
 def test_threshold_zero_selects_everything_and_no_change_scores_zero():
     spec = odd_spec("bf16", True, s_max=1000)
     p = Pair(spec, LC.LC_MODE_ACCUM, [0.0] * spec.n_layers)
