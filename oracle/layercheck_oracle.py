@@ -37,7 +37,8 @@ selected layers in ascending layer id, each record [W | master | m | v],
 every (array, tensor) block zero-padded to a multiple of 256 bytes) is this
 implementation's own, since the paper only says a DeepSpeed-compatible
 checkpoint is assembled; after recovery Delta_l = 0, t_l = the restored step
-and S = W.
+and S = W; with eps_w = 0 an all-zero, unchanged layer scores 0/0 = NaN,
+which never meets the threshold, so only the staleness guard persists it.
 
 Parity status: every function here is pinned by the ``-m "not gpu"`` tests
 (closed forms, exact-rational brute force, invariants, the paper's Table 1
