@@ -255,7 +255,10 @@ lc_status lc_sgd_step_score(lc_ctx *c, int64_t step, const void *const *grads, i
  * inconsistent lines, files of the wrong size and names other than a plain
  * "v*.lcr" file of the directory itself are ignored.  A store is
  * used from one thread; it owns a small pool of writer threads, and versions
- * become visible in the order they were appended. */
+ * become visible in the order they were appended.  A directory is open in at
+ * most one store at a time (an exclusive lock on its "store.lock" file, held
+ * until lc_store_close): a second lc_store_open of it, from this process or
+ * another, returns LC_ERR_BAD_STATE. */
 typedef struct lc_store lc_store;
 
 /* Opens (creating the directory itself, not its parents) the store of a

@@ -12,6 +12,7 @@
 // Versions are made durable in the order they were appended.
 #include <dirent.h>
 #include <fcntl.h>
+#include <sys/file.h>
 #include <sys/stat.h>
 #include <sys/types.h>
 #include <unistd.h>
@@ -144,6 +145,7 @@ struct lc_store {
   size_t next_final = 0;               // writing[] below this index are finalised
   bool finalising = false;             // one thread at a time makes versions durable
   int manifest_fd = -1;
+  int lock_fd = -1;                    // holds the directory's exclusive lock while open
   uint64_t seq = 0;
   uint64_t skipped = 0;                // manifest lines ignored at open
   // drain pipeline
@@ -612,15 +614,33 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
   s->slot_bytes = std::min<uint64_t>(64ull << 20, ring / (2 * kWriters));
   s->slot_bytes = (s->slot_bytes + 4095) / 4096 * 4096;
   s->n_slots = static_cast<uint32_t>(std::max<uint64_t>(2 * kWriters, ring / s->slot_bytes));
+  // One writer per directory: a lock on a file that is never replaced (the
+  // manifest itself is, by compaction), held until lc_store_close.
+  const std::string lpath = s->dir + "/store.lock";
+  s->lock_fd = open(lpath.c_str(), O_RDWR | O_CREAT, 0644);
+  if (s->lock_fd < 0) {
+    delete s;
+    return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", lpath.c_str(), std::strerror(errno));
+  }
+  if (flock(s->lock_fd, LOCK_EX | LOCK_NB) != 0) {
+    const int err = errno;
+    close(s->lock_fd);
+    delete s;
+    if (err == EWOULDBLOCK)
+      return fail(LC_ERR_BAD_STATE, "store %s is already open (another store holds its lock)", dir);
+    return fail(LC_ERR_INVALID_ARG, "cannot lock %s: %s", lpath.c_str(), std::strerror(err));
+  }
   const std::string mpath = s->dir + "/manifest.lcm";
   s->manifest_fd = open(mpath.c_str(), O_RDWR | O_CREAT, 0644);
   if (s->manifest_fd < 0) {
+    close(s->lock_fd);
     delete s;
     return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", mpath.c_str(), std::strerror(errno));
   }
   lc_status st = parse_manifest(s);
   if (st != LC_OK) {
     close(s->manifest_fd);
+    close(s->lock_fd);
     delete s;
     return st;
   }
@@ -935,6 +955,7 @@ lc_status lc_store_close(lc_store* s) {
     release_gpu(s);
   }
   if (s->manifest_fd >= 0) close(s->manifest_fd);
+  if (s->lock_fd >= 0) close(s->lock_fd);  // releases the directory
   delete s;
   return st;
 }

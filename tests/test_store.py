@@ -291,3 +291,31 @@ def test_discard_after_for_a_resumed_run(lib, tmp_path):
     for t in range(0, 8):
         assert st.plan(t).tolist() == [timeline[i]["step"] for i in O.plan_versions(timeline, orc.N, t)]
     st.close()
+
+
+def test_one_store_per_directory(lib, tmp_path):
+    """A directory is open in one store at a time: a second open, in this
+    process or another, is refused until the first store is closed; the lock
+    file survives compaction (only version files are ever removed)."""
+    import subprocess
+    import sys
+    orc, versions = oracle_history(steps=3)
+    d = str(tmp_path / "lk")
+    a = LC.Store(d, orc.R)
+    for v in versions:
+        a.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    with pytest.raises(LC.LCError) as e:
+        LC.Store(d, orc.R)
+    assert e.value.code == LC.LC_ERR_BAD_STATE
+    child = (f"import sys; sys.path.insert(0, {os.path.dirname(os.path.dirname(os.path.abspath(__file__)))!r})\n"
+             "from paper_2609_27193_amd import layercheck as LC\n"
+             f"try:\n    LC.Store({d!r}, {list(orc.R)!r})\n    print('opened')\n"
+             "except LC.LCError as e:\n    print('refused', e.code)\n")
+    r = subprocess.run([sys.executable, "-c", child], capture_output=True, text=True, timeout=120)
+    assert r.stdout.strip() == f"refused {LC.LC_ERR_BAD_STATE}", (r.stdout, r.stderr)
+    a.compact(versions[-1]["step"])
+    assert os.path.exists(os.path.join(d, "store.lock"))
+    a.close()
+    b = LC.Store(d, orc.R)
+    assert [e["step"] for e in b.entries()]
+    b.close()
