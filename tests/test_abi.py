@@ -149,6 +149,22 @@ def test_null_handling(lib):
     assert lib.lc_pack_selected(None, None, 0, 0, None) == LC.LC_ERR_INVALID_ARG
     assert lib.lc_read_state(None, None, None, None) == LC.LC_ERR_INVALID_ARG
     assert lib.lc_restore_composite(None, None, 0, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_rebase(None, 1) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_adamw_step_score(None, 1, None, LC.LC_DT_BF16, None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_sgd_step_score(None, 1, None, LC.LC_DT_BF16, None, None) == LC.LC_ERR_INVALID_ARG
+    # the store: NULL handles and arguments are refused, closing NULL is a no-op
+    assert lib.lc_store_open(None, 1, None, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_append(None, 0, None, None, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_append_async(None, 0, None, None, 0, None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_sync(None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_count(None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_entry(None, 0, None, None, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_plan(None, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_restore(None, None, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_compact(None, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_discard_after(None, 0, None) == LC.LC_ERR_INVALID_ARG
+    assert lib.lc_store_close(None) == LC.LC_OK
+    assert lib.lc_last_error()  # the last refusal's message
 
 
 def test_invalid_init_enqueues_nothing(lib):
