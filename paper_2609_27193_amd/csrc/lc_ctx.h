@@ -88,12 +88,13 @@ struct lc_ctx {
 
 
 namespace lc {
-// Restore helpers used by lc_restore_composite and the store: enqueue the
-// copies of one layer's record (device or host memory) into its arrays and
-// shadow; finish sets Delta = 0, t_l = steps and the call-order state.
-lc_status restore_layer_from_host(lc_ctx* c, uint32_t layer, const uint8_t* record);
-// The same for the bytes [rec_off, rec_off + len) of the layer's record,
-// held at `bytes` (host memory): only the parts of blocks inside the range.
+// Restore helpers used by lc_restore_composite and the store.  The first
+// enqueues the host-to-device copies of the bytes [rec_off, rec_off + len)
+// of one layer's record, held at `bytes` in host memory, into the layer's
+// arrays (only the parts of blocks inside the range, padding skipped) and
+// refreshes the shadow from the copied weights; the whole record is
+// [0, record bytes).  restore_finish sets Delta = 0, t_l = steps and the
+// call-order state.
 lc_status restore_range_from_host(lc_ctx* c, uint32_t layer, uint64_t rec_off, uint64_t len, const uint8_t* bytes);
 lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& steps);
 }  // namespace lc

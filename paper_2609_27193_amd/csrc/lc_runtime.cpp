@@ -275,23 +275,6 @@ lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode) {
 
 namespace lc {
 
-lc_status restore_layer_from_host(lc_ctx* c, uint32_t l, const uint8_t* record) {
-  const HostLayout& L = c->L;
-  const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
-  uint32_t ub = 0;
-  for (uint32_t j = 0; j < l; ++j) ub += (L.layer_seg_begin[j + 1] - L.layer_seg_begin[j]) * per_seg;
-  const uint32_t nu = (L.layer_seg_begin[l + 1] - L.layer_seg_begin[l]) * per_seg;
-  for (uint32_t k = 0; k < nu; ++k) {
-    const CopyUnit& u = L.units[ub + k];
-    LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.arr), record + u.rec_off, u.bytes, hipMemcpyHostToDevice,
-                             c->stream));
-    if (u.shadow)
-      LC_HIP(c, hipMemcpyAsync(reinterpret_cast<void*>(u.shadow), reinterpret_cast<void*>(u.arr), u.bytes,
-                               hipMemcpyDeviceToDevice, c->stream));
-  }
-  return LC_OK;
-}
-
 lc_status restore_range_from_host(lc_ctx* c, uint32_t l, uint64_t rec_off, uint64_t len, const uint8_t* bytes) {
   const HostLayout& L = c->L;
   const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
@@ -653,7 +636,7 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
   }
   // host-resident records: one copy per block, then S <- W
   for (const auto& hl : host_layers) {
-    st = restore_layer_from_host(c, hl.first, hl.second);
+    st = restore_range_from_host(c, hl.first, 0, L.rec_bytes[hl.first], hl.second);
     if (st != LC_OK) return st;
   }
   std::vector<int64_t> steps(N);
