@@ -1,6 +1,7 @@
 """The C interface on the CPU: the library loads, exports every declared
 entry point, and its host-side validation and record layout behave as
 specified (no device work is issued by these calls)."""
+import ctypes as C
 import os
 import re
 
@@ -185,3 +186,38 @@ def test_missing_library_fails_loudly(tmp_path):
     out = subprocess.run([sys.executable, "-c", code], env=env, capture_output=True, text=True, timeout=120)
     assert out.returncode == 0, out.stderr
     assert "refused:" in out.stdout and "not built" in out.stdout
+
+
+def test_struct_layouts_match_header(tmp_path):
+    """The binding's ctypes structures have the C compiler's layout of the
+    header's structures: every size and member offset, from a probe compiled
+    against include/layercheck.h."""
+    import shutil
+    import subprocess
+    gcc = shutil.which("gcc") or shutil.which("cc")
+    if gcc is None:
+        pytest.skip("no C compiler")
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    structs = {"lc_segment": LC.lc_segment, "lc_layout_desc": LC.lc_layout_desc,
+               "lc_select_stats": LC.lc_select_stats, "lc_pack_result": LC.lc_pack_result,
+               "lc_version": LC.lc_version, "lc_adamw_params": LC.lc_adamw_params,
+               "lc_sgd_params": LC.lc_sgd_params}
+    lines = ["#include <stddef.h>", "#include <stdio.h>", '#include "layercheck.h"', "int main(void) {"]
+    for name, cls in structs.items():
+        lines.append(f'  printf("{name} size %zu\\n", sizeof({name}));')
+        for field, _ in cls._fields_:
+            lines.append(f'  printf("{name} {field} %zu\\n", offsetof({name}, {field}));')
+    lines += ["  return 0;", "}"]
+    src = tmp_path / "layout.c"
+    src.write_text("\n".join(lines) + "\n")
+    exe = tmp_path / "layout"
+    subprocess.run([gcc, "-std=c11", "-I", os.path.join(root, "include"), "-o", str(exe), str(src)], check=True,
+                   capture_output=True, timeout=120)
+    got = {}
+    for line in subprocess.run([str(exe)], capture_output=True, text=True, check=True).stdout.splitlines():
+        name, key, value = line.split()
+        got[(name, key)] = int(value)
+    for name, cls in structs.items():
+        assert got[(name, "size")] == C.sizeof(cls), name
+        for field, _ in cls._fields_:
+            assert got[(name, field)] == getattr(cls, field).offset, (name, field)
