@@ -35,6 +35,10 @@ MUTANTS = {
     "accum_shadow_stale": ("        if self.mode == MODE_ACCUM:\n            # the next step's",
                            "        if False:\n            # the next step's"),
     "forced_count_wrong": ("forced[l] = 0 if by_drift else 1", "forced[l] = 1 if by_age else 0"),
+    "pack_descending_ids": ("sel = [l for l in range(self.N) if self.mask[l]]\n        if first_rank < 0",
+                            "sel = [l for l in reversed(range(self.N)) if self.mask[l]]\n        if first_rank < 0"),
+    "snapshot_pack_keeps_shadow": ("        if self.mode == MODE_SNAPSHOT:\n            for l in sel[first_rank:last]:",
+                                   "        if False:\n            for l in sel[first_rank:last]:"),
     "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
     "moments_swapped": ('["exp_avg", "exp_avg_sq"] if has_moments', '["exp_avg_sq", "exp_avg"] if has_moments'),
     "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),
