@@ -39,6 +39,10 @@ MUTANTS = {
                             "sel = [l for l in reversed(range(self.N)) if self.mask[l]]\n        if first_rank < 0"),
     "snapshot_pack_keeps_shadow": ("        if self.mode == MODE_SNAPSHOT:\n            for l in sel[first_rank:last]:",
                                    "        if False:\n            for l in sel[first_rank:last]:"),
+    "restore_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = int(v[\"step\"])",
+                            "            self.t_last[l] = int(v[\"step\"])"),
+    "restore_stamps_t_fail": ("            self.t_last[l] = int(v[\"step\"])\n            chosen[l]",
+                              "            self.t_last[l] = t_fail\n            chosen[l]"),
     "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
     "moments_swapped": ('["exp_avg", "exp_avg_sq"] if has_moments', '["exp_avg_sq", "exp_avg"] if has_moments'),
     "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),
