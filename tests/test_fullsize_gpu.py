@@ -4,6 +4,8 @@ The whole workload state lives on the GPU (8.0 - 14.8 B parameters).  The
 oracle cannot process it every step, so it checks sampled outputs one by one,
 and properties that hold at any size cover the rest:
 
+* the decision steps of the 8B, 13B, Qwen2.5-14B (no master) and 70B-shard
+  states over one staleness period, including the burst of forced layers;
 * u of sampled layers (a rotating transformer block, the final norm, and the
   embedding / lm_head on the first step and on the staleness burst) against
   the oracle's Eq. 1 on host copies, within 1e-5;
@@ -177,6 +179,7 @@ def sample_for(t, N, s_max):
 WORKLOADS = [
     ("llama3-8b", LC.LC_MODE_ACCUM, 0.0391),
     ("llama2-13b", LC.LC_MODE_ACCUM, 0.03),
+    ("qwen2.5-14b", LC.LC_MODE_ACCUM, 0.0498),  # no master; the bench's calibrated threshold (~26% of layers)
     ("llama3-70b-shard0", LC.LC_MODE_SNAPSHOT, 0.03),
 ]
 
