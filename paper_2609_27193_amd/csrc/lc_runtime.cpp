@@ -209,6 +209,16 @@ lc_status dev_alloc(lc_ctx* c, T** p, size_t count) {
   return LC_OK;
 }
 
+// Host vectors that feed asynchronous uploads must outlive the copies: a
+// function that uploads from locals holds one of these, so that an early
+// return (a failed call after some copies were enqueued) still waits for
+// the stream before the vectors go.  On the normal path the stream has
+// already been synchronised and the wait returns at once.
+struct UploadsDrained {
+  lc_ctx* c;
+  ~UploadsDrained() { (void)hipStreamSynchronize(c->stream); }
+};
+
 template <typename T>
 lc_status upload(lc_ctx* c, T* dst, const std::vector<T>& src) {
   if (src.empty()) return LC_OK;
@@ -298,6 +308,7 @@ lc_status restore_range_from_host(lc_ctx* c, uint32_t l, uint64_t rec_off, uint6
 lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& steps) {
   const uint32_t N = c->L.N;
   std::vector<double> zeros(N, 0.0);
+  UploadsDrained drained{c};
   lc_status st = upload(c, c->dt.delta, zeros);
   if (st != LC_OK) return st;
   st = upload(c, c->dt.t_last, steps);
@@ -624,6 +635,7 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
       host_layers.emplace_back(l, static_cast<const uint8_t*>(v[i].payload) + off);
     }
   }
+  UploadsDrained drained{c};  // declared after the tables it protects, so it runs first
   if (!rank_layer.empty()) {
     st = upload(c, c->dt.rank_layer, rank_layer);
     if (st != LC_OK) return st;
@@ -656,6 +668,7 @@ lc_status lc_rebase(lc_ctx* c, int64_t step) {
   const uint32_t N = c->L.N;
   std::vector<double> zeros(N, 0.0);
   std::vector<int64_t> tl(N, step);
+  UploadsDrained drained{c};
   st = upload(c, c->dt.delta, zeros);
   if (st != LC_OK) return st;
   st = upload(c, c->dt.t_last, tl);
