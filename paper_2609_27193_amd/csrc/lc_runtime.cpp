@@ -253,7 +253,10 @@ lc_status fetch_result(lc_ctx* c) {
   c->sel_rec_prefix.assign(1, 0);
   c->sel_piece_prefix.assign(1, 0);
   for (uint32_t l = 0; l < N; ++l) {
-    if (mask[l] > 1) return fail(LC_ERR_HIP, "corrupt selection mask");
+    if (mask[l] > 1) {
+      c->poisoned = true;
+      return fail(LC_ERR_HIP, "corrupt selection mask");
+    }
     if (mask[l]) {
       c->sel.push_back(l);
       c->sel_rec_prefix.push_back(c->sel_rec_prefix.back() + c->L.rec_bytes[l]);
