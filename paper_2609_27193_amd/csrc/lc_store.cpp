@@ -465,19 +465,23 @@ lc_status keep_only(lc_store* s, const std::vector<uint8_t>& keep, uint32_t* rem
   if (gone.empty()) return LC_OK;
   if (kept.size() != n) {
     const std::string mpath = s->dir + "/manifest.lcm", tpath = s->dir + "/manifest.lcm.tmp";
-    const int fd = open(tpath.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
+    // the descriptor of the new file becomes the manifest's once renamed
+    const int fd = open(tpath.c_str(), O_RDWR | O_CREAT | O_TRUNC, 0644);
     if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", tpath.c_str(), std::strerror(errno));
     std::string text;
     for (const StoredVersion& v : kept) text += manifest_line(v);
-    const bool ok = write_all(fd, reinterpret_cast<const uint8_t*>(text.data()), text.size(), 0) && fsync(fd) == 0;
-    close(fd);
-    if (!ok || rename(tpath.c_str(), mpath.c_str()) != 0 || !fsync_dir(s->dir))
-      return fail(LC_ERR_INVALID_ARG, "rewriting the manifest failed: %s", std::strerror(errno));
-    const int mfd = open(mpath.c_str(), O_RDWR);
-    if (mfd < 0) return fail(LC_ERR_INVALID_ARG, "cannot reopen %s: %s", mpath.c_str(), std::strerror(errno));
+    if (!write_all(fd, reinterpret_cast<const uint8_t*>(text.data()), text.size(), 0) || fsync(fd) != 0 ||
+        rename(tpath.c_str(), mpath.c_str()) != 0) {
+      const int err = errno;
+      close(fd);
+      (void)unlink(tpath.c_str());
+      return fail(LC_ERR_INVALID_ARG, "rewriting the manifest failed: %s", std::strerror(err));
+    }
     close(s->manifest_fd);
-    s->manifest_fd = mfd;
+    s->manifest_fd = fd;
     s->durable = kept;
+    if (!fsync_dir(s->dir))
+      return fail(LC_ERR_INVALID_ARG, "directory fsync after the manifest rewrite failed: %s", std::strerror(errno));
   }
   uint32_t removed = 0;
   for (const std::string& f : gone)
