@@ -136,7 +136,10 @@ lc_status lc_query_layout(const lc_layout_desc *d, uint64_t *numel_out,
  * layer (Section 3.2; the base full checkpoint of Section 3.4 counts as the
  * last persist).  The base selection (every layer, at t_base) is left
  * pending so the caller can pack the base version with lc_pack_selected.
- * Work runs on d->stream; returns once the device state is ready. */
+ * Every array must be device (or managed) memory holding its segment's
+ * numel elements, as far as HIP can report the allocation's extent;
+ * otherwise LC_ERR_INVALID_ARG before any work is enqueued.  Work runs on
+ * d->stream; returns once the device state is ready. */
 lc_status lc_init_layout(const lc_layout_desc *d, lc_ctx **out);
 
 /* Eq. 1-2 for every layer at decision step `step` (> every earlier step and
@@ -164,7 +167,8 @@ lc_status lc_select(lc_ctx *c, int64_t step, double lr_scale, uint8_t *mask_out,
  * order holding the raw little-endian bytes, zero-padded to a multiple of 256
  * bytes.  Records are concatenated without gaps.  SNAPSHOT mode also sets
  * S <- W for the packed layers in the same pass.  Returns LC_ERR_CAPACITY if
- * the record at first_rank alone exceeds `capacity`.  Synchronises the stream
+ * the record at first_rank alone exceeds `capacity`, LC_ERR_INVALID_ARG if
+ * `staging` is not device memory with room for the bytes to be written.  Synchronises the stream
  * only when the selection mask is not yet on the host; the copy itself is
  * asynchronous. */
 lc_status lc_pack_selected(lc_ctx *c, void *staging, uint64_t capacity, uint32_t first_rank,
@@ -176,8 +180,9 @@ lc_status lc_pack_selected(lc_ctx *c, void *staging, uint64_t capacity, uint32_t
  * next step must exceed t_fail.  A version newer than t_fail is ignored.  No
  * candidate for a layer: LC_ERR_NO_VERSION; two candidates at the same
  * greatest step: LC_ERR_INVALID_ARG.  `chosen_step_out` (host [n_layers] or
- * NULL) receives the step each layer was restored from.  Returns after the
- * restore has completed on the device. */
+ * NULL) receives the step each layer was restored from.  A device payload
+ * shorter than its payload_bytes is refused (LC_ERR_INVALID_ARG) before any
+ * work is enqueued.  Returns after the restore has completed on the device. */
 lc_status lc_restore_composite(lc_ctx *c, const lc_version *versions, uint32_t n_versions,
                                int64_t t_fail, int64_t *chosen_step_out);
 

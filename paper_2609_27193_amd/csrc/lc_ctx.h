@@ -96,5 +96,9 @@ namespace lc {
 // [0, record bytes).  restore_finish sets Delta = 0, t_l = steps and the
 // call-order state.
 lc_status restore_range_from_host(lc_ctx* c, uint32_t layer, uint64_t rec_off, uint64_t len, const uint8_t* bytes);
+// True when [p, p + bytes) is device (or managed) memory inside one
+// allocation, as far as HIP can tell: pointers a kernel or a device copy
+// could only fault on are refused before any work is enqueued.
+bool device_range_ok(const void* p, uint64_t bytes);
 lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& steps);
 }  // namespace lc

@@ -288,6 +288,24 @@ lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode) {
 
 namespace lc {
 
+bool device_range_ok(const void* p, uint64_t bytes) {
+  if (!p) return false;
+  hipPointerAttribute_t attr;
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (attr.type != hipMemoryTypeDevice && attr.type != hipMemoryTypeManaged) return false;
+  hipDeviceptr_t base = nullptr;
+  size_t size = 0;
+  if (hipMemGetAddressRange(&base, &size, const_cast<void*>(p)) != hipSuccess) {
+    (void)hipGetLastError();
+    return true;  // the extent is not known (a virtual-memory mapping, say): the type check stands
+  }
+  const uintptr_t b = reinterpret_cast<uintptr_t>(base), q = reinterpret_cast<uintptr_t>(p);
+  return q >= b && q - b <= size && bytes <= size - (q - b);
+}
+
 lc_status restore_range_from_host(lc_ctx* c, uint32_t l, uint64_t rec_off, uint64_t len, const uint8_t* bytes) {
   const HostLayout& L = c->L;
   const uint32_t per_seg = 1u + (L.has_master ? 1u : 0u) + (L.has_moments ? 2u : 0u);
@@ -352,6 +370,22 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
   if (st != LC_OK) {
     delete c;
     return st;
+  }
+  // every array a kernel will stream must be device memory of its full
+  // extent: refused here rather than faulting in a kernel
+  for (uint32_t i = 0; i < c->L.segs.size(); ++i) {
+    const lc_segment& sg = c->L.segs[i];
+    const void* arr[5] = {sg.weight, sg.shadow, sg.master, sg.exp_avg, sg.exp_avg_sq};
+    static const char* const kName[5] = {"weight", "shadow", "master", "exp_avg", "exp_avg_sq"};
+    for (int a = 0; a < 5; ++a) {
+      if (!arr[a]) continue;
+      const uint64_t bytes = sg.numel * (a < 2 ? c->L.esz : 4u);
+      if (!device_range_ok(arr[a], bytes)) {
+        delete c;
+        return fail(LC_ERR_INVALID_ARG, "segment %u: %s is not device memory holding %llu bytes", i, kName[a],
+                    static_cast<unsigned long long>(bytes));
+      }
+    }
   }
   c->mode = d->mode;
   c->s_max = d->s_max;
@@ -549,6 +583,9 @@ lc_status lc_pack_selected(lc_ctx* c, void* staging, uint64_t capacity, uint32_t
     if (!staging) return fail(LC_ERR_INVALID_ARG, "staging is NULL");
     if (reinterpret_cast<uintptr_t>(staging) % kRecordAlign)
       return fail(LC_ERR_INVALID_ARG, "staging must be %u-byte aligned", kRecordAlign);
+    if (!device_range_ok(staging, bytes))
+      return fail(LC_ERR_INVALID_ARG, "staging is not device memory holding the %llu bytes to pack",
+                  static_cast<unsigned long long>(bytes));
     const uint64_t pieces = c->sel_piece_prefix[last] - c->sel_piece_prefix[first_rank];
     LC_HIP(c, launch_pack(c->dt, first_rank, last, c->sel_piece_prefix[first_rank], pieces,
                           c->sel_rec_prefix[first_rank], staging, c->mode == LC_MODE_SNAPSHOT, c->stream));
@@ -620,6 +657,8 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
       hipPointerAttribute_t attr;
       hipError_t e = hipPointerGetAttributes(&attr, v[i].payload);
       if (e == hipSuccess && attr.type == hipMemoryTypeDevice) {
+        if (!device_range_ok(v[i].payload, v[i].payload_bytes))
+          return fail(LC_ERR_INVALID_ARG, "version %u: the device payload is shorter than payload_bytes", i);
         kind[i] = 0;
         dev_base[i] = static_cast<const uint8_t*>(v[i].payload);
       } else {

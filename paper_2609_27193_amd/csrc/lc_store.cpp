@@ -692,6 +692,8 @@ lc_status append_impl(lc_store* s, int64_t step, const uint8_t* mask, const void
     if (e == hipSuccess && attr.type == hipMemoryTypeDevice) device = true;
     else (void)hipGetLastError();
   }
+  if (device && !device_range_ok(payload, bytes))
+    return fail(LC_ERR_INVALID_ARG, "the device payload is shorter than payload_bytes");
   if (device && !caller_waits && !reuse_event)
     return fail(LC_ERR_INVALID_ARG, "a device payload needs reuse_event");
   char name[96];
