@@ -221,3 +221,14 @@ def test_struct_layouts_match_header(tmp_path):
         assert got[(name, "size")] == C.sizeof(cls), name
         for field, _ in cls._fields_:
             assert got[(name, field)] == getattr(cls, field).offset, (name, field)
+
+
+def test_init_refuses_memory_hip_does_not_know(lib):
+    """The device-range check runs before anything is allocated or enqueued:
+    arrays that are not device memory (here, addresses no GPU allocation
+    holds) are refused with LC_ERR_INVALID_ARG, so the call needs no GPU."""
+    segs = fake_segments([[4], [4]])
+    with pytest.raises(LC.LCError) as e:
+        LC.lc_init_layout(desc(segs, 2))
+    assert e.value.code == LC.LC_ERR_INVALID_ARG
+    assert "not device memory" in lib.lc_last_error().decode()
