@@ -1,5 +1,6 @@
 """GPU: draining device staging into the persistence store and composite
-recovery from it (Section 3.5), against the oracle.
+recovery from it (Section 3.5), against the oracle; the recovery runs after
+the store has been compacted to what a recovery at t_fail can use.
 
 One staging buffer is reused every step with no synchronisation between
 lc_store_append and the next lc_pack_selected: the drain's copies must be
@@ -80,6 +81,11 @@ def test_drain_and_restore_from_store(tmp_path, maker, mode, buf, overlapped):
         store.close()
         store = LC.Store(d, p.R)
         t_fail = 6
+        assert store.plan(t_fail).tolist() == [expected[i]["step"] for i in O.plan_versions(expected, p.N, t_fail)]
+        # reclaiming space keeps every record a recovery at t_fail or later can choose
+        before = len(store.entries())
+        removed = store.compact(t_fail)
+        assert removed > 0 and len(store.entries()) == before - removed
         assert store.plan(t_fail).tolist() == [expected[i]["step"] for i in O.plan_versions(expected, p.N, t_fail)]
         # fail-stop, then recover from the store
         for a in (p.dW, p.dS, p.dm, p.dv) + ((p.dM,) if p.dM is not None else ()):
