@@ -79,7 +79,8 @@ def test_fused_step_state_rules():
 
 def test_layout_without_shadow():
     """A context fed only by the fused step needs no shadow copies (16 GB less
-    on an 8B-parameter state); it refuses the standalone score."""
+    on an 8B-parameter state); it refuses the standalone score, packs and
+    restores its records like any other layout."""
     import torch
     spec = reduced_8b()
     p = Pair(spec, LC.LC_MODE_ACCUM, k0_for(spec, 0.02))
@@ -91,6 +92,11 @@ def test_layout_without_shadow():
             with pytest.raises(LC.LCError) as e:
                 LC.lc_score_layers(ctx, 1)
             assert e.value.code == LC.LC_ERR_BAD_STATE
+            # the base version (every layer, pending since init), then one fused step
+            base = torch.empty(sum(p.R), dtype=torch.uint8, device="cuda")
+            assert LC.lc_pack_selected(ctx, base.data_ptr(), base.numel(), 0)["done"] == 1
+            arrays = (p.dW, p.dM, p.dm, p.dv)
+            before = [a.clone() for a in arrays]
             g = torch.randn(spec.numel, device="cuda").to(torch.bfloat16)
             ptrs = [g[s.offset:s.offset + s.numel].data_ptr() for s in p.gen.segments]
             LC.lc_adamw_step_score(ctx, 1, ptrs, LC.LC_DT_BF16, 1e-3, 0.9, 0.95, 1e-8, 0.0, 1)
@@ -98,6 +104,18 @@ def test_layout_without_shadow():
             assert (u > 0).all()
             mask, st = LC.lc_select(ctx, 1, 1.0, p.N)
             assert st["n_selected"] == int(mask.sum())
+            assert not torch.equal(p.dm, before[2])
+            # recovery to the base: every array as it was (there is no shadow to refresh)
+            chosen = LC.lc_restore_composite(ctx, [{"step": 0, "mask": np.ones(p.N, np.uint8),
+                                                    "payload": base.data_ptr(), "payload_bytes": base.numel()}],
+                                             0, p.N)
+            torch.cuda.synchronize()
+            assert chosen.tolist() == [0] * p.N
+            for a, b in zip(arrays, before):
+                assert torch.equal(a.view(torch.uint8), b.view(torch.uint8))
+            _, d, tl = LC.lc_read_state(ctx, p.N)
+            assert not d.any() and tl.tolist() == [0] * p.N
+            LC.lc_adamw_step_score(ctx, 1, ptrs, LC.LC_DT_BF16, 1e-3, 0.9, 0.95, 1e-8, 0.0, 1)  # resumes
         finally:
             LC.lc_destroy(ctx)
         with pytest.raises(LC.LCError) as e:
