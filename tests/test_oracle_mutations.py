@@ -43,6 +43,11 @@ MUTANTS = {
                             "            self.t_last[l] = int(v[\"step\"])"),
     "restore_stamps_t_fail": ("            self.t_last[l] = int(v[\"step\"])\n            chosen[l]",
                               "            self.t_last[l] = t_fail\n            chosen[l]"),
+    "sums_not_means": ("np.float64(A / n) / np.float64(B / n + eps_w)", "np.float64(A) / np.float64(B + eps_w)"),
+    "master_after_moments": ('return (["weight"] + (["master"] if has_master else [])\n            + (["exp_avg", "exp_avg_sq"] if has_moments else []))',
+                             'return (["weight"] + (["exp_avg", "exp_avg_sq"] if has_moments else [])\n            + (["master"] if has_master else []))'),
+    "snapshot_score_refreshes_shadow": ("        if self.mode == MODE_ACCUM:\n            # the next step's W(t-1)",
+                                        "        if True:\n            # the next step's W(t-1)"),
     "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
     "moments_swapped": ('["exp_avg", "exp_avg_sq"] if has_moments', '["exp_avg_sq", "exp_avg"] if has_moments'),
     "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),
