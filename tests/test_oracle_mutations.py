@@ -48,6 +48,9 @@ MUTANTS = {
                              'return (["weight"] + (["exp_avg", "exp_avg_sq"] if has_moments else [])\n            + (["master"] if has_master else []))'),
     "snapshot_score_refreshes_shadow": ("        if self.mode == MODE_ACCUM:\n            # the next step's W(t-1)",
                                         "        if True:\n            # the next step's W(t-1)"),
+    "adamw_betas_swapped": ('m_new = (sc["b1"] * m).astype(f) + (sc["omb1"] * g).astype(f)',
+                            'm_new = (sc["b2"] * m).astype(f) + (sc["omb2"] * g).astype(f)'),
+    "adamw_v_linear_in_g": ('(sc["omb2"] * (g * g).astype(f)).astype(f)', '(sc["omb2"] * np.abs(g)).astype(f)'),
     "no_padding": ("out += bytes(padded(len(raw)) - len(raw))", "pass"),
     "moments_swapped": ('["exp_avg", "exp_avg_sq"] if has_moments', '["exp_avg_sq", "exp_avg"] if has_moments'),
     "restore_oldest": ('if best is None or v["step"] > best_step:', 'if best is None or v["step"] < best_step:'),
