@@ -81,6 +81,7 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
     if (static_cast<int64_t>(s.layer) != prev) L.layer_seg_begin[s.layer] = i;
     prev = s.layer;
     L.numel[s.layer] += s.numel;
+    if (L.numel[s.layer] > (1ull << 52)) return fail(LC_ERR_INVALID_ARG, "layer %u: too many elements", s.layer);
   }
   if (prev != static_cast<int64_t>(N) - 1)
     return fail(LC_ERR_INVALID_ARG, "layer %lld has no segment", static_cast<long long>(prev + 1));
@@ -111,7 +112,10 @@ lc_status build_layout(const lc_layout_desc* d, HostLayout& L) {
   }
   L.layer_seg_begin[N] = d->n_segments;
   L.total_numel = 0;
-  for (uint32_t l = 0; l < N; ++l) L.total_numel += L.numel[l];
+  for (uint32_t l = 0; l < N; ++l) {
+    L.total_numel += L.numel[l];
+    if (L.total_numel > (1ull << 56)) return fail(LC_ERR_INVALID_ARG, "too many elements in all");
+  }
   // the staleness numerator sum_l n_l * age_l (age <= S_max - 1) must fit in 64 bits
   if (L.total_numel > static_cast<uint64_t>(std::numeric_limits<int64_t>::max()) / static_cast<uint64_t>(d->s_max))
     return fail(LC_ERR_INVALID_ARG, "total elements times s_max overflows 63 bits");

@@ -136,6 +136,13 @@ def test_validation_errors(lib):
     q(segs=tight)
     big = fake_segments([[1 << 40]])
     _expect(I, lambda: q(segs=big, n=1, k0=[1e-3], s_max=1 << 30))  # staleness numerator overflow
+    # element counts are bounded before any byte count is formed from them
+    huge = fake_segments([[1 << 46] * 65])
+    _expect(I, lambda: q(segs=huge, n=1, k0=[1e-3]))
+    assert "too many elements" in lib.lc_last_error().decode()
+    huge = fake_segments([[1 << 46] * 64] * 17)
+    _expect(I, lambda: q(segs=huge, n=17, k0=[1e-3] * 17))
+    assert "too many elements" in lib.lc_last_error().decode()
     with pytest.raises(ValueError):
         desc(good, 2, k0=[1e-3])
 
