@@ -1,7 +1,8 @@
 """GPU: independent contexts.  Two contexts over different layouts, each on
 its own HIP stream and driven from its own host thread at the same time,
-must each agree with their oracle at every step (the library keeps no
-shared mutable state beyond the per-thread error message)."""
+must each agree with their oracle at every step and in a composite restore
+(the library keeps no shared mutable state beyond the per-thread error
+message)."""
 import threading
 
 import numpy as np
@@ -10,7 +11,7 @@ import pytest
 from paper_2609_27193_amd import layercheck as LC
 from tests.conftest import gpu_available
 from tests.gpu_harness import Pair, log
-from tests.test_parity_gpu import k0_for, reduced_8b, reduced_qwen
+from tests.test_parity_gpu import _restore_and_compare, k0_for, reduced_8b, reduced_qwen
 
 pytestmark = pytest.mark.gpu
 
@@ -38,6 +39,8 @@ def test_two_contexts_two_streams_two_threads():
                     p.pack(0, np.ones(p.N, np.uint8))
                     for t in range(1, 9):
                         p.step(t, lr_scale=1.0 if t < 5 else 0.5)
+                    chosen = _restore_and_compare(p, 7, "device")
+                    log(f"  [{spec.name}] restored from steps {sorted(set(chosen.tolist()))}")
                     # an error on this thread leaves its message here, not on the other thread
                     with pytest.raises(LC.LCError):
                         LC.lc_select(p.ctx, 99, 1.0, p.N)
