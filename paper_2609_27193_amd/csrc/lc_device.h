@@ -129,7 +129,8 @@ __device__ __forceinline__ void block_sum2(double& a, double& b) {
 }
 
 // Blocks per launch: one per work item up to the dispatch limit of 2^32
-// work-items per dimension; beyond it the kernels loop.
+// work-items per dimension.  Beyond it the score and copy kernels are launched
+// again over the next range of items; the optimizer kernels loop.
 __host__ inline uint32_t grid_for(uint64_t items, uint32_t threads) {
   uint64_t cap = (0xFFFFFFFFull / threads) & ~7ull;
   if (LC_MAX_GRID_BLOCKS > 0 && cap > LC_MAX_GRID_BLOCKS) cap = LC_MAX_GRID_BLOCKS;

@@ -133,22 +133,13 @@ __device__ __forceinline__ void score_chunk(const DeviceTables& t, uint32_t c) {
   if (tid == 0) t.partials[c] = make_double2(a, b);
 }
 
-// LOOP = false: one chunk per block (the common case; the chunk's tables are
-// read before any store, so they stay on the scalar path).  LOOP = true: the
-// grid is capped by the dispatch limit and blocks take several rounds.
-template <int DT, bool ACCUM, bool LOOP>
-__global__ __launch_bounds__(kScoreThreads) void score_kernel(const DeviceTables t) {
-  if constexpr (!LOOP) {
-    score_chunk<DT, ACCUM>(t, remap_xcd(blockIdx.x, gridDim.x));
-  } else {
-    for (uint64_t base = 0; base < t.n_chunks; base += gridDim.x) {
-      const uint64_t left = t.n_chunks - base;
-      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
-      if (blockIdx.x >= span) return;
-      score_chunk<DT, ACCUM>(t, static_cast<uint32_t>(base + remap_xcd(blockIdx.x, span)));
-      __syncthreads();  // the block reduction's LDS is reused by the next round
-    }
-  }
+// One chunk per block: the chunk's tables are read before any store, so they
+// stay on the scalar path.  A layout with more chunks than one dispatch takes
+// (2^32 work-items) is scored by consecutive launches, each over the next
+// range of chunks starting at chunk_base.
+template <int DT, bool ACCUM>
+__global__ __launch_bounds__(kScoreThreads) void score_kernel(const DeviceTables t, uint32_t chunk_base) {
+  score_chunk<DT, ACCUM>(t, chunk_base + remap_xcd(blockIdx.x, gridDim.x));
 }
 
 // ---- finalize: Eq. 1 and Eq. 2 per layer, one block per layer -----------------
@@ -324,21 +315,13 @@ __device__ __forceinline__ void pack_piece(const DeviceTables& t, uint32_t first
   }
 }
 
-template <bool REFRESH, bool LOOP>
+// One piece per block; piece_base is the first piece of this launch (a pack
+// with more pieces than one dispatch takes is split into consecutive launches).
+template <bool REFRESH>
 __global__ __launch_bounds__(kCopyThreads) void pack_kernel(const DeviceTables t, uint32_t first,
                                                             uint32_t last, uint64_t piece_base,
-                                                            uint64_t n_pieces, uint64_t rec_base,
-                                                            uint8_t* staging) {
-  if constexpr (!LOOP) {
-    pack_piece<REFRESH>(t, first, last, piece_base + remap_xcd(blockIdx.x, gridDim.x), rec_base, staging);
-  } else {
-    for (uint64_t base = 0; base < n_pieces; base += gridDim.x) {
-      const uint64_t left = n_pieces - base;
-      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
-      if (blockIdx.x >= span) return;
-      pack_piece<REFRESH>(t, first, last, piece_base + base + remap_xcd(blockIdx.x, span), rec_base, staging);
-    }
-  }
+                                                            uint64_t rec_base, uint8_t* staging) {
+  pack_piece<REFRESH>(t, first, last, piece_base + remap_xcd(blockIdx.x, gridDim.x), rec_base, staging);
 }
 
 // ---- unpack: composite restore from device-resident records --------------------
@@ -363,40 +346,33 @@ __device__ __forceinline__ void unpack_piece(const DeviceTables& t, uint32_t n_r
   copy_piece(src, dst, dst2, len, u.vec_ok != 0 && (rec & 15) == 0);
 }
 
-template <bool LOOP>
+// One piece per block, from piece_base on (split like the pack).
 __global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables t, uint32_t n_ranks,
-                                                              uint64_t n_pieces) {
-  if constexpr (!LOOP) {
-    unpack_piece(t, n_ranks, remap_xcd(blockIdx.x, gridDim.x));
-  } else {
-    for (uint64_t base = 0; base < n_pieces; base += gridDim.x) {
-      const uint64_t left = n_pieces - base;
-      const uint32_t span = left < gridDim.x ? static_cast<uint32_t>(left) : gridDim.x;
-      if (blockIdx.x >= span) return;
-      unpack_piece(t, n_ranks, base + remap_xcd(blockIdx.x, span));
-    }
-  }
+                                                              uint64_t piece_base) {
+  unpack_piece(t, n_ranks, piece_base + remap_xcd(blockIdx.x, gridDim.x));
 }
 
+// Each launch takes the largest grid one dispatch allows (grid_for) and the
+// next range of work items; every block does exactly one item.
 template <int DT, bool ACCUM>
 void launch_score_t(const DeviceTables& t, hipStream_t st) {
-  const uint32_t g = grid_for(t.n_chunks, kScoreThreads);
-  if (g == t.n_chunks)
-    hipLaunchKernelGGL((score_kernel<DT, ACCUM, false>), dim3(g), dim3(kScoreThreads), 0, st, t);
-  else
-    hipLaunchKernelGGL((score_kernel<DT, ACCUM, true>), dim3(g), dim3(kScoreThreads), 0, st, t);
+  for (uint64_t done = 0; done < t.n_chunks;) {
+    const uint32_t g = grid_for(t.n_chunks - done, kScoreThreads);
+    hipLaunchKernelGGL((score_kernel<DT, ACCUM>), dim3(g), dim3(kScoreThreads), 0, st, t,
+                       static_cast<uint32_t>(done));
+    done += g;
+  }
 }
 
 template <bool REFRESH>
 void launch_pack_t(const DeviceTables& t, uint32_t first, uint32_t last, uint64_t piece_base, uint64_t n_pieces,
                    uint64_t rec_base, uint8_t* stg, hipStream_t st) {
-  const uint32_t g = grid_for(n_pieces, kCopyThreads);
-  if (g == n_pieces)
-    hipLaunchKernelGGL((pack_kernel<REFRESH, false>), dim3(g), dim3(kCopyThreads), 0, st, t, first, last,
-                       piece_base, n_pieces, rec_base, stg);
-  else
-    hipLaunchKernelGGL((pack_kernel<REFRESH, true>), dim3(g), dim3(kCopyThreads), 0, st, t, first, last,
-                       piece_base, n_pieces, rec_base, stg);
+  for (uint64_t done = 0; done < n_pieces;) {
+    const uint32_t g = grid_for(n_pieces - done, kCopyThreads);
+    hipLaunchKernelGGL((pack_kernel<REFRESH>), dim3(g), dim3(kCopyThreads), 0, st, t, first, last,
+                       piece_base + done, rec_base, stg);
+    done += g;
+  }
 }
 
 }  // namespace
@@ -434,11 +410,11 @@ hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last
 }
 
 hipError_t launch_unpack(const DeviceTables& t, uint32_t n_ranks, uint64_t n_pieces, hipStream_t st) {
-  const uint32_t g = grid_for(n_pieces, kCopyThreads);
-  if (g == n_pieces)
-    hipLaunchKernelGGL(unpack_kernel<false>, dim3(g), dim3(kCopyThreads), 0, st, t, n_ranks, n_pieces);
-  else
-    hipLaunchKernelGGL(unpack_kernel<true>, dim3(g), dim3(kCopyThreads), 0, st, t, n_ranks, n_pieces);
+  for (uint64_t done = 0; done < n_pieces;) {
+    const uint32_t g = grid_for(n_pieces - done, kCopyThreads);
+    hipLaunchKernelGGL(unpack_kernel, dim3(g), dim3(kCopyThreads), 0, st, t, n_ranks, done);
+    done += g;
+  }
   return hipGetLastError();
 }
 
