@@ -29,8 +29,9 @@ def hipcc() -> str:
 
 
 SANITIZED_LIB = os.path.join(HERE, "liblayercheck_hostsan.so")
-# Test build: every grid capped at 40 blocks, so each kernel runs the looped
-# form it uses beyond the 2^32 work-item dispatch limit.
+# Test build: every grid capped at 40 blocks, so each kernel runs the form it
+# takes beyond the 2^32 work-item dispatch limit (consecutive launches for the
+# score and copy kernels, an in-kernel loop for the optimizer kernels).
 GRID_CAPPED_LIB = os.path.join(HERE, "liblayercheck_gridcap.so")
 GRID_CAP_DEFINES = ("LC_MAX_GRID_BLOCKS=40",)
 # AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (the

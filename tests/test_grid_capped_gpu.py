@@ -1,9 +1,11 @@
-"""GPU: the looped form of every kernel.  Kernels take one work item per
-block up to the 2^32 work-item dispatch limit and loop beyond it; no layout
-that fits one GPU's memory reaches the limit in the single-shot tests, so a
-build with every grid capped at 40 blocks (`__graft_entry__.build()` makes
-it) runs the parity, edge and optimizer tests again in a child process, each
-kernel then looping over many rounds."""
+"""GPU: work beyond one dispatch's grid.  Kernels take one work item per
+block up to the 2^32 work-item dispatch limit; beyond it the score and copy
+kernels are launched again over the next range of items and the optimizer
+kernels loop.  The parity tests rarely reach the limit, so a build with
+every grid capped at 40 blocks (`__graft_entry__.build()` makes it) runs the
+parity, edge and optimizer tests again in a child process: the score and
+copy kernels then run as many consecutive launches, the optimizer kernels
+over many rounds."""
 import os
 import subprocess
 import sys
@@ -17,7 +19,7 @@ pytestmark = pytest.mark.gpu
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
-def test_parity_with_looped_kernels():
+def test_parity_with_capped_grids():
     if not gpu_available():
         pytest.skip("needs an MI355X")
     assert os.path.exists(GRID_CAPPED_LIB), "the grid-capped build is made by __graft_entry__.build()"
