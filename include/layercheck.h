@@ -124,6 +124,21 @@ typedef struct {
   uint64_t payload_bytes; /* must equal the sum of their record sizes         */
 } lc_version;
 
+/* Tiles this build of the library works in (no GPU work).  A score chunk is
+ * the run of one segment's weights that one score-kernel block reduces to one
+ * fp64 pair (the fused optimizer steps use the same chunks); a piece is the
+ * part of one record block that one pack or unpack block moves; every record
+ * block starts record_align bytes aligned and is zero-padded to a multiple of
+ * it. */
+typedef struct {
+  uint32_t chunk_bytes;  /* bytes of weights per score chunk                  */
+  uint32_t piece_bytes;  /* bytes per pack / unpack piece                     */
+  uint32_t record_align; /* block alignment and padding inside a record (256) */
+  uint32_t reserved;
+} lc_build_info;
+
+lc_status lc_query_build(lc_build_info *out);
+
 /* Layout query without any GPU work: validates `d` as lc_init_layout does and
  * reports per-layer element counts and record sizes (host arrays of n_layers
  * entries, either may be NULL). */
@@ -146,13 +161,23 @@ lc_status lc_init_layout(const lc_layout_desc *d, lc_ctx **out);
  * > t_base):  u_l = mean|W_l - S_l| / (mean|S_l| + eps_w), means taken jointly
  * over all elements of all segments of layer l, accumulated in fp64.
  * ACCUM: Delta_l += u_l and S <- W for all layers in the same pass.
- * SNAPSHOT: Delta_l = u_l; requires the previous selection fully packed.
- * In ACCUM mode an unpacked selection is discarded.  Asynchronous. */
+ * SNAPSHOT: Delta_l = u_l.
+ * A selection made by lc_select or lc_rebase has already reset Delta_l and
+ * t_l of its layers (Eq. 4), so until every one of its records has been
+ * packed this call returns LC_ERR_BAD_STATE with the state unchanged (a
+ * dropped selection would let recovery fall back to older records and break
+ * the staleness bound of Section 3.3).  The base that lc_init_layout leaves
+ * pending resets nothing: in ACCUM mode a warm-up may leave it unpacked
+ * (this call then drops it); SNAPSHOT mode needs it packed first.
+ * Synchronises the stream only when it must read back whether the previous
+ * selection is packed (a selection whose mask never reached the host);
+ * otherwise asynchronous. */
 lc_status lc_score_layers(lc_ctx *c, int64_t step);
 
 /* Eq. 3-5 for every layer: K_l = K0_l * lr_scale (lr_scale = s(lr(t)) > 0,
  * finite); select l when Delta_l >= K_l or step - t_l >= S_max; a selected
- * layer gets Delta_l = 0 and t_l = step (Eq. 4).  Must follow
+ * layer gets Delta_l = 0 and t_l = step (Eq. 4), so its record must be packed
+ * (lc_pack_selected) before the next score or optimizer step.  Must follow
  * lc_score_layers(step).  Writes the 0/1 mask (host [n_layers]) and stats
  * when the pointers are non-NULL, which synchronises the stream; with both
  * NULL the call is asynchronous. */
@@ -203,7 +228,8 @@ typedef struct {
  * the fallback for rarely updated layers).  Every layer counts as persisted
  * at `step`: Delta_l = 0, t_l = step, S <- W when the layout has a shadow.
  * Every layer is selected, as after lc_select, for lc_pack_selected to pack
- * (any selection still pending is dropped).  `step` must not precede the
+ * (any selection still pending is replaced: the base holds every layer), and
+ * the next score or optimizer step waits for that pack as after lc_select.  `step` must not precede the
  * last scored, optimizer or restore step; it may equal it (the warm-up's last
  * optimizer step, then its base).  Warm-up steps before it call
  * lc_adamw_step_score (or nothing) and skip lc_select.  Synchronises the
@@ -226,7 +252,9 @@ lc_status lc_rebase(lc_ctx *c, int64_t step);
  *               NULL for all segments (the paper's with/without weight-decay
  *               parameter groups)
  * Requires LC_MODE_ACCUM and `step` greater than every earlier step; follows
- * the same call sequence as lc_score_layers (select and pack next).  The
+ * the same call sequence as lc_score_layers (select and pack next) and, like
+ * it, returns LC_ERR_BAD_STATE while a selection made by lc_select or
+ * lc_rebase is not fully packed.  The
  * shadow is left as it was, so lc_score_layers is refused afterwards until a
  * restore or lc_rebase re-synchronises it.  Asynchronous. */
 lc_status lc_adamw_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,

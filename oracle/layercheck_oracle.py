@@ -40,9 +40,18 @@ checkpoint is assembled; after recovery Delta_l = 0, t_l = the restored step
 and S = W; with eps_w = 0 an all-zero, unchanged layer scores 0/0 = NaN,
 which never meets the threshold, so only the staleness guard persists it.
 
+A selection made by ``select`` or ``rebase`` has reset Delta_l and t_l of its
+layers (Eq. 4), so it must be packed in full before the next score or
+optimizer step (otherwise recovery would silently take older records and the
+Section 3.3 bound would fail); the base selected at construction resets
+nothing and may stay unpacked in ACCUM mode (a warm-up), while SNAPSHOT mode
+needs it packed.
+
 Parity status: every function here is pinned by the ``-m "not gpu"`` tests
 (closed forms, exact-rational brute force, invariants, the paper's Table 1
-record-size and layer-count figures); no function is "parity unpinned".
+record-size and layer-count figures; ``bf16_round`` against hand-worked bit
+patterns and torch's independent conversion; ``resync`` against taking the
+same decision directly); no function is "parity unpinned".
 """
 from __future__ import annotations
 
@@ -287,6 +296,20 @@ class LayerCheckOracle:
         self.mask = np.ones(n_layers, dtype=np.uint8)
         self.mask_step = self.t_base
         self.unpacked = set(range(n_layers))
+        # The base selected at init resets nothing (Delta is 0 and t_l = t_base
+        # already), so a warm-up may leave it unpacked in ACCUM mode; a
+        # selection made by ``select`` or ``rebase`` has reset its layers.
+        self.pending_persists = False
+
+    def _require_packed(self) -> None:
+        """Eq. 4 resets Delta_l and t_l of a selected layer as if it were
+        already persisted, so the layers of a selection made by ``select`` or
+        ``rebase`` must all be packed before the state moves on (otherwise a
+        recovery would silently fall back to an older record and the Section
+        3.3 bound would not hold).  SNAPSHOT mode also needs the base packed:
+        its pack is what refreshes the shadow."""
+        if self.unpacked and (self.pending_persists or self.mode == MODE_SNAPSHOT):
+            raise OracleError(LC_ERR_BAD_STATE, "previous selection not fully packed")
 
     # -- Section 3.4: AdamW step with the drift taken from the update --------
     def _optimizer_step(self, step: int, grads, decayed, update) -> None:
@@ -300,6 +323,7 @@ class LayerCheckOracle:
             raise OracleError(LC_ERR_BAD_STATE, "decision steps must strictly increase")
         if self.mode != MODE_ACCUM:
             raise OracleError(LC_ERR_BAD_STATE, "the fused optimizer step accumulates (ACCUM mode)")
+        self._require_packed()
         segs = [s for g in self.by_layer for s in g]
         for i, (s, g) in enumerate(zip(segs, grads)):
             if s.master is not None:
@@ -353,8 +377,7 @@ class LayerCheckOracle:
     def score(self, step: int) -> None:
         if step <= self.last_step:
             raise OracleError(LC_ERR_BAD_STATE, "decision steps must strictly increase")
-        if self.mode == MODE_SNAPSHOT and self.unpacked:
-            raise OracleError(LC_ERR_BAD_STATE, "previous selection not fully packed")
+        self._require_packed()
         for l, g in enumerate(self.by_layer):
             _, _, _, u = layer_update_score([s.weight for s in g], [s.shadow for s in g],
                                             self.dtype, self.eps_w)
@@ -391,6 +414,7 @@ class LayerCheckOracle:
         self.mask = mask
         self.mask_step = step
         self.unpacked = {l for l in range(self.N) if mask[l]}
+        self.pending_persists = True
         return mask.copy(), self.stats(step, mask, n_forced)
 
     # -- Section 3.4 warm-up and base checkpoint ------------------------------
@@ -414,6 +438,7 @@ class LayerCheckOracle:
         self.mask = np.ones(self.N, dtype=np.uint8)
         self.mask_step = step
         self.unpacked = set(range(self.N))
+        self.pending_persists = True
 
     def stats(self, step: int, mask: np.ndarray, n_forced: int) -> dict:
         ages = [step - self.t_last[l] for l in range(self.N)]

@@ -79,6 +79,8 @@ struct lc_ctx {
   int64_t scored_step = 0;
   bool have_selection = false; // a selection (or the base) exists to pack
   bool pending = false;        // a selection whose records are not all packed
+  bool pending_persists = false; // it came from lc_select or lc_rebase, which reset
+                                 // Delta and t_l of its layers: it must be packed
   bool result_on_host = false; // h_result reflects the pending selection
   std::vector<uint32_t> sel;            // selected layers, ascending
   std::vector<uint64_t> sel_rec_prefix, sel_piece_prefix;

@@ -278,13 +278,33 @@ lc_status fetch_result(lc_ctx* c) {
   return LC_OK;
 }
 
-lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode) {
+lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode, bool persists) {
   LC_HIP(c, launch_select(c->dt, step, lr, base_mode, c->stream));
   LC_HIP(c, hipMemcpyAsync(c->h_result, c->dt.result, sizeof(SelectHeader) + c->L.N,
                            hipMemcpyDeviceToHost, c->stream));
   c->have_selection = true;
   c->pending = true;
+  c->pending_persists = persists;
   c->result_on_host = false;
+  return LC_OK;
+}
+
+// Eq. 4 resets Delta_l and t_l of every selected layer as if it were already
+// persisted.  A selection made by lc_select or lc_rebase therefore has to be
+// packed in full before the state moves on: were it dropped, a recovery would
+// fall back to an older record of those layers without any error and the
+// staleness bound of Section 3.3 would no longer hold.  The base selected by
+// lc_init_layout resets nothing, so in ACCUM mode a warm-up may leave it
+// unpacked; SNAPSHOT mode needs it packed, since its pack refreshes the shadow.
+lc_status require_packed(lc_ctx* c) {
+  if (!c->pending || !(c->pending_persists || c->mode == LC_MODE_SNAPSHOT)) return LC_OK;
+  if (!c->result_on_host) {
+    lc_status st = fetch_result(c);
+    if (st != LC_OK) return st;
+  }
+  if (c->pending)
+    return fail(LC_ERR_BAD_STATE, "the previous selection is not fully packed (%u of its layers are not)",
+                c->n_unpacked);
   return LC_OK;
 }
 
@@ -343,6 +363,7 @@ lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& 
   c->scored = false;
   c->have_selection = false;
   c->pending = false;
+  c->pending_persists = false;
   c->shadow_valid = c->L.has_shadow;
   c->result_on_host = false;
   return LC_OK;
@@ -353,6 +374,15 @@ lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& 
 extern "C" {
 
 const char* lc_last_error(void) { return g_error.c_str(); }
+
+lc_status lc_query_build(lc_build_info* out) {
+  if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
+  out->chunk_bytes = kChunkBytes;
+  out->piece_bytes = kPieceBytes;
+  out->record_align = kRecordAlign;
+  out->reserved = 0;
+  return LC_OK;
+}
 
 lc_status lc_query_layout(const lc_layout_desc* d, uint64_t* numel_out, uint64_t* record_bytes_out) {
   HostLayout L;
@@ -500,7 +530,7 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
     if (e != hipSuccess) return bail(fail(LC_ERR_HIP, "shadow init copy failed: %s", hipGetErrorString(e)));
   }
   // base selection: every layer, at t_base
-  LC_TRY(enqueue_select(c, d->t_base, 1.0, 1));
+  LC_TRY(enqueue_select(c, d->t_base, 1.0, 1, false));
   {
     hipError_t e = hipStreamSynchronize(c->stream);
     if (e != hipSuccess) return bail(fail(LC_ERR_HIP, "init failed: %s", hipGetErrorString(e)));
@@ -521,14 +551,8 @@ lc_status lc_score_layers(lc_ctx* c, int64_t step) {
                                       ? "the shadow is stale after a fused optimizer step; a restore or "
                                         "lc_rebase re-synchronises it"
                                       : "the layout has no shadow copies; use a fused optimizer step");
-  if (c->mode == LC_MODE_SNAPSHOT && c->pending) {
-    if (!c->result_on_host) {
-      st = fetch_result(c);
-      if (st != LC_OK) return st;
-    }
-    if (c->pending)
-      return fail(LC_ERR_BAD_STATE, "SNAPSHOT mode: the previous selection is not fully packed");
-  }
+  st = require_packed(c);
+  if (st != LC_OK) return st;
   LC_HIP(c, launch_score(c->dt, c->stream));
   c->last_step = step;
   c->scored = true;
@@ -547,7 +571,7 @@ lc_status lc_select(lc_ctx* c, int64_t step, double lr_scale, uint8_t* mask_out,
                 static_cast<long long>(step));
   if (!(lr_scale > 0.0) || !std::isfinite(lr_scale))
     return fail(LC_ERR_INVALID_ARG, "lr_scale must be positive and finite");
-  st = enqueue_select(c, step, lr_scale, 0);
+  st = enqueue_select(c, step, lr_scale, 0, true);
   if (st != LC_OK) return st;
   c->scored = false;
   if (mask_out || stats_out) {
@@ -724,7 +748,7 @@ lc_status lc_rebase(lc_ctx* c, int64_t step) {
     LC_HIP(c, hipMemcpyAsync(sg.shadow, sg.weight, sg.numel * c->L.esz, hipMemcpyDeviceToDevice, c->stream));
   }
   c->shadow_valid = c->L.has_shadow;
-  st = enqueue_select(c, step, 1.0, 1);
+  st = enqueue_select(c, step, 1.0, 1, true);
   if (st != LC_OK) return st;
   // the uploads read host vectors that end with this call
   LC_HIP(c, hipStreamSynchronize(c->stream));
@@ -749,6 +773,8 @@ lc_status optimizer_begin(lc_ctx* c, int64_t step, const void* const* grads, int
   if (step <= c->last_step)
     return fail(LC_ERR_BAD_STATE, "step %lld must exceed the previous step %lld", static_cast<long long>(step),
                 static_cast<long long>(c->last_step));
+  lc_status st = require_packed(c);
+  if (st != LC_OK) return st;
   const size_t ns = c->L.opt_segs.size();
   const uint32_t gsz = grad_dtype == LC_DT_BF16 ? 2 : 4;
   for (size_t i = 0; i < ns; ++i) {

@@ -23,7 +23,7 @@ LC_OK, LC_ERR_INVALID_ARG, LC_ERR_BAD_STATE, LC_ERR_CAPACITY, LC_ERR_NO_VERSION,
 LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 
-EXPORTED = ("lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
+EXPORTED = ("lc_query_build", "lc_query_layout", "lc_init_layout", "lc_score_layers", "lc_select", "lc_pack_selected",
             "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_sgd_step_score", "lc_store_open",
             "lc_store_append", "lc_store_append_async", "lc_store_sync", "lc_store_count", "lc_store_entry",
             "lc_store_plan", "lc_store_restore", "lc_store_compact", "lc_store_discard_after", "lc_store_close",
@@ -34,6 +34,11 @@ class lc_segment(C.Structure):
     _fields_ = [("layer", C.c_uint32), ("reserved", C.c_uint32), ("numel", C.c_uint64),
                 ("weight", C.c_void_p), ("shadow", C.c_void_p), ("master", C.c_void_p),
                 ("exp_avg", C.c_void_p), ("exp_avg_sq", C.c_void_p)]
+
+
+class lc_build_info(C.Structure):
+    _fields_ = [("chunk_bytes", C.c_uint32), ("piece_bytes", C.c_uint32), ("record_align", C.c_uint32),
+                ("reserved", C.c_uint32)]
 
 
 class lc_layout_desc(C.Structure):
@@ -86,6 +91,7 @@ def load_library(path: str = LIB_PATH):
         lib = C.CDLL(path)
         P = C.POINTER
         sig = {
+            "lc_query_build": (C.c_int, [P(lc_build_info)]),
             "lc_query_layout": (C.c_int, [P(lc_layout_desc), P(C.c_uint64), P(C.c_uint64)]),
             "lc_init_layout": (C.c_int, [P(lc_layout_desc), P(C.c_void_p)]),
             "lc_score_layers": (C.c_int, [C.c_void_p, C.c_int64]),
@@ -156,6 +162,12 @@ class LayoutDesc:
         self.n_layers = n_layers
         self.desc = lc_layout_desc(n_layers, len(segments), self._segs, weight_dtype, int(has_master),
                                    mode, 0, self._k0, s_max, eps_w, t_base, stream or None)
+
+
+def lc_query_build() -> dict:
+    info = lc_build_info()
+    _check(load_library().lc_query_build(C.byref(info)), "lc_query_build")
+    return {"chunk_bytes": info.chunk_bytes, "piece_bytes": info.piece_bytes, "record_align": info.record_align}
 
 
 def lc_query_layout(layout: LayoutDesc):

@@ -463,3 +463,194 @@ def check_accum_equals_snapshot_first_step(cls):
         g = [s for s in lb.segs if s.layer == l]
         a_snap = O.layer_update_score([s.weight for s in g], [s.shadow for s in g], O.DT_BF16, 0.0)[0]
         assert 0 < a_snap <= acc[l] * (1 + 1e-12)
+
+
+# ------------------------------------------------------ bf16 weight copy ----
+# Section 4.1: every checkpoint stores a bf16 copy of the weights, and the
+# fused optimizer step (Section 3.4) writes those weights back from its fp32
+# parameters.  Converting fp32 to bf16 keeps the sign, the 8 exponent bits
+# and the top 7 fraction bits; the 16 dropped bits decide the rounding, to
+# the nearest representable value and, on an exact tie (dropped bits
+# 0x8000), to the neighbour whose last kept bit is 0.  Each case below is
+# worked out by hand from that rule: (fp32 bits, bf16 bits).
+BF16_CASES = [
+    (0x3F800000, 0x3F80),  # 1.0 is exact
+    (0x3F808000, 0x3F80),  # tie between 0x3F80 (even) and 0x3F81
+    (0x3F818000, 0x3F82),  # tie between 0x3F81 and 0x3F82 (even)
+    (0xBF808000, 0xBF80),  # the same ties, negated
+    (0xBF818000, 0xBF82),
+    (0x3F808001, 0x3F81),  # just above a tie rounds up
+    (0x3F807FFF, 0x3F80),  # just below a tie rounds down
+    (0x3F81FFFF, 0x3F82),  # carry into the kept bits
+    (0x3FFF8000, 0x4000),  # tie to even carries into the exponent
+    (0x7F7F7FFF, 0x7F7F),  # large finite, rounds down
+    (0x7F7FFFFF, 0x7F80),  # FLT_MAX rounds up to +inf
+    (0x7F7F8000, 0x7F80),  # tie between 0x7F7F and +inf (even)
+    (0xFF7FFFFF, 0xFF80),  # -FLT_MAX rounds to -inf
+    (0x00000000, 0x0000),  # +0
+    (0x80000000, 0x8000),  # -0 keeps its sign
+    (0x7F800000, 0x7F80),  # +inf
+    (0xFF800000, 0xFF80),  # -inf
+    (0x00000001, 0x0000),  # smallest subnormal rounds to +0
+    (0x00008000, 0x0000),  # subnormal tie to even (0)
+    (0x00018000, 0x0002),  # subnormal tie to even (2)
+    (0x80018000, 0x8002),
+    (0x007FFFFF, 0x0080),  # largest subnormal rounds up to the smallest normal
+    (0x00400000, 0x0040),  # a subnormal that is exact in bf16
+    (0x7FC00000, 0x7FC0),  # NaN: the quiet pattern
+    (0x7F800001, 0x7FC0),  # a signalling NaN whose payload would round into +inf
+    (0xFFC00000, 0x7FC0),  # a negative NaN
+    (0xFFFFFFFF, 0x7FC0),
+]
+
+
+def check_bf16_round(bf16_round):
+    bits = np.array([c[0] for c in BF16_CASES], dtype=np.uint32)
+    got = bf16_round(bits.view(np.float32))
+    assert got.dtype == np.uint16 and got.shape == bits.shape
+    for (x, want), g in zip(BF16_CASES, got.tolist()):
+        assert g == want, f"fp32 {x:#010x}: got {g:#06x}, want {want:#06x}"
+    # Against an independent implementation: torch's fp32 -> bf16 conversion,
+    # over random bit patterns (every exponent, both signs, subnormals, inf,
+    # NaN), exact ties of both parities and their neighbours.  torch writes
+    # NaN as 0xFFFF; the oracle writes the quiet NaN 0x7FC0 (checked above),
+    # so NaN inputs need only give a NaN here.
+    import torch
+    rng = np.random.default_rng(2609)
+    rand = rng.integers(0, 1 << 32, size=1 << 20, dtype=np.uint64).astype(np.uint32)
+    hi = rng.integers(0, 1 << 16, size=1 << 16, dtype=np.uint64).astype(np.uint32) << np.uint32(16)
+    ties = np.concatenate([hi | np.uint32(0x8000), hi | np.uint32(0x7FFF), hi | np.uint32(0x8001), hi])
+    bits = np.concatenate([rand, ties])
+    x = bits.view(np.float32)
+    got = bf16_round(x)
+    want = torch.from_numpy(x.copy()).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    nan = np.isnan(x)
+    assert nan.any() and np.array_equal(got[~nan], want[~nan])
+    assert np.all(got[nan] == 0x7FC0)
+    # and the value view: each result is one of the two bf16 neighbours of x,
+    # the nearer one (finite, non-overflowing inputs)
+    with np.errstate(invalid="ignore"):  # signalling NaNs raise the flag when widened
+        fin = np.isfinite(x) & (np.abs(x.astype(np.float64)) < 3.38e38)
+    xv = x[fin].astype(np.float64)
+    gv = (got[fin].astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    down = ((bits[fin] >> np.uint32(16)) << np.uint32(16)).view(np.float32).astype(np.float64)
+    up = (((bits[fin] >> np.uint32(16)) + np.uint32(1)) << np.uint32(16)).view(np.float32).astype(np.float64)
+    assert np.all((gv == down) | (gv == up))
+    assert np.all(np.abs(gv - xv) <= np.minimum(np.abs(down - xv), np.abs(up - xv)))
+
+
+# ------------------------------------------------ the parity-protocol resync -
+def _resync_pair(cls, mode, k0_a, k0_b):
+    """Two identical three-layer states; W moves by 2^-8 from 0.5, so every
+    layer scores u = 2^-7 exactly at step 1 (eps_w = 0)."""
+    out = []
+    for k0 in (k0_a, k0_b):
+        segs = _const_layout(3)
+        orc = cls(segs, 3, O.DT_F32, True, mode, k0, s_max=100, eps_w=0.0)
+        orc.pack(0, 1 << 30)
+        for s in segs:
+            s.weight[...] = 0.5 + 2.0 ** -8
+        orc.score(1)
+        orc.select(1, 1.0)
+        out.append((orc, segs))
+    return out
+
+
+def _same_state(a, b, segs_a, segs_b):
+    assert a.delta == b.delta, (a.delta, b.delta)
+    assert a.t_last == b.t_last, (a.t_last, b.t_last)
+    assert np.array_equal(a.mask, b.mask), (a.mask, b.mask)
+    assert a.unpacked == b.unpacked, (a.unpacked, b.unpacked)
+    pa, ra = a.pack(0, 1 << 30)
+    pb, rb = b.pack(0, 1 << 30)
+    assert np.array_equal(pa, pb) and ra == rb
+    for x, y in zip(segs_a, segs_b):
+        assert np.array_equal(x.shadow, y.shadow)
+    # one more step: the accumulators carry on from the same values
+    for segs in (segs_a, segs_b):
+        for s in segs:
+            s.weight[...] = 0.5 + 2.0 ** -7
+    a.score(2)
+    b.score(2)
+    assert a.delta == b.delta and a.u == b.u
+
+
+def check_resync(cls):
+    """The parity protocol lets the oracle adopt the other side's decision on
+    a layer whose accumulator lies within the tolerance band of K.  Adopting
+    a decision must leave exactly the state that taking it directly leaves:
+    persisting resets Delta and t_l (Eq. 4) and the layer joins the pack;
+    not persisting keeps the accumulated Delta and the older t_l."""
+    never, always = 1e300, 0.0
+    for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
+        # persist layer 1 by resync == persist it by drift
+        (direct, sd), (adopted, sa) = _resync_pair(cls, mode, [never, always, never], [never, never, never])
+        assert list(adopted.mask) == [0, 0, 0]
+        adopted.resync(1, True)
+        _same_state(direct, adopted, sd, sa)
+        # drop layer 1 by resync == never select it
+        (direct, sd), (adopted, sa) = _resync_pair(cls, mode, [never, never, always], [never, always, always])
+        assert list(adopted.mask) == [0, 1, 1]
+        adopted.resync(1, False)
+        assert adopted.delta[1] == 2.0 ** -7  # the accumulated drift is back
+        _same_state(direct, adopted, sd, sa)
+        # adopting the decision already taken changes nothing
+        (direct, sd), (adopted, sa) = _resync_pair(cls, mode, [never, always, never], [never, always, never])
+        adopted.resync(0, False)
+        adopted.resync(1, True)
+        _same_state(direct, adopted, sd, sa)
+    segs = _const_layout(2)
+    orc = cls(segs, 2, O.DT_F32, True, O.MODE_ACCUM, [1.0, 1.0], s_max=100)
+    orc.pack(0, 1 << 30)
+    orc.score(1)
+    expect_error(lambda: orc.resync(0, True), O.LC_ERR_BAD_STATE)  # no selection to adjust
+
+
+# -------------------------------------------- a selection must be packed ----
+def check_unpacked_selection_blocks(cls):
+    """Eq. 4 resets Delta and t_l of a selected layer as if it were persisted,
+    so the next score or optimizer step refuses while a selection made by
+    ``select`` or ``rebase`` has layers not yet packed (both modes; the state
+    is left as it was), and goes ahead once the rest is packed.  The base
+    pending at init resets nothing: in ACCUM mode a warm-up may leave it
+    unpacked, while SNAPSHOT mode needs it packed first."""
+    for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
+        segs = _const_layout(3)
+        orc = cls(segs, 3, O.DT_F32, True, mode, [0.0, 0.0, 1e300], s_max=100, eps_w=0.0)
+        if mode == O.MODE_SNAPSHOT:
+            expect_error(lambda: orc.score(1), O.LC_ERR_BAD_STATE)
+        orc.pack(0, 1 << 30)
+        for s in segs:
+            s.weight[...] = 0.5 + 2.0 ** -8
+        orc.score(1)
+        mask, _ = orc.select(1, 1.0)
+        assert list(mask) == [1, 1, 0]
+        state = (list(orc.delta), list(orc.t_last))
+        expect_error(lambda: orc.score(2), O.LC_ERR_BAD_STATE)
+        orc.pack(0, orc.R[0])  # the first record only
+        expect_error(lambda: orc.score(2), O.LC_ERR_BAD_STATE)
+        if mode == O.MODE_ACCUM:
+            grads = [np.zeros(3, np.float32) for _ in segs]
+            expect_error(lambda: orc.sgd_step_score(2, grads, 1e-3, 0.0), O.LC_ERR_BAD_STATE)
+        assert (list(orc.delta), list(orc.t_last)) == state
+        orc.pack(1, 1 << 30)
+        orc.score(2)
+        # a base checkpoint taken again blocks the same way until packed
+        orc.select(2, 1.0)
+        orc.pack(0, 1 << 30)
+        orc.rebase(2)
+        expect_error(lambda: orc.score(3), O.LC_ERR_BAD_STATE)
+        orc.pack(0, 1 << 30)
+        orc.score(3)
+    # ACCUM warm-up: the init base may stay unpacked; the first step drops it
+    segs = _const_layout(2)
+    orc = cls(segs, 2, O.DT_F32, True, O.MODE_ACCUM, [1e300, 1e300], s_max=100)
+    orc.score(1)
+    assert orc.unpacked == set()
+    # ... and the base that ends the warm-up must be packed before the next step
+    orc.rebase(1)
+    expect_error(lambda: orc.score(2), O.LC_ERR_BAD_STATE)
+    orc.pack(0, 1 << 30)
+    orc.score(2)
+    orc.select(2, 1.0)  # nothing is due: the next step goes ahead
+    orc.score(3)

@@ -239,3 +239,32 @@ def test_init_refuses_memory_hip_does_not_know(lib):
         LC.lc_init_layout(desc(segs, 2))
     assert e.value.code == LC.LC_ERR_INVALID_ARG
     assert "not device memory" in lib.lc_last_error().decode()
+
+
+def test_build_info(lib):
+    info = LC.lc_query_build()
+    assert info["record_align"] == 256
+    assert info["chunk_bytes"] % (16 * 256) == 0 and info["piece_bytes"] % (16 * 256) == 0
+
+
+def test_reduced_layouts_span_tiles(lib):
+    """The reduced layouts of the GPU parity tests reach every kernel path at
+    the tile sizes this build reports: for each array, some tensor spans full
+    tiles and ends in a ragged one (score chunks over the weights; pack and
+    restore pieces over the weights, master and moments), and some tensor is
+    smaller than one tile."""
+    from paper_2609_27193_amd import inputs as I
+    from tests.test_parity_gpu import reduced_13b, reduced_8b, reduced_qwen, tied_spec
+    info = LC.lc_query_build()
+    for spec in (reduced_8b(), reduced_qwen(), reduced_13b(), tied_spec()):
+        sizes = [t.numel for l in spec.layers for t in l.tensors]
+        w = spec.weight_bytes
+        arrays = [("weight", w, (info["chunk_bytes"], info["piece_bytes"]))]
+        arrays += [(a, 4, (info["piece_bytes"],)) for a in (["master"] if spec.has_master else [])
+                   + ["exp_avg", "exp_avg_sq"]]
+        for name, esz, tiles in arrays:
+            for tile in tiles:
+                nbytes = [n * esz for n in sizes]
+                assert any(b > tile and b % tile for b in nbytes), (spec.name, name, tile)
+                assert any(b < tile for b in nbytes), (spec.name, name, tile)
+                assert sum(b // tile for b in nbytes) >= 8, (spec.name, name, tile)

@@ -85,6 +85,26 @@ MUTANTS = {
                                   "_, _, _, u = layer_update_score([s._p_old for s in g], [s._p_new for s in g], DT_F32, self.eps_w)"),
     "adamw_weights_not_rounded": ("s.weight[...] = bf16_round(p_new) if self.dtype == DT_BF16 else p_new",
                                   "s.weight[...] = (p_new.view(np.uint32) >> 16).astype(np.uint16) if self.dtype == DT_BF16 else p_new"),
+    "bf16_ties_away": ("r = ((b + np.uint64(0x7FFF) + ((b >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)).astype(np.uint16)",
+                       "r = ((b + np.uint64(0x8000)) >> np.uint64(16)).astype(np.uint16)"),
+    "bf16_truncates": ("r = ((b + np.uint64(0x7FFF) + ((b >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)).astype(np.uint16)",
+                       "r = (b >> np.uint64(16)).astype(np.uint16)"),
+    "bf16_ties_to_odd": ("r = ((b + np.uint64(0x7FFF) + ((b >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)).astype(np.uint16)",
+                         "r = ((b + np.uint64(0x8000) - ((b >> np.uint64(16)) & np.uint64(1))) >> np.uint64(16)).astype(np.uint16)"),
+    "bf16_nan_unquieted": ("        r[nan] = np.uint16(0x7FC0)", "        pass"),
+    "resync_unpersist_keeps_reset": ("            self.delta[layer] = self._pre_delta[layer]\n", ""),
+    "resync_unpersist_keeps_timestamp": ("            self.t_last[layer] = self._pre_t_last[layer]\n", ""),
+    "resync_persist_keeps_delta": ("            self.mask[layer] = 1\n            self.delta[layer] = 0.0\n",
+                                   "            self.mask[layer] = 1\n"),
+    "resync_persist_no_timestamp": ("            self.t_last[layer] = self.mask_step\n", ""),
+    "resync_persist_not_packed": ("            self.unpacked.add(layer)\n", ""),
+    "resync_unpersist_still_packed": ("            self.unpacked.discard(layer)\n", ""),
+    "accum_drops_unpacked_selection": ("if self.unpacked and (self.pending_persists or self.mode == MODE_SNAPSHOT):",
+                                       "if self.unpacked and self.mode == MODE_SNAPSHOT:"),
+    "rebase_selection_droppable": ("        self.unpacked = set(range(self.N))\n        self.pending_persists = True\n\n    def stats(",
+                                   "        self.unpacked = set(range(self.N))\n\n    def stats("),
+    "init_base_blocks_warmup": ("        self.pending_persists = False\n\n    def _require_packed",
+                                "        self.pending_persists = True\n\n    def _require_packed"),
 }
 
 
@@ -103,8 +123,10 @@ def all_checks(M):
         P.check_zero_change, P.check_eps_in_denominator, P.check_scale_invariance,
         P.check_exact_rational)]
     cls = M.LayerCheckOracle
+    yield lambda: P.check_bf16_round(M.bf16_round)
     for c in (P.check_ge_threshold, P.check_k0_extremes, P.check_record_format, P.check_capacity,
-              P.check_restore_errors, P.check_accum_equals_snapshot_first_step):
+              P.check_restore_errors, P.check_accum_equals_snapshot_first_step, P.check_resync,
+              P.check_unpacked_selection_blocks):
         yield lambda c=c: c(cls)
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
         yield lambda mode=mode: P.check_staleness_period(cls, mode)

@@ -17,7 +17,8 @@ def test_score_pins(check):
 
 @pytest.mark.parametrize("check", [P.check_ge_threshold, P.check_k0_extremes, P.check_record_format,
                                    P.check_capacity, P.check_restore_errors,
-                                   P.check_accum_equals_snapshot_first_step],
+                                   P.check_accum_equals_snapshot_first_step, P.check_resync,
+                                   P.check_unpacked_selection_blocks],
                          ids=lambda f: f.__name__)
 def test_state_pins(check):
     check(O.LayerCheckOracle)
@@ -46,6 +47,12 @@ def test_stats_invariants(mode):
 @pytest.mark.parametrize("mode", [O.MODE_ACCUM, O.MODE_SNAPSHOT])
 def test_restore_roundtrip(mode):
     P.check_restore_roundtrip(O.LayerCheckOracle, mode)
+
+
+def test_bf16_round():
+    """Section 4.1's bf16 weight copy: round to nearest, ties to even, against
+    hand-worked bit patterns and torch's independent conversion."""
+    P.check_bf16_round(O.bf16_round)
 
 
 def test_fourteen_bytes_per_param():

@@ -1,8 +1,9 @@
 """GPU parity: the HIP library through its C interface against the CPU oracle.
 
 Sizes are chosen so the oracle finishes in seconds while the layouts still
-span many score chunks (32768 bf16 / 16384 fp32 elements) and pack pieces
-(64 KiB) with ragged tails.
+span many score chunks and pack pieces (8 KiB each: 4096 bf16 / 2048 fp32
+elements per chunk) with ragged tails; test_reduced_layouts_span_tiles
+checks that against the tile sizes the library reports.
 """
 import numpy as np
 import pytest
@@ -28,7 +29,7 @@ def k0_for(spec, base):
 
 
 def reduced_8b():
-    return I.scaled_spec(I.llama3_8b_spec(), hidden=256, ffn=896, n_blocks=4, vocab=1000, n_q=8, n_kv=2)
+    return I.scaled_spec(I.llama3_8b_spec(), hidden=256, ffn=896, n_blocks=4, vocab=1003, n_q=8, n_kv=2)
 
 
 def reduced_qwen():
@@ -37,7 +38,7 @@ def reduced_qwen():
 
 
 def reduced_13b():
-    return I.scaled_spec(I.llama2_13b_spec(), hidden=320, ffn=864, n_blocks=4, vocab=640, n_q=5, n_kv=5)
+    return I.scaled_spec(I.llama2_13b_spec(), hidden=320, ffn=864, n_blocks=4, vocab=641, n_q=5, n_kv=5)
 
 
 def run_steps(p, steps, lr=lambda t: 1.0, capacity=None, stats=None):
@@ -289,6 +290,71 @@ def test_state_machine_errors():
         expect(I_, lambda: LC.lc_restore_composite(p.ctx, [dict(v0, payload_bytes=sum(p.R) - 256)], 3, p.N))
         expect(I_, lambda: LC.lc_restore_composite(p.ctx, [], 3, p.N))
         p.check_arrays()  # failed calls changed nothing
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_unpacked_selection_blocks_the_next_step(mode):
+    """Eq. 4 resets Delta and t_l of a selected layer as if it were persisted,
+    so a selection must be packed in full before the next score or optimizer
+    step: both sides refuse (LC_ERR_BAD_STATE, state unchanged) while a record
+    is missing, also after a base taken again with lc_rebase, and continue in
+    parity once the rest is packed."""
+    import torch
+    spec = reduced_8b()
+    p = Pair(spec, mode, k0_for(spec, 1e-9))  # every layer persists by drift
+    try:
+        def refused(fn_lib, fn_orc):
+            with pytest.raises(LC.LCError) as e:
+                fn_lib()
+            assert e.value.code == LC.LC_ERR_BAD_STATE, str(e.value)
+            with pytest.raises(O.OracleError) as e:
+                fn_orc()
+            assert e.value.code == O.LC_ERR_BAD_STATE
+
+        p.pack(0, np.ones(p.N, np.uint8))
+        p.advance(1)
+        d, tl = p.score(1)
+        mask, _ = p.select(1, 1.0, d, tl)
+        assert mask.all()
+        state = LC.lc_read_state(p.ctx, p.N)
+        # one record packed, the rest not
+        st = torch.empty(p.R[0], dtype=torch.uint8, device="cuda")
+        res = LC.lc_pack_selected(p.ctx, st.data_ptr(), p.R[0], 0)
+        pay_o, res_o = p.orc.pack(0, p.R[0])
+        assert res == res_o and not res["done"]
+        torch.cuda.synchronize()
+        assert np.array_equal(torch_bytes(st), pay_o)
+        p.advance(2)
+        refused(lambda: LC.lc_score_layers(p.ctx, 2), lambda: p.orc.score(2))
+        if mode == LC.LC_MODE_ACCUM:
+            g = torch.zeros(spec.numel, dtype=torch.bfloat16, device="cuda")
+            ptrs = [g[s.offset:s.offset + s.numel].data_ptr() for s in p.gen.segments]
+            grads = [np.zeros(s.numel, np.float32) for s in p.gen.segments]
+            refused(lambda: LC.lc_sgd_step_score(p.ctx, 2, ptrs, LC.LC_DT_BF16, 1e-3, 0.0),
+                    lambda: p.orc.sgd_step_score(2, grads, 1e-3, 0.0))
+        after = LC.lc_read_state(p.ctx, p.N)
+        for a, b in zip(state, after):
+            assert np.array_equal(a, b)
+        # the rest of the selection, then the step goes ahead in parity
+        total = sum(p.R[1:])
+        st = torch.empty(total, dtype=torch.uint8, device="cuda")
+        res = LC.lc_pack_selected(p.ctx, st.data_ptr(), total, 1)
+        pay_o, res_o = p.orc.pack(1, total)
+        assert res == res_o and res["done"]
+        torch.cuda.synchronize()
+        assert np.array_equal(torch_bytes(st), pay_o)
+        p.check_arrays()
+        d, tl = p.score(2)
+        mask, _ = p.select(2, 1.0, d, tl)
+        p.pack(2, mask)
+        # a base taken again blocks the same way until it is packed
+        p.rebase(2)
+        p.advance(3)
+        refused(lambda: LC.lc_score_layers(p.ctx, 3), lambda: p.orc.score(3))
+        p.pack(2, np.ones(p.N, np.uint8))
+        p.step(3)
     finally:
         p.close()
 
