@@ -174,6 +174,35 @@ lc_status lc_init_layout(const lc_layout_desc *d, lc_ctx **out);
  * otherwise asynchronous. */
 lc_status lc_score_layers(lc_ctx *c, int64_t step);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the score
+ * of lc_score_layers with no context and no allocation.  For every layer of
+ * the segment list, u_l = mean|W_l - S_l| / (mean|S_l| + eps_w) between its
+ * `weight` and `shadow` arrays (the other segment fields are ignored), with
+ * the same kernels, chunking and fixed-order sums as lc_score_layers, so u_l
+ * is bit-identical to the u_l that lc_score_layers reports for the same
+ * arrays.  Nothing is accumulated or written besides u_out: no Delta, no
+ * shadow refresh, no state.
+ *   segments:     host array, grouped by ascending layer, every layer in
+ *                 [0, n_layers) present; weight and shadow device memory of
+ *                 numel elements of weight_dtype each
+ *   u_out:        device memory, n_layers doubles, written in full
+ *   stream:       hipStream_t of the current device (NULL = null stream)
+ * The device tables live in one fixed array per GPU of 16 MiB
+ * (LC_NOALLOC_SCRATCH_BYTES), which the library holds from the first call
+ * on that GPU until the process ends; a layout whose tables exceed it is
+ * scored in consecutive batches of whole layers (about 6.9 GB of bf16
+ * weights per batch), and a single layer whose tables alone exceed it is
+ * refused with LC_ERR_CAPACITY before any work.  The call allocates no
+ * device or pinned memory (small host-side tables live in ordinary heap
+ * memory until it returns).  Every call on one GPU uses that GPU's array:
+ * calls that overlap on one GPU (two host threads, or two streams whose
+ * work overlaps) race and give wrong scores.  Argument errors:
+ * LC_ERR_INVALID_ARG before any work.  Returns after u_out is written
+ * (synchronises the stream). */
+lc_status lc_score_layers_static(const lc_segment *segments, uint32_t n_segments, uint32_t n_layers,
+                                 int32_t weight_dtype, double eps_w, double *u_out, void *stream);
+
 /* Eq. 3-5 for every layer: K_l = K0_l * lr_scale (lr_scale = s(lr(t)) > 0,
  * finite); select l when Delta_l >= K_l or step - t_l >= S_max; a selected
  * layer gets Delta_l = 0 and t_l = step (Eq. 4), so its record must be packed

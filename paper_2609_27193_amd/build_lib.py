@@ -12,7 +12,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 LIB = os.path.join(HERE, "liblayercheck.so")
-SOURCES = ["lc_runtime.cpp", "lc_store.cpp", "lc_kernels.hip", "lc_optim.hip"]
+SOURCES = ["lc_runtime.cpp", "lc_store.cpp", "lc_kernels.hip", "lc_optim.hip", "lc_noalloc.hip"]
 
 HIPCC_FLAGS = [
     "--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC", "-shared",

@@ -27,7 +27,7 @@ EXPORTED = ("lc_query_build", "lc_query_layout", "lc_init_layout", "lc_score_lay
             "lc_restore_composite", "lc_rebase", "lc_adamw_step_score", "lc_sgd_step_score", "lc_store_open",
             "lc_store_append", "lc_store_append_async", "lc_store_sync", "lc_store_count", "lc_store_entry",
             "lc_store_plan", "lc_store_restore", "lc_store_compact", "lc_store_discard_after", "lc_store_close",
-            "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error")
+            "lc_read_state", "lc_record_bytes", "lc_destroy", "lc_last_error", "lc_score_layers_static")
 
 
 class lc_segment(C.Structure):
@@ -95,6 +95,8 @@ def load_library(path: str = LIB_PATH):
             "lc_query_layout": (C.c_int, [P(lc_layout_desc), P(C.c_uint64), P(C.c_uint64)]),
             "lc_init_layout": (C.c_int, [P(lc_layout_desc), P(C.c_void_p)]),
             "lc_score_layers": (C.c_int, [C.c_void_p, C.c_int64]),
+            "lc_score_layers_static": (C.c_int, [P(lc_segment), C.c_uint32, C.c_uint32, C.c_int32, C.c_double,
+                                                 C.c_void_p, C.c_void_p]),
             "lc_select": (C.c_int, [C.c_void_p, C.c_int64, C.c_double, P(C.c_uint8), P(lc_select_stats)]),
             "lc_pack_selected": (C.c_int, [C.c_void_p, C.c_void_p, C.c_uint64, C.c_uint32, P(lc_pack_result)]),
             "lc_restore_composite": (C.c_int, [C.c_void_p, P(lc_version), C.c_uint32, C.c_int64, P(C.c_int64)]),
@@ -186,6 +188,17 @@ def lc_init_layout(layout: LayoutDesc) -> C.c_void_p:
 
 def lc_score_layers(ctx, step: int) -> None:
     _check(load_library().lc_score_layers(ctx, step), "lc_score_layers")
+
+
+def lc_score_layers_static(segments: Sequence["Segment"], n_layers: int, weight_dtype: int, eps_w: float,
+                           u_out: int, stream: int = 0) -> None:
+    """u_out: device address of n_layers doubles."""
+    arr = (lc_segment * len(segments))()
+    for i, s in enumerate(segments):
+        arr[i] = lc_segment(s.layer, 0, s.numel, s.weight, s.shadow or None, s.master or None,
+                            s.exp_avg or None, s.exp_avg_sq or None)
+    _check(load_library().lc_score_layers_static(arr, len(segments), n_layers, weight_dtype, eps_w,
+                                                 u_out or None, stream or None), "lc_score_layers_static")
 
 
 def lc_select(ctx, step: int, lr_scale: float, n_layers: Optional[int] = None):

@@ -268,3 +268,24 @@ def test_reduced_layouts_span_tiles(lib):
                 assert any(b > tile and b % tile for b in nbytes), (spec.name, name, tile)
                 assert any(b < tile for b in nbytes), (spec.name, name, tile)
                 assert sum(b // tile for b in nbytes) >= 8, (spec.name, name, tile)
+
+
+def test_static_score_refuses_before_any_device_work(lib):
+    """lc_score_layers_static checks its arguments and sizes on the host before
+    it touches the GPU: a layer whose tables exceed the fixed device array is
+    refused with LC_ERR_CAPACITY, malformed lists with LC_ERR_INVALID_ARG."""
+    big = fake_segments([[1 << 30], [4_000_000_000]])  # 4e9 bf16 weights: ~19 MB of chunk tables
+    u = 0x7E0000000000
+
+    def status(segs, n_layers, dtype=LC.LC_DT_BF16, u_out=u):
+        arr = (LC.lc_segment * len(segs))()
+        for i, s in enumerate(segs):
+            arr[i] = LC.lc_segment(s.layer, 0, s.numel, s.weight, s.shadow, None, None, None)
+        return lib.lc_score_layers_static(arr, len(segs), n_layers, dtype, 1e-8, u_out, None)
+
+    assert status(big, 2) == LC.LC_ERR_CAPACITY
+    assert b"layer 1" in LC.load_library().lc_last_error()
+    assert status(big, 3) == LC.LC_ERR_INVALID_ARG        # layer 2 has no segment
+    assert status(big[::-1], 2) == LC.LC_ERR_INVALID_ARG  # not grouped by ascending layer
+    assert status(big, 2, dtype=5) == LC.LC_ERR_INVALID_ARG
+    assert status(big, 2, u_out=None) == LC.LC_ERR_INVALID_ARG
