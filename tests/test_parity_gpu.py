@@ -303,7 +303,7 @@ def test_unpacked_selection_blocks_the_next_step(mode):
     parity once the rest is packed."""
     import torch
     spec = reduced_8b()
-    p = Pair(spec, mode, k0_for(spec, 1e-9))  # every layer persists by drift
+    p = Pair(spec, mode, k0_for(spec, 0.0))  # K0 = 0: every layer persists by drift every step
     try:
         def refused(fn_lib, fn_orc):
             with pytest.raises(LC.LCError) as e:
