@@ -43,7 +43,9 @@ typedef enum {
   LC_ERR_CAPACITY = 3,    /* next record does not fit the staging buffer  */
   LC_ERR_NO_VERSION = 4,  /* a layer has no persisted record <= t_fail    */
   LC_ERR_HIP = 5,         /* a HIP runtime call failed                    */
-  LC_ERR_OOM = 6          /* host or device allocation of library tables  */
+  LC_ERR_OOM = 6,         /* host or device allocation of library tables  */
+  LC_ERR_IO = 7           /* a file operation of the persistence store
+                             failed (the message names it and its errno) */
 } lc_status;
 
 typedef enum { LC_DT_BF16 = 1, LC_DT_F32 = 2 } lc_dtype;
@@ -320,7 +322,12 @@ lc_status lc_sgd_step_score(lc_ctx *c, int64_t step, const void *const *grads, i
  * become visible in the order they were appended.  A directory is open in at
  * most one store at a time (an exclusive lock on its "store.lock" file, held
  * until lc_store_close): a second lc_store_open of it, from this process or
- * another, returns LC_ERR_BAD_STATE. */
+ * another, returns LC_ERR_BAD_STATE.  Any failed file operation (create,
+ * open, read, write, fsync, rename, lock) returns LC_ERR_IO with the path and
+ * errno in lc_last_error().  A writer thread's failure drops the version it
+ * was writing (the manifest never names it) and is reported by the call that
+ * meets it and by every later append, lc_store_sync and compaction, all with
+ * LC_ERR_IO; the history already durable stays readable. */
 typedef struct lc_store lc_store;
 
 /* Opens (creating the directory itself, not its parents) the store of a

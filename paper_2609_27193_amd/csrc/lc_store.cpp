@@ -294,7 +294,7 @@ lc_status parse_manifest(lc_store* s) {
       const ssize_t r = read(s->manifest_fd, buf, sizeof(buf));
       if (r < 0) {
         if (errno == EINTR) continue;
-        return fail(LC_ERR_INVALID_ARG, "cannot read the manifest: %s", std::strerror(errno));
+        return fail(LC_ERR_IO, "cannot read the manifest: %s", std::strerror(errno));
       }
       if (r == 0) break;
       text.append(buf, static_cast<size_t>(r));
@@ -306,7 +306,7 @@ lc_status parse_manifest(lc_store* s) {
     if (nl == std::string::npos) {  // torn last line: never durable, cut it off
       ++s->skipped;
       if (ftruncate(s->manifest_fd, static_cast<off_t>(pos)) != 0 || fsync(s->manifest_fd) != 0)
-        return fail(LC_ERR_INVALID_ARG, "cannot repair the manifest: %s", std::strerror(errno));
+        return fail(LC_ERR_IO, "cannot repair the manifest: %s", std::strerror(errno));
       break;
     }
     const std::string line = text.substr(pos, nl - pos);
@@ -434,7 +434,7 @@ lc_status wait_idle(lc_store* s) {
   s->cv.wait(lk, [&] { return s->outstanding == 0 && s->next_final == s->writing.size(); });
   s->writing.clear();
   s->next_final = 0;
-  if (!s->writer_error.empty()) return fail(LC_ERR_BAD_STATE, "store failed: %s", s->writer_error.c_str());
+  if (!s->writer_error.empty()) return fail(LC_ERR_IO, "store failed: %s", s->writer_error.c_str());
   return LC_OK;
 }
 
@@ -467,7 +467,7 @@ lc_status keep_only(lc_store* s, const std::vector<uint8_t>& keep, uint32_t* rem
     const std::string mpath = s->dir + "/manifest.lcm", tpath = s->dir + "/manifest.lcm.tmp";
     // the descriptor of the new file becomes the manifest's once renamed
     const int fd = open(tpath.c_str(), O_RDWR | O_CREAT | O_TRUNC, 0644);
-    if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", tpath.c_str(), std::strerror(errno));
+    if (fd < 0) return fail(LC_ERR_IO, "cannot create %s: %s", tpath.c_str(), std::strerror(errno));
     std::string text;
     for (const StoredVersion& v : kept) text += manifest_line(v);
     if (!write_all(fd, reinterpret_cast<const uint8_t*>(text.data()), text.size(), 0) || fsync(fd) != 0 ||
@@ -475,13 +475,13 @@ lc_status keep_only(lc_store* s, const std::vector<uint8_t>& keep, uint32_t* rem
       const int err = errno;
       close(fd);
       (void)unlink(tpath.c_str());
-      return fail(LC_ERR_INVALID_ARG, "rewriting the manifest failed: %s", std::strerror(err));
+      return fail(LC_ERR_IO, "rewriting the manifest failed: %s", std::strerror(err));
     }
     close(s->manifest_fd);
     s->manifest_fd = fd;
     s->durable = kept;
     if (!fsync_dir(s->dir))
-      return fail(LC_ERR_INVALID_ARG, "directory fsync after the manifest rewrite failed: %s", std::strerror(errno));
+      return fail(LC_ERR_IO, "directory fsync after the manifest rewrite failed: %s", std::strerror(errno));
   }
   uint32_t removed = 0;
   for (const std::string& f : gone)
@@ -559,7 +559,7 @@ lc_status restore_pipeline(lc_store* s, lc_ctx* c, const std::vector<size_t>& ch
       std::unique_lock<std::mutex> lk(mu);
       cv.wait(lk, [&] { return failed || read_done[i]; });
       if (!read_done[i]) {
-        st = fail(LC_ERR_INVALID_ARG, "reading a stored record failed");
+        st = fail(LC_ERR_IO, "reading a stored record failed");
         break;
       }
     }
@@ -606,7 +606,7 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
     if (record_bytes[l] == 0 || record_bytes[l] % kRecordAlign)
       return fail(LC_ERR_INVALID_ARG, "record_bytes[%u] must be a positive multiple of %u", l, kRecordAlign);
   if (mkdir(dir, 0755) != 0 && errno != EEXIST)
-    return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", dir, std::strerror(errno));
+    return fail(LC_ERR_IO, "cannot create %s: %s", dir, std::strerror(errno));
   lc_store* s = new (std::nothrow) lc_store();
   if (!s) return fail(LC_ERR_OOM, "host allocation failed");
   s->dir = dir;
@@ -624,7 +624,7 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
   s->lock_fd = open(lpath.c_str(), O_RDWR | O_CREAT, 0644);
   if (s->lock_fd < 0) {
     delete s;
-    return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", lpath.c_str(), std::strerror(errno));
+    return fail(LC_ERR_IO, "cannot open %s: %s", lpath.c_str(), std::strerror(errno));
   }
   if (flock(s->lock_fd, LOCK_EX | LOCK_NB) != 0) {
     const int err = errno;
@@ -632,14 +632,14 @@ lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* reco
     delete s;
     if (err == EWOULDBLOCK)
       return fail(LC_ERR_BAD_STATE, "store %s is already open (another store holds its lock)", dir);
-    return fail(LC_ERR_INVALID_ARG, "cannot lock %s: %s", lpath.c_str(), std::strerror(err));
+    return fail(LC_ERR_IO, "cannot lock %s: %s", lpath.c_str(), std::strerror(err));
   }
   const std::string mpath = s->dir + "/manifest.lcm";
   s->manifest_fd = open(mpath.c_str(), O_RDWR | O_CREAT, 0644);
   if (s->manifest_fd < 0) {
     close(s->lock_fd);
     delete s;
-    return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", mpath.c_str(), std::strerror(errno));
+    return fail(LC_ERR_IO, "cannot open %s: %s", mpath.c_str(), std::strerror(errno));
   }
   lc_status st = parse_manifest(s);
   if (st != LC_OK) {
@@ -678,7 +678,7 @@ lc_status append_impl(lc_store* s, int64_t step, const uint8_t* mask, const void
   if (bytes && !payload) return fail(LC_ERR_INVALID_ARG, "payload is NULL");
   {
     std::lock_guard<std::mutex> lk(s->mu);
-    if (!s->writer_error.empty()) return fail(LC_ERR_BAD_STATE, "store failed earlier: %s", s->writer_error.c_str());
+    if (!s->writer_error.empty()) return fail(LC_ERR_IO, "store failed earlier: %s", s->writer_error.c_str());
     for (const auto* list : {&s->durable, &s->writing})
       for (const StoredVersion& o : *list)
         if (o.step == step)
@@ -702,7 +702,7 @@ lc_status append_impl(lc_store* s, int64_t step, const uint8_t* mask, const void
   v.file = name;
   const std::string path = s->dir + "/" + v.file;
   const int fd = open(path.c_str(), O_WRONLY | O_CREAT | O_TRUNC, 0644);
-  if (fd < 0) return fail(LC_ERR_INVALID_ARG, "cannot create %s: %s", path.c_str(), std::strerror(errno));
+  if (fd < 0) return fail(LC_ERR_IO, "cannot create %s: %s", path.c_str(), std::strerror(errno));
   size_t vi;
   v.fd = fd;
   // device payloads leave the pinned ring by direct I/O where the file system allows it
@@ -772,7 +772,7 @@ lc_status append_impl(lc_store* s, int64_t step, const uint8_t* mask, const void
         lk.unlock();
         abandon(s, vi, bytes - off, why.c_str());
         (void)hipStreamSynchronize(s->copy_stream);  // nothing reads the payload after an error return
-        return fail(LC_ERR_BAD_STATE, "store: %s", why.c_str());
+        return fail(LC_ERR_IO, "store: %s", why.c_str());
       }
       for (uint32_t k = 0; k < s->n_slots; ++k)
         if (s->slot_free[k]) {
@@ -896,7 +896,7 @@ lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chos
     const int fd = open(path.c_str(), O_RDONLY);
     if (fd < 0) {
       for (auto& kv : fds) close(kv.second);
-      return fail(LC_ERR_INVALID_ARG, "cannot open %s: %s", path.c_str(), std::strerror(errno));
+      return fail(LC_ERR_IO, "cannot open %s: %s", path.c_str(), std::strerror(errno));
     }
     fds[i] = fd;
   }

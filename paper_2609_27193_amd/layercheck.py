@@ -19,7 +19,8 @@ import numpy as np
 LIB_PATH = os.environ.get("LAYERCHECK_LIB") or os.path.join(os.path.dirname(os.path.abspath(__file__)),
                                                               "liblayercheck.so")
 
-LC_OK, LC_ERR_INVALID_ARG, LC_ERR_BAD_STATE, LC_ERR_CAPACITY, LC_ERR_NO_VERSION, LC_ERR_HIP, LC_ERR_OOM = range(7)
+LC_OK, LC_ERR_INVALID_ARG, LC_ERR_BAD_STATE, LC_ERR_CAPACITY, LC_ERR_NO_VERSION, LC_ERR_HIP, LC_ERR_OOM, \
+    LC_ERR_IO = range(8)
 LC_DT_BF16, LC_DT_F32 = 1, 2
 LC_MODE_ACCUM, LC_MODE_SNAPSHOT = 0, 1
 

@@ -229,7 +229,7 @@ def test_store_context_manager(lib, tmp_path):
 def test_write_failure_drops_the_version(lib, tmp_path):
     """An I/O failure in the writers (here the file-size limit of a child
     process, so a write fails with EFBIG) drops the version being written,
-    fails the call with LC_ERR_BAD_STATE and every later append too; the
+    fails the call with LC_ERR_IO and every later append too; the
     manifest never names the failed version, and the earlier history stays
     restorable after reopening."""
     import subprocess
@@ -258,7 +258,7 @@ print(codes)
 """
     r = subprocess.run([sys.executable, "-c", child], capture_output=True, text=True, timeout=120)
     assert r.returncode == 0, r.stderr
-    assert r.stdout.strip() == f"[{LC.LC_ERR_BAD_STATE}, {LC.LC_ERR_BAD_STATE}]", r.stdout
+    assert r.stdout.strip() == f"[{LC.LC_ERR_IO}, {LC.LC_ERR_IO}]", r.stdout
     st = LC.Store(d, [256 * 1024, 4 * 1024 * 1024])
     assert [e["step"] for e in st.entries()] == [0]
     assert "LCV1 1 " not in open(os.path.join(d, "manifest.lcm")).read()
@@ -319,3 +319,34 @@ def test_one_store_per_directory(lib, tmp_path):
     b = LC.Store(d, orc.R)
     assert [e["step"] for e in b.entries()]
     b.close()
+
+
+def test_file_failures_return_lc_err_io(lib, tmp_path):
+    """Every failed file operation of the store returns LC_ERR_IO, whatever
+    the call: opening a store under a missing parent, and, once the directory
+    of an open store is gone, creating a version file and rewriting the
+    manifest for a compaction or a discard.  Argument errors keep
+    LC_ERR_INVALID_ARG."""
+    import shutil
+    orc, versions = oracle_history(steps=3)
+    with pytest.raises(LC.LCError) as e:
+        LC.Store(str(tmp_path / "missing" / "store"), orc.R)
+    assert e.value.code == LC.LC_ERR_IO and "missing" in str(e.value)
+    d = str(tmp_path / "gone")
+    st = LC.Store(d, orc.R)
+    for v in versions:
+        st.append(v["step"], v["mask"], v["payload"].ctypes.data if len(v["payload"]) else 0, len(v["payload"]))
+    st.sync()
+    shutil.rmtree(d)
+    v = [x for x in versions[1:] if x["mask"].any()][0]
+    step = versions[-1]["step"] + 1
+    for call in (lambda: st.append(step, v["mask"], v["payload"].ctypes.data, len(v["payload"])),
+                 lambda: st.compact(versions[-1]["step"]),  # removes versions: rewrites the manifest
+                 lambda: st.discard_after(0)):
+        with pytest.raises(LC.LCError) as e:
+            call()
+        assert e.value.code == LC.LC_ERR_IO, str(e.value)
+    with pytest.raises(LC.LCError) as e:
+        st.append(step, v["mask"], v["payload"].ctypes.data, len(v["payload"]) - 256)
+    assert e.value.code == LC.LC_ERR_INVALID_ARG
+    st.close()
