@@ -67,6 +67,13 @@ def parse():
     ap.add_argument("--restore-bench", action="store_true",
                     help="measure the composite restore from device-resident and from pinned-host versions "
                          "(default workload llama3.2-1b)")
+    ap.add_argument("--placement-ceiling", action="store_true",
+                    help="after the timed steps, time the score and copy access patterns with no arithmetic "
+                         "over the same arrays (the ceiling of this placement in the memory interleave)")
+    ap.add_argument("--placement-sweep", action="store_true",
+                    help="with --placement-ceiling: also time the score pattern over the same arrays shifted "
+                         "against each other by a set of byte offsets, and the copy into the staging buffer at "
+                         "a set of offsets")
     ap.add_argument("--k0", type=float, default=None,
                     help="base threshold (skips the calibration window)")
     ap.add_argument("--json-out", default=None)
@@ -144,60 +151,146 @@ def calibrate_k0(u_hist: np.ndarray, embed_mask: np.ndarray, s_max: int, target:
     return 10.0 ** hi
 
 
-def cpu_baseline(state, spec, mode_name, n_layers=3):
-    """Time the oracle on the first ``n_layers`` transformer blocks of the same
-    state (host copy, D2H excluded): score + select (all forced) + pack."""
-    import torch
-    from oracle import layercheck_oracle as O
-    from paper_2609_27193_amd.inputs import to_numpy_weight
-
-    blocks = [i for i, l in enumerate(spec.layers) if l.name.startswith("block_")][:n_layers]
-    segs = [s for s in state.segments if s.layer in blocks]
-    a, b = segs[0].offset, segs[-1].offset + segs[-1].numel
-    t0 = time.perf_counter()
-    hW = to_numpy_weight(state.weight[a:b])
-    hS = to_numpy_weight(state.shadow[a:b])
-    hM = None if state.master is None else state.master[a:b].cpu().numpy()
-    hm = state.exp_avg[a:b].cpu().numpy()
-    hv = state.exp_avg_sq[a:b].cpu().numpy()
-    copy_s = time.perf_counter() - t0
-    osegs = []
-    for s in segs:
-        x, y = s.offset - a, s.offset - a + s.numel
-        osegs.append(O.OSegment(blocks.index(s.layer), hW[x:y], hS[x:y].copy(),
-                                None if hM is None else hM[x:y], hm[x:y], hv[x:y]))
-    dt = O.DT_BF16 if spec.weight_dtype == "bf16" else O.DT_F32
-    mode = O.MODE_ACCUM if mode_name == "accum" else O.MODE_SNAPSHOT
-    orc = O.LayerCheckOracle(osegs, len(blocks), dt, spec.has_master, mode, [0.0] * len(blocks), spec.s_max)
-    # the oracle's init set S <- W; restore the device shadow so the score sees real drift
-    for s, seg in zip(osegs, segs):
-        x = seg.offset - a
-        s.shadow[...] = hS[x:x + seg.numel]
-    if mode == O.MODE_SNAPSHOT:
-        orc.pack(0, 1 << 62)  # the pending base must be written first (untimed)
-    n = b - a
-    t1 = time.perf_counter()
-    orc.score(1)
-    orc.select(1, 1.0)
-    payload, _ = orc.pack(0, 1 << 62)
-    elapsed = time.perf_counter() - t1
-    w = spec.weight_bytes
-    score_bytes = (3 if mode == O.MODE_ACCUM else 2) * w * n
-    rec_unpadded = n * (w + 4 * (3 if spec.has_master else 2))
-    pack_bytes = rec_unpadded + len(payload) + (w * n if mode == O.MODE_SNAPSHOT else 0)
-    gbs = (score_bytes + pack_bytes) / elapsed / 1e9
-    cpu = "unknown CPU"
+def cpu_model() -> str:
     try:
         for line in open("/proc/cpuinfo"):
             if line.startswith("model name"):
-                cpu = line.split(":", 1)[1].strip()
-                break
+                return line.split(":", 1)[1].strip()
     except OSError:
         pass
-    return {"value": round(gbs, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-            "sample": f"{len(blocks)} transformer blocks ({n} params) of the same state: "
-                      f"score + select + pack in {elapsed:.2f} s, host copy {copy_s:.2f} s excluded; "
-                      f"numpy fp64, single thread on {cpu} ({len(os.sched_getaffinity(0))} cores visible)"}
+    return "unknown CPU"
+
+
+def cpu_baseline(state, spec, mode_name, sel_fraction, n_blocks=16):
+    """Time the oracle (unchanged, numpy fp64) on a bounded sample of the same
+    state with the GPU step's mix: ``n_blocks`` transformer blocks, of which
+    the share of parameters the timed GPU steps selected on average is
+    selected (K0 = 0 for those blocks, no threshold the others can reach, no
+    staleness due) and packed; host copies made beforehand, not timed.  The
+    oracle holds one layer per instance, so the sample runs as one instance
+    per block: first one after the other on one thread, then spread over a
+    thread per visible core (numpy releases the interpreter lock in its array
+    loops)."""
+    from concurrent.futures import ThreadPoolExecutor
+    from oracle import layercheck_oracle as O
+    from paper_2609_27193_amd.inputs import to_numpy_weight
+
+    blocks = [i for i, l in enumerate(spec.layers) if l.name.startswith("block_")][:n_blocks]
+    k_sel = max(1, int(round(sel_fraction * len(blocks))))
+    dt = O.DT_BF16 if spec.weight_dtype == "bf16" else O.DT_F32
+    mode = O.MODE_ACCUM if mode_name == "accum" else O.MODE_SNAPSHOT
+    w = spec.weight_bytes
+    t0 = time.perf_counter()
+    host = []
+    for b in blocks:
+        segs = [s for s in state.segments if s.layer == b]
+        a, e = segs[0].offset, segs[-1].offset + segs[-1].numel
+        arrs = {"W": to_numpy_weight(state.weight[a:e]), "S": to_numpy_weight(state.shadow[a:e]),
+                "M": None if state.master is None else state.master[a:e].cpu().numpy(),
+                "m": state.exp_avg[a:e].cpu().numpy(), "v": state.exp_avg_sq[a:e].cpu().numpy()}
+        host.append(([(s.offset - a, s.numel) for s in segs], arrs))
+    copy_s = time.perf_counter() - t0
+    n = sum(arrs["W"].size for _, arrs in host)
+    n_sel = sum(host[i][1]["W"].size for i in range(k_sel))
+
+    def make(i):
+        cuts, arrs = host[i]
+        osegs = [O.OSegment(0, arrs["W"][x:x + m], arrs["S"][x:x + m].copy(),
+                            None if arrs["M"] is None else arrs["M"][x:x + m], arrs["m"][x:x + m],
+                            arrs["v"][x:x + m]) for x, m in cuts]
+        orc = O.LayerCheckOracle(osegs, 1, dt, spec.has_master, mode, [0.0 if i < k_sel else float("inf")],
+                                 1 << 40)
+        for (x, m), sg in zip(cuts, osegs):  # construction set S <- W: put the device shadow back
+            sg.shadow[...] = arrs["S"][x:x + m]
+        if mode == O.MODE_SNAPSHOT:
+            orc.pack(0, 1 << 62)  # SNAPSHOT scores only after the pending base is packed (untimed)
+        return orc
+
+    def decide(orc):
+        orc.score(1)
+        mask, _ = orc.select(1, 1.0)
+        payload, _ = orc.pack(0, 1 << 62)
+        return int(mask[0]), len(payload)
+
+    legs = []
+    for threads in (1, max(1, min(len(blocks), len(os.sched_getaffinity(0))))):
+        oracles = [make(i) for i in range(len(blocks))]
+        t1 = time.perf_counter()
+        if threads == 1:
+            res = [decide(o) for o in oracles]
+        else:
+            with ThreadPoolExecutor(threads) as pool:
+                res = list(pool.map(decide, oracles))
+        elapsed = time.perf_counter() - t1
+        assert [r[0] for r in res] == [int(i < k_sel) for i in range(len(blocks))]
+        payload = sum(r[1] for r in res)
+        score_bytes = (3 if mode == O.MODE_ACCUM else 2) * w * n
+        pack_bytes = n_sel * (w + 4 * (3 if spec.has_master else 2)) + payload + (w * n_sel if mode == O.MODE_SNAPSHOT else 0)
+        legs.append({"value": round((score_bytes + pack_bytes) / elapsed / 1e9, 4), "cores": threads,
+                     "seconds": round(elapsed, 2)})
+        del oracles
+    best = legs[-1]
+    return {"value": best["value"], "unit": "GB/s", "cores": best["cores"], "kind": "oracle",
+            "legs": legs,
+            "sample": f"{len(blocks)} transformer blocks ({n} params) of the same state after one more "
+                      f"synthetic step; score all, select and pack {k_sel} ({n_sel / n:.1%} of the params, "
+                      f"the timed steps selected {sel_fraction:.1%}); host copy {copy_s:.1f} s excluded; "
+                      f"numpy fp64, one oracle per block, {legs[0]['seconds']:.1f} s on 1 thread, "
+                      f"{best['seconds']:.1f} s on {best['cores']} threads; {cpu_model()}, "
+                      f"{len(os.sched_getaffinity(0))} cores visible"}
+
+
+def placement_ceiling(state, staging, mode_name, score_gbs, pack_gbs, sweep=False):
+    """The access patterns of the score and pack kernels with no arithmetic
+    (the kernels' tile and block mapping, from the probe library) over the
+    very arrays the timed steps used: ACCUM's two reads and one write over W
+    and S (S <- W, which the last ACCUM score already left in place), or
+    SNAPSHOT's two reads, and a copy from the largest fp32 array into the
+    staging buffer.  A kernel's rate over this ceiling is what its arithmetic
+    and tables cost on top of where the arrays sit in the memory interleave."""
+    import ctypes as C
+    import torch
+    from paper_2609_27193_amd.build_lib import PROBE_LIB
+    if not os.path.exists(PROBE_LIB):
+        raise SystemExit("the probe library is built by __graft_entry__.build()")
+    lib = C.CDLL(PROBE_LIB)
+    lib.lc_probe_arrays.restype = C.c_int
+    lib.lc_probe_arrays.argtypes = [C.c_int, C.c_void_p, C.c_void_p, C.c_uint64, C.c_int, C.POINTER(C.c_double)]
+    torch.cuda.synchronize()
+
+    def rate(pattern, a, b, nbytes):
+        g = C.c_double()
+        if lib.lc_probe_arrays(pattern, a, b, nbytes, 8, C.byref(g)) != 0:
+            raise RuntimeError("lc_probe_arrays failed")
+        return g.value
+
+    w_bytes = state.weight.numel() * state.weight.element_size()
+    score_pattern = 3 if mode_name == "accum" else 1
+    ceil_score = rate(score_pattern, state.weight.data_ptr(), state.shadow.data_ptr(), w_bytes)
+    src = state.master if state.master is not None else state.exp_avg
+    n = min(src.numel() * 4, staging.numel())
+    ceil_copy = rate(2, src.data_ptr(), staging.data_ptr(), n)
+    out = {"score_pattern": "r2w1" if score_pattern == 3 else "read2", "score_gbs": round(ceil_score, 1),
+           "score_kernel_frac": round(score_gbs / ceil_score, 4), "copy_gbs": round(ceil_copy, 1),
+           "copy_bytes": n}
+    if pack_gbs:
+        out["pack_kernel_frac"] = round(pack_gbs / ceil_copy, 4)
+    if sweep:
+        # the shadow (or both arrays) entered `off` bytes later: tiles then pair
+        # W and S at other relative positions of the interleave
+        offs = (0, 256, 1024, 4096, 8192, 20480, 65536, 1 << 20)
+        out["score_vs_shadow_offset"] = {
+            o: round(rate(score_pattern, state.weight.data_ptr(), state.shadow.data_ptr() + o, w_bytes - (1 << 20)), 1)
+            for o in offs}
+        out["score_vs_both_offset"] = {
+            o: round(rate(score_pattern, state.weight.data_ptr() + o, state.shadow.data_ptr() + o, w_bytes - (1 << 20)), 1)
+            for o in offs}
+        out["copy_vs_staging_offset"] = {
+            o: round(rate(2, src.data_ptr(), staging.data_ptr() + o, n - (1 << 20)), 1) for o in offs}
+        if score_pattern == 3:  # the shifted r2w1 runs wrote W's bytes into S at an offset: S <- W again
+            state.shadow.copy_(state.weight)
+            torch.cuda.synchronize()
+    return out
 
 
 def main():
@@ -314,7 +407,8 @@ def main():
         row = {"t": t, "step_ms": ev[0].elapsed_time(ev[3]), "score_ms": ev[0].elapsed_time(ev[1]),
                "select_ms": ev[1].elapsed_time(ev[2]), "pack_ms": ev[2].elapsed_time(ev[3]),
                "wall_ms": wall * 1e3, "n_sel": st["n_selected"], "n_forced": st["n_forced"],
-               "pack_bytes": pack_bytes, "bytes": score_bytes + pack_bytes, "payload": packed}
+               "pack_bytes": pack_bytes, "bytes": score_bytes + pack_bytes, "payload": packed,
+               "sel_elems": sel_elems}
         log(f"[bench] {'warm' if i < warmup else 'time'} t={t} sel {st['n_selected']:2d}/{spec.n_layers} "
             f"(forced {st['n_forced']}) step {row['step_ms']:.3f} ms score {row['score_ms']:.3f} "
             f"select {row['select_ms']:.3f} pack {row['pack_ms']:.3f} "
@@ -349,11 +443,16 @@ def main():
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": traffic},
     }
+    if args.placement_ceiling:
+        out["placement_ceiling"] = placement_ceiling(state, staging, args.mode, achieved, pack_gbs,
+                                                     args.placement_sweep)
+        log(f"[bench] placement ceiling {out['placement_ceiling']}")
     if not args.no_cpu_baseline:
-        log("[bench] timing the CPU oracle on one block")
+        log("[bench] timing the CPU oracle on a sample of the state")
         state.step(t + 1)  # fresh drift against the current shadow (untimed)
         torch.cuda.synchronize()
-        out["cpu_baseline"] = cpu_baseline(state, spec, args.mode)
+        sel_params = float(np.mean([r["sel_elems"] for r in rows])) / P
+        out["cpu_baseline"] = cpu_baseline(state, spec, args.mode, sel_params)
     line = json.dumps(out)
     print(line, flush=True)
     if args.json_out:

@@ -147,7 +147,7 @@ lc_status lc_query_build(lc_build_info *out);
 lc_status lc_query_layout(const lc_layout_desc *d, uint64_t *numel_out,
                           uint64_t *record_bytes_out);
 
-/* Layer-aligned layout (Section 3.4 "Layer-aligned optimizer state layout"):
+/* Layer-aligned layout (Section 3.4: optimizer state laid out by layer):
  * builds the per-layer chunk and copy tables, allocates the small device
  * state, sets S <- W for every segment, Delta_l = 0 and t_l = t_base for every
  * layer (Section 3.2; the base full checkpoint of Section 3.4 counts as the
@@ -267,8 +267,8 @@ typedef struct {
  * stream.  LC_ERR_BAD_STATE for an earlier step or a poisoned context. */
 lc_status lc_rebase(lc_ctx *c, int64_t step);
 
-/* The optimizer step with the drift taken from the update itself (Section 3.4,
- * "Reusing the optimizer update to compute drift"; AdamW as trained in
+/* The optimizer step with the drift taken from the update itself (Section 3.4
+ * computes the drift inside the optimizer step; AdamW as trained in
  * Section 4.1).  For every element, in fp32 with one rounding per operation:
  *   m <- b1 m + (1-b1) g;  v <- b2 v + (1-b2) g*g;
  *   p_new = p * (1 - lr wd) - lr * (m / (1-b1^t)) / (sqrt(v / (1-b2^t)) + eps)
@@ -310,7 +310,7 @@ typedef struct {
 lc_status lc_sgd_step_score(lc_ctx *c, int64_t step, const void *const *grads, int32_t grad_dtype,
                             const uint8_t *decay_mask, const lc_sgd_params *p);
 
-/* ---- Persistence store (Section 3.5 "Metadata-driven reconstruction") ------
+/* ---- Persistence store (Section 3.5: reconstruction from persisted metadata) --
  * A directory of version files plus an append-only manifest recording the
  * persistence history: per version its step, its layer mask and its payload
  * (records in the lc_pack_selected format).  A version is visible once its

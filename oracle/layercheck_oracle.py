@@ -2,9 +2,9 @@
 
 Only the tests, the package's smoke check and the benchmark's CPU-baseline leg
 may import this module.  It is a plain, slow, obviously-correct restatement
-of the paper's method (Section 3.2 "Layer-wise Monitoring and Checkpointing",
-Section 3.3 "Bounding Mixed-Timestamp Staleness", Section 3.5 "Recovery from
-LayerCheck Checkpoints", Equations 1-5 and 8) on host numpy arrays, in fp64.
+of the paper's method (Section 3.2, per-layer drift monitoring and selective
+persistence; Section 3.3, the bound on mixed-timestamp staleness; Section 3.5,
+recovery from the persisted records; Equations 1-5 and 8) on host numpy arrays, in fp64.
 It shares no code with the HIP library and imports nothing from it.
 
 What it computes, in the paper's notation:
@@ -181,8 +181,8 @@ def plan_versions(versions: Sequence[dict], n_layers: int, t_fail: int) -> List[
 
 
 # ----------------------------------------------------------------------------
-# AdamW with drift taken from the update itself (Section 3.4, "Reusing the
-# optimizer update to compute drift").  The paper trains with AdamW
+# AdamW with drift taken from the update itself (Section 3.4 computes the
+# drift inside the optimizer step).  The paper trains with AdamW
 # (Section 4.1) but does not restate it; this follows the published
 # definition (Adam with bias correction, decoupled weight decay):
 #   m <- b1 m + (1 - b1) g ;  v <- b2 v + (1 - b2) g^2
@@ -468,7 +468,7 @@ class LayerCheckOracle:
             self.t_last[layer] = self._pre_t_last[layer]
             self.unpacked.discard(layer)
 
-    # -- Section 3.2 "writes the full layer state" ----------------------------
+    # -- Section 3.2: a persisted layer's record holds all of its state ---------
     def layer_record(self, l: int) -> bytes:
         out = bytearray()
         g = self.by_layer[l]

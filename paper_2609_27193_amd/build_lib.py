@@ -70,20 +70,24 @@ def build(verbose: bool = False, out: str = LIB, defines=(), sanitize: bool = Fa
 
 
 HBM_PROBE = os.path.join(HERE, "lc_hbm_probe")
+PROBE_LIB = os.path.join(HERE, "liblcprobe.so")
 
 
 def build_hbm_probe(verbose: bool = False) -> str:
-    """Compile the stand-alone HBM ceiling probe (``bench.py --ceilings``)."""
-    cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17",
-           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
-           "-o", HBM_PROBE + ".tmp", os.path.join(CSRC, "hbm_probe.hip")]
-    if verbose:
-        print(" ".join(cmd), flush=True)
-    res = subprocess.run(cmd, capture_output=True, text=True)
-    if res.returncode != 0:
-        sys.stderr.write(res.stdout + res.stderr)
-        raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
-    os.replace(HBM_PROBE + ".tmp", HBM_PROBE)
+    """Compile the HBM ceiling probe twice: the stand-alone sweep
+    (``bench.py --ceilings``) and the library that probes arrays the caller
+    holds (``bench.py --placement-ceiling``)."""
+    for out, extra in ((HBM_PROBE, ["-DLC_PROBE_MAIN"]), (PROBE_LIB, ["-fPIC", "-shared"])):
+        cmd = [hipcc(), "--offload-arch=gfx950", "-O3", "-std=c++17", *extra,
+               "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-Wall",
+               "-o", out + ".tmp", os.path.join(CSRC, "hbm_probe.hip")]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        res = subprocess.run(cmd, capture_output=True, text=True)
+        if res.returncode != 0:
+            sys.stderr.write(res.stdout + res.stderr)
+            raise RuntimeError(f"hipcc failed with exit code {res.returncode}")
+        os.replace(out + ".tmp", out)
     return HBM_PROBE
 
 

@@ -1,35 +1,49 @@
 // Practical HBM ceilings of the access patterns the library's kernels use,
-// measured with no arithmetic in the way: read-only, copy (one read and one
-// write stream) and two reads plus one write (the ACCUM score pattern: W and
-// S read, S written).  Same tile as the kernels (256 threads, two 16-byte
-// vectors per thread and stream, so 8 KiB per stream per block, accessed
-// through a buffer resource per tile with the non-temporal, device-scope
-// cache policy) and the same XCD-contiguous block mapping.  The second array
-// starts `skew` bytes into its allocation, so the two streams need not sit
-// at the same offsets of the memory interleave.  Prints one JSON line.
+// measured with no arithmetic in the way:
+//   read1   one array read                    (a bound for any read stream)
+//   read2   two arrays read                   (the SNAPSHOT score: W and S)
+//   copy    one array read, another written   (pack and restore)
+//   r2w1    two arrays read, the second written (the ACCUM score: W, S read, S <- W)
+// Each block moves one tile per stream: `threads` lanes, `vec` 16-byte
+// vectors per lane, all loads issued before any use, accessed through a
+// buffer resource per tile with the non-temporal, device-scope cache policy,
+// and the XCD-contiguous block mapping of the kernels.  The sweep covers
+// vec in {2, 4, 8} and threads in {256, 512}; the arrays can be placed so the
+// streams sit at chosen offsets of the memory interleave:
+//   skew    the second array starts `skew` bytes further into its allocation
+//   offset  both arrays start `offset` bytes past an allocation boundary, so
+//           tiles straddle the boundaries a caller's layout can put them across
+// Prints one JSON line per (pattern, vec, threads) with the best of two
+// rounds of `reps` launches.
 //
-//   lc_hbm_probe [GiB per array, default 16] [skew bytes, default 20480]
+//   lc_hbm_probe [GiB per array, default 16] [skew bytes, default 20480] [offset bytes, default 0]
+//
+// Built a second time as a shared library (without LC_PROBE_MAIN), it
+// exports lc_probe_arrays: the kernels' own tile over arrays the caller
+// already holds, so a kernel's rate can be set against the ceiling of the
+// same placement.
 #include <hip/hip_runtime.h>
 
+#include <cstdint>
 #include <cstdio>
 #include <cstdlib>
 
 namespace {
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
-constexpr int kThreads = 256;
-constexpr int kVec = 2;
-constexpr unsigned kTile = kThreads * kVec * 16;  // 8 KiB
-constexpr int kPolicy = 2 | 16;                   // nt | sc1
+constexpr int kPolicy = 2 | 16;  // nt | sc1
 
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile(const u32x4* base, size_t t) {
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<u32x4*>(base) + t * kThreads * kVec, 0, kTile, 0x00020000);
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t tile(const char* base, size_t t, unsigned bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(base) + t * bytes, 0, static_cast<int>(bytes),
+                                           0x00020000);
 }
+template <int NT>
 __device__ __forceinline__ u32x4 ld(__amdgpu_buffer_rsrc_t r, int k) {
-  return __builtin_amdgcn_raw_buffer_load_b128(r, (threadIdx.x + k * kThreads) * 16, 0, kPolicy);
+  return __builtin_amdgcn_raw_buffer_load_b128(r, (threadIdx.x + k * NT) * 16, 0, kPolicy);
 }
+template <int NT>
 __device__ __forceinline__ void st(__amdgpu_buffer_rsrc_t r, int k, u32x4 v) {
-  __builtin_amdgcn_raw_buffer_store_b128(v, r, (threadIdx.x + k * kThreads) * 16, 0, kPolicy);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, (threadIdx.x + k * NT) * 16, 0, kPolicy);
 }
 
 #define CK(x)                                                                  \
@@ -48,96 +62,157 @@ __device__ __forceinline__ size_t tile_of(unsigned x, unsigned G) {
   return x < full ? static_cast<size_t>(x % 8u) * (full / 8u) + x / 8u : x;
 }
 
-__global__ __launch_bounds__(kThreads) void read_only(const u32x4* a, unsigned* sink) {
-  const auto ra = tile(a, tile_of(blockIdx.x, gridDim.x));
-  unsigned acc = 0;
-  u32x4 v[kVec];
-#pragma unroll
-  for (int k = 0; k < kVec; ++k) v[k] = ld(ra, k);
-#pragma unroll
-  for (int k = 0; k < kVec; ++k) acc ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
-  if (acc == 0x9e3779b9u) sink[threadIdx.x] = acc;  // keeps the loads; the pattern never occurs
-}
-
-__global__ __launch_bounds__(kThreads) void copy(const u32x4* a, u32x4* b) {
+// PAT: 0 read1, 1 read2, 2 copy, 3 r2w1.  The xor into `sink` under a
+// condition that never holds keeps the loads of the read patterns.
+template <int PAT, int VEC, int NT>
+__global__ __launch_bounds__(NT) void probe(const char* a, char* b, unsigned* sink) {
+  constexpr unsigned kTile = NT * VEC * 16;
   const size_t t = tile_of(blockIdx.x, gridDim.x);
-  const auto ra = tile(a, t), rb = tile(b, t);
-  u32x4 v[kVec];
+  const auto ra = tile(a, t, kTile), rb = tile(b, t, kTile);
+  u32x4 v[VEC], w[VEC];
 #pragma unroll
-  for (int k = 0; k < kVec; ++k) v[k] = ld(ra, k);
-#pragma unroll
-  for (int k = 0; k < kVec; ++k) st(rb, k, v[k]);
-}
-
-__global__ __launch_bounds__(kThreads) void read2_write1(const u32x4* a, u32x4* b, unsigned* sink) {
-  const size_t t = tile_of(blockIdx.x, gridDim.x);
-  const auto ra = tile(a, t), rb = tile(b, t);
-  u32x4 v[kVec], w[kVec];
-  unsigned acc = 0;
-#pragma unroll
-  for (int k = 0; k < kVec; ++k) {
-    v[k] = ld(ra, k);
-    w[k] = ld(rb, k);
+  for (int k = 0; k < VEC; ++k) {
+    v[k] = ld<NT>(ra, k);
+    if constexpr (PAT == 1 || PAT == 3) w[k] = ld<NT>(rb, k);
   }
+  unsigned acc = 0;
 #pragma unroll
-  for (int k = 0; k < kVec; ++k) {
-    acc += w[k].x ^ v[k].y;
-    st(rb, k, v[k]);
+  for (int k = 0; k < VEC; ++k) {
+    if constexpr (PAT == 2 || PAT == 3) st<NT>(rb, k, v[k]);
+    acc ^= v[k].x ^ v[k].w;
+    if constexpr (PAT == 1 || PAT == 3) acc += w[k].y;
   }
   if (acc == 0x9e3779b9u) sink[threadIdx.x] = acc;
 }
 
 template <typename F>
-float mean_ms(F launch, int reps) {
+double best_ms(F launch, int reps) {
   hipEvent_t e0, e1;
   CK(hipEventCreate(&e0));
   CK(hipEventCreate(&e1));
   launch();
   CK(hipDeviceSynchronize());
-  CK(hipEventRecord(e0));
-  for (int i = 0; i < reps; ++i) launch();
-  CK(hipEventRecord(e1));
-  CK(hipEventSynchronize(e1));
-  float ms = 0.f;
-  CK(hipEventElapsedTime(&ms, e0, e1));
+  double best = 1e30;
+  for (int round = 0; round < 2; ++round) {
+    CK(hipEventRecord(e0));
+    for (int i = 0; i < reps; ++i) launch();
+    CK(hipEventRecord(e1));
+    CK(hipEventSynchronize(e1));
+    float ms = 0.f;
+    CK(hipEventElapsedTime(&ms, e0, e1));
+    if (ms / reps < best) best = ms / reps;
+  }
   CK(hipEventDestroy(e0));
   CK(hipEventDestroy(e1));
-  return ms / reps;
+  return best;
+}
+
+const char* const kNames[4] = {"read1", "read2", "copy", "r2w1"};
+const int kStreams[4] = {1, 2, 2, 3};
+
+template <int PAT, int VEC, int NT>
+void run(const char* a, char* b, unsigned* sink, size_t bytes, long skew, long offset) {
+  constexpr unsigned kTile = NT * VEC * 16;
+  const unsigned grid = static_cast<unsigned>(bytes / kTile);
+  const double ms = best_ms([&] { hipLaunchKernelGGL((probe<PAT, VEC, NT>), dim3(grid), dim3(NT), 0, 0, a, b, sink); },
+                            8);
+  CK(hipGetLastError());
+  std::printf("{\"pattern\": \"%s\", \"vec\": %d, \"threads\": %d, \"tile_bytes\": %u, \"bytes_per_array\": %zu, "
+              "\"skew\": %ld, \"offset\": %ld, \"gbs\": %.1f}\n",
+              kNames[PAT], VEC, NT, kTile, bytes, skew, offset, kStreams[PAT] * static_cast<double>(bytes) / ms / 1e6);
+  std::fflush(stdout);
+}
+
+template <int PAT>
+void sweep(const char* a, char* b, unsigned* sink, size_t bytes, long skew, long offset) {
+  run<PAT, 2, 256>(a, b, sink, bytes, skew, offset);
+  run<PAT, 4, 256>(a, b, sink, bytes, skew, offset);
+  run<PAT, 8, 256>(a, b, sink, bytes, skew, offset);
+  run<PAT, 2, 512>(a, b, sink, bytes, skew, offset);
+  run<PAT, 4, 512>(a, b, sink, bytes, skew, offset);
 }
 
 }  // namespace
 
+// Rate in GB/s of `pattern` (0 read1, 1 read2, 2 copy, 3 r2w1) with the
+// kernels' tile (2 vectors x 256 lanes, 8 KiB per stream) over the first
+// bytes - bytes % 8 KiB of `a` and `b` (device memory the caller owns; b is
+// written by copy and r2w1, with a's bytes), on the null stream; the best of
+// two rounds of `reps` launches.  Returns 0, or -1 for bad arguments or a
+// HIP error (nothing is launched for bad arguments).
+extern "C" int lc_probe_arrays(int pattern, const void* a, void* b, uint64_t bytes, int reps, double* gbs_out) {
+  constexpr unsigned kTile = 256 * 2 * 16;
+  const uint64_t tiles = bytes / kTile;
+  if (!a || !b || !gbs_out || pattern < 0 || pattern > 3 || reps < 1 || tiles == 0 || tiles > 0xFFFFFFFFull / 256)
+    return -1;
+  unsigned* sink = nullptr;
+  if (hipMalloc(&sink, 256 * sizeof(unsigned)) != hipSuccess) return -1;
+  const char* pa = static_cast<const char*>(a);
+  char* pb = static_cast<char*>(b);
+  const dim3 grid(static_cast<unsigned>(tiles)), block(256);
+  hipEvent_t e0, e1;
+  if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return -1;
+  auto launch = [&] {
+    switch (pattern) {
+      case 0: hipLaunchKernelGGL((probe<0, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
+      case 1: hipLaunchKernelGGL((probe<1, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
+      case 2: hipLaunchKernelGGL((probe<2, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
+      default: hipLaunchKernelGGL((probe<3, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
+    }
+  };
+  launch();
+  double best = 1e30;
+  bool ok = hipDeviceSynchronize() == hipSuccess;
+  for (int round = 0; ok && round < 2; ++round) {
+    ok = hipEventRecord(e0) == hipSuccess;
+    for (int i = 0; ok && i < reps; ++i) launch();
+    ok = ok && hipEventRecord(e1) == hipSuccess && hipEventSynchronize(e1) == hipSuccess;
+    float ms = 0.f;
+    ok = ok && hipEventElapsedTime(&ms, e0, e1) == hipSuccess;
+    if (ok && ms / reps < best) best = ms / reps;
+  }
+  ok = ok && hipGetLastError() == hipSuccess;
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  (void)hipFree(sink);
+  if (!ok) return -1;
+  *gbs_out = kStreams[pattern] * static_cast<double>(tiles * kTile) / best / 1e6;
+  return 0;
+}
+
+#ifdef LC_PROBE_MAIN
 int main(int argc, char** argv) {
   const long gib = argc > 1 ? std::atol(argv[1]) : 16;
   const long skew = argc > 2 ? std::atol(argv[2]) : 20480;
-  if (gib < 1 || gib > 64 || skew < 0 || skew > (1l << 30) || skew % 16) {
-    std::fprintf(stderr, "lc_hbm_probe: GiB per array in [1, 64]; skew a multiple of 16 in [0, 1 GiB]\n");
+  const long offset = argc > 3 ? std::atol(argv[3]) : 0;
+  if (gib < 1 || gib > 64 || skew < 0 || skew > (1l << 30) || skew % 16 || offset < 0 || offset > (1l << 21) ||
+      offset % 16) {
+    std::fprintf(stderr, "lc_hbm_probe: GiB per array in [1, 64]; skew a multiple of 16 in [0, 1 GiB]; "
+                         "offset a multiple of 16 in [0, 2 MiB]\n");
     return 2;
   }
+  // every tile of every sweep lies inside [0, bytes) of each array: bytes is a
+  // multiple of the largest tile (64 KiB), and each allocation holds
+  // offset (+ skew) + bytes
   const size_t bytes = static_cast<size_t>(gib) << 30;
-  const size_t tiles = bytes / kTile;  // exact: GiB multiple
-  if (tiles > 0xFFFFFFFFull) return 2;
-  const unsigned grid = static_cast<unsigned>(tiles);
-  u32x4 *a = nullptr, *b0 = nullptr, *b = nullptr;
+  if (bytes / (256 * 2 * 16) > 0xFFFFFFFFull) return 2;
+  char *a0 = nullptr, *b0 = nullptr;
   unsigned* sink = nullptr;
-  CK(hipMalloc(&a, bytes));
-  CK(hipMalloc(&b0, bytes + skew));
-  b = reinterpret_cast<u32x4*>(reinterpret_cast<char*>(b0) + skew);
-  CK(hipMalloc(&sink, kThreads * sizeof(unsigned)));
-  CK(hipMemset(a, 1, bytes));
-  CK(hipMemset(b, 2, bytes));
+  CK(hipMalloc(&a0, bytes + offset));
+  CK(hipMalloc(&b0, bytes + offset + skew));
+  char* a = a0 + offset;
+  char* b = b0 + offset + skew;
+  CK(hipMalloc(&sink, 512 * sizeof(unsigned)));
+  CK(hipMemset(a0, 1, bytes + offset));
+  CK(hipMemset(b0, 2, bytes + offset + skew));
   CK(hipDeviceSynchronize());
-  const int reps = 10;
-  const double r = mean_ms([&] { hipLaunchKernelGGL(read_only, dim3(grid), dim3(kThreads), 0, 0, a, sink); }, reps);
-  const double c = mean_ms([&] { hipLaunchKernelGGL(copy, dim3(grid), dim3(kThreads), 0, 0, a, b); }, reps);
-  const double w = mean_ms([&] { hipLaunchKernelGGL(read2_write1, dim3(grid), dim3(kThreads), 0, 0, a, b, sink); },
-                           reps);
-  CK(hipGetLastError());
-  std::printf("{\"bytes_per_array\": %zu, \"skew\": %ld, \"read_gbs\": %.1f, \"copy_gbs\": %.1f, "
-              "\"read2_write1_gbs\": %.1f}\n",
-              bytes, skew, bytes / r / 1e6, 2.0 * bytes / c / 1e6, 3.0 * bytes / w / 1e6);
-  CK(hipFree(a));
+  sweep<0>(a, b, sink, bytes, skew, offset);
+  sweep<1>(a, b, sink, bytes, skew, offset);
+  sweep<2>(a, b, sink, bytes, skew, offset);
+  sweep<3>(a, b, sink, bytes, skew, offset);
+  CK(hipFree(a0));
   CK(hipFree(b0));
   CK(hipFree(sink));
   return 0;
 }
+#endif  // LC_PROBE_MAIN
