@@ -17,6 +17,7 @@
 // rounds of `reps` launches.
 //
 //   lc_hbm_probe [GiB per array, default 16] [skew bytes, default 20480] [offset bytes, default 0]
+//   lc_hbm_probe empty     (dispatch cost of blocks that find no work)
 //
 // Built a second time as a shared library (without LC_PROBE_MAIN), it
 // exports lc_probe_arrays: the kernels' own tile over arrays the caller
@@ -27,6 +28,7 @@
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
+#include <string>
 
 namespace {
 
@@ -83,6 +85,13 @@ __global__ __launch_bounds__(NT) void probe(const char* a, char* b, unsigned* si
     if constexpr (PAT == 1 || PAT == 3) acc += w[k].y;
   }
   if (acc == 0x9e3779b9u) sink[threadIdx.x] = acc;
+}
+
+// Every block reads the amount of work from device memory and finds none:
+// the cost of dispatching blocks that exit at once (a grid sized for the
+// worst case whose work is decided on the device).
+__global__ __launch_bounds__(256) void empty_blocks(const unsigned* n_work, unsigned* sink) {
+  if (blockIdx.x < *n_work) sink[threadIdx.x] = blockIdx.x;
 }
 
 template <typename F>
@@ -182,6 +191,21 @@ extern "C" int lc_probe_arrays(int pattern, const void* a, void* b, uint64_t byt
 
 #ifdef LC_PROBE_MAIN
 int main(int argc, char** argv) {
+  if (argc > 1 && std::string(argv[1]) == "empty") {
+    unsigned *n_work = nullptr, *sink = nullptr;
+    CK(hipMalloc(&n_work, sizeof(unsigned)));
+    CK(hipMalloc(&sink, 256 * sizeof(unsigned)));
+    CK(hipMemset(n_work, 0, sizeof(unsigned)));
+    for (unsigned grid : {1u << 16, 1u << 20, 1u << 22, 14u << 20}) {  // 14 M blocks: the 8B worst-case pack
+      const double ms = best_ms([&] { hipLaunchKernelGGL(empty_blocks, dim3(grid), dim3(256), 0, 0, n_work, sink); }, 8);
+      CK(hipGetLastError());
+      std::printf("{\"pattern\": \"empty\", \"blocks\": %u, \"threads\": 256, \"us\": %.1f}\n", grid, ms * 1e3);
+      std::fflush(stdout);
+    }
+    CK(hipFree(n_work));
+    CK(hipFree(sink));
+    return 0;
+  }
   const long gib = argc > 1 ? std::atol(argv[1]) : 16;
   const long skew = argc > 2 ? std::atol(argv[2]) : 20480;
   const long offset = argc > 3 ? std::atol(argv[3]) : 0;

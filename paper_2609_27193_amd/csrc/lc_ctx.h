@@ -65,7 +65,8 @@ struct lc_ctx {
   hipStream_t stream = nullptr;
   DeviceTables dt{};
   std::vector<void*> allocations;
-  SelectHeader* h_result = nullptr;  // pinned: header + mask[N]
+  SelectHeader* h_result = nullptr;  // pinned, coherent: header + mask[N], written by the select kernel
+  uint64_t result_seq = 0;           // sequence number of the last select kernel enqueued
   GradSeg* h_grad = nullptr;         // pinned: per-call gradient table
   GradSeg* d_grad = nullptr;
   hipEvent_t grad_event = nullptr;   // marks the upload of h_grad

@@ -89,8 +89,10 @@ struct SgdScalars {
   float lr, decay;
 };
 
-// Written by the select kernel, copied to pinned host memory, followed by the
-// 0/1 mask of n_layers bytes.
+// Written by the select kernel to device memory and to a pinned host mirror,
+// followed by the 0/1 mask of n_layers bytes.  In the mirror `seq` is written
+// last, after a system-scope fence: the host waits for the number it passed
+// to the kernel instead of synchronising the stream.
 struct SelectHeader {
   uint32_t n_selected;
   uint32_t n_forced;
@@ -99,7 +101,8 @@ struct SelectHeader {
   double weighted_age;
   uint64_t total_pieces;
   uint64_t age_numerator;
-  uint64_t reserved[2];
+  uint64_t seq;
+  uint64_t reserved;
 };
 static_assert(sizeof(SelectHeader) == 64, "header layout");
 
@@ -130,6 +133,7 @@ struct DeviceTables {
   uint64_t* sel_rec_prefix;           // [N+1] record byte offsets by rank
   uint64_t* sel_piece_prefix;         // [N+1] piece offsets by rank
   SelectHeader* result;               // header + mask[N]
+  SelectHeader* host_result;          // pinned host mirror of result (device address)
   const OptSeg* opt_segs;             // [n_segments]
   const GradSeg* grad_segs;           // [n_segments], refreshed per optimizer call
   // restore scratch
@@ -143,7 +147,7 @@ struct DeviceTables {
 hipError_t launch_score(const DeviceTables& t, hipStream_t st);
 // Eq. 1-2 from the per-chunk partials alone (after an optimizer step).
 hipError_t launch_finalize(const DeviceTables& t, hipStream_t st);
-hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode,
+hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode, uint64_t seq,
                          hipStream_t st);
 hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last_rank,
                        uint64_t piece_base, uint64_t n_pieces, uint64_t rec_base,

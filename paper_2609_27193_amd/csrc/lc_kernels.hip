@@ -184,7 +184,7 @@ __global__ __launch_bounds__(kFinalizeThreads) void finalize_kernel(const Device
 
 // ---- select: Eq. 3-5, reset, staleness stats, pack plan ------------------------
 __global__ __launch_bounds__(kSelectThreads) void select_kernel(const DeviceTables t, int64_t step,
-                                                                double lr_scale, int base_mode) {
+                                                                double lr_scale, int base_mode, uint64_t seq) {
   uint8_t* mask = reinterpret_cast<uint8_t*>(t.result + 1);
   const uint32_t N = t.n_layers;
   for (uint32_t l = threadIdx.x; l < N; l += kSelectThreads) {
@@ -235,8 +235,22 @@ __global__ __launch_bounds__(kSelectThreads) void select_kernel(const DeviceTabl
     h.weighted_age = static_cast<double>(num) / static_cast<double>(den);
     h.total_pieces = pieces;
     h.age_numerator = num;
-    h.reserved[0] = h.reserved[1] = 0;
+    h.seq = 0;
+    h.reserved = 0;
     *t.result = h;
+    // The host's copy, read with no device-to-host copy and no stream
+    // synchronisation: the mask, then the header with seq = 0, then -- once a
+    // system-scope fence has made those visible -- the number the host waits
+    // for.
+    SelectHeader* hr = t.host_result;
+    const uint32_t* m32 = reinterpret_cast<const uint32_t*>(mask);
+    uint32_t* h32 = reinterpret_cast<uint32_t*>(hr + 1);
+    for (uint32_t w = 0; w < N / 4; ++w) h32[w] = m32[w];
+    uint8_t* h8 = reinterpret_cast<uint8_t*>(hr + 1);
+    for (uint32_t l = N & ~3u; l < N; ++l) h8[l] = mask[l];
+    *hr = h;
+    __threadfence_system();
+    hr->seq = seq;
   }
 }
 
@@ -394,9 +408,9 @@ hipError_t launch_finalize(const DeviceTables& t, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode,
+hipError_t launch_select(const DeviceTables& t, int64_t step, double lr_scale, int base_mode, uint64_t seq,
                          hipStream_t st) {
-  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelectThreads), 0, st, t, step, lr_scale, base_mode);
+  hipLaunchKernelGGL(select_kernel, dim3(1), dim3(kSelectThreads), 0, st, t, step, lr_scale, base_mode, seq);
   return hipGetLastError();
 }
 

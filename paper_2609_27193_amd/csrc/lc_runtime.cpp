@@ -4,6 +4,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
@@ -247,10 +248,39 @@ lc_status check_ctx(lc_ctx* c) {
   return LC_OK;
 }
 
+// Wait until the select kernel has written the pending selection into the
+// pinned host mirror (its sequence number appears last, after a system-scope
+// fence).  The flag is polled, so the host reacts within a microsecond or two
+// of the kernel's store instead of after a device-to-host copy and a stream
+// synchronisation; every 256 polls the stream is queried, so an error or a
+// stream that drained without the flag ends the wait.
+lc_status wait_result(lc_ctx* c) {
+  const volatile uint64_t* flag = &c->h_result->seq;
+  for (uint32_t spin = 1;; ++spin) {
+    if (*flag == c->result_seq) break;
+    if (spin % 256 == 0) {
+      const hipError_t q = hipStreamQuery(c->stream);
+      if (q == hipSuccess) {
+        if (*flag == c->result_seq) break;
+        c->poisoned = true;
+        return fail(LC_ERR_HIP, "the selection never reached the host");
+      }
+      if (q != hipErrorNotReady) {
+        (void)hipGetLastError();
+        c->poisoned = true;
+        return fail(LC_ERR_HIP, "waiting for the selection failed: %s", hipGetErrorString(q));
+      }
+    }
+  }
+  std::atomic_thread_fence(std::memory_order_acquire);
+  return LC_OK;
+}
+
 // Make the pending selection's mask available on the host.
 lc_status fetch_result(lc_ctx* c) {
   if (c->result_on_host) return LC_OK;
-  LC_HIP(c, hipStreamSynchronize(c->stream));
+  lc_status st = wait_result(c);
+  if (st != LC_OK) return st;
   const uint32_t N = c->L.N;
   const uint8_t* mask = reinterpret_cast<const uint8_t*>(c->h_result + 1);
   c->sel.clear();
@@ -279,9 +309,8 @@ lc_status fetch_result(lc_ctx* c) {
 }
 
 lc_status enqueue_select(lc_ctx* c, int64_t step, double lr, int base_mode, bool persists) {
-  LC_HIP(c, launch_select(c->dt, step, lr, base_mode, c->stream));
-  LC_HIP(c, hipMemcpyAsync(c->h_result, c->dt.result, sizeof(SelectHeader) + c->L.N,
-                           hipMemcpyDeviceToHost, c->stream));
+  ++c->result_seq;
+  LC_HIP(c, launch_select(c->dt, step, lr, base_mode, c->result_seq, c->stream));
   c->have_selection = true;
   c->pending = true;
   c->pending_persists = persists;
@@ -482,13 +511,23 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
   LC_TRY(dev_alloc(c, &rank_src, N));
   LC_TRY(dev_alloc(c, &rpp, N + 1));
   {
+    // the select kernel writes this mirror itself: coherent (fine-grained)
+    // pinned memory, so its stores reach the host without a copy
     void* h = nullptr;
-    hipError_t e = hipHostMalloc(&h, sizeof(SelectHeader) + N, hipHostMallocDefault);
+    hipError_t e = hipHostMalloc(&h, sizeof(SelectHeader) + N, hipHostMallocCoherent);
     if (e != hipSuccess) {
       (void)hipGetLastError();
       return bail(fail(LC_ERR_OOM, "hipHostMalloc failed: %s", hipGetErrorString(e)));
     }
     c->h_result = static_cast<SelectHeader*>(h);
+    std::memset(h, 0, sizeof(SelectHeader) + N);
+    void* dh = nullptr;
+    e = hipHostGetDevicePointer(&dh, h, 0);
+    if (e != hipSuccess) {
+      (void)hipGetLastError();
+      return bail(fail(LC_ERR_HIP, "hipHostGetDevicePointer failed: %s", hipGetErrorString(e)));
+    }
+    t.host_result = static_cast<SelectHeader*>(dh);
     h = nullptr;
     e = hipHostMalloc(&h, sizeof(GradSeg) * L.opt_segs.size(), hipHostMallocDefault);
     if (e != hipSuccess) {
