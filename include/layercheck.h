@@ -171,9 +171,9 @@ lc_status lc_init_layout(const lc_layout_desc *d, lc_ctx **out);
  * the staleness bound of Section 3.3).  The base that lc_init_layout leaves
  * pending resets nothing: in ACCUM mode a warm-up may leave it unpacked
  * (this call then drops it); SNAPSHOT mode needs it packed first.
- * Synchronises the stream only when it must read back whether the previous
- * selection is packed (a selection whose mask never reached the host);
- * otherwise asynchronous. */
+ * Waits for the previous select kernel only when it must learn whether that
+ * selection is packed (a selection whose mask was never read); otherwise
+ * asynchronous. */
 lc_status lc_score_layers(lc_ctx *c, int64_t step);
 
 /* For callers that cannot allocate device memory (code under HIP graph
@@ -210,8 +210,9 @@ lc_status lc_score_layers_static(const lc_segment *segments, uint32_t n_segments
  * layer gets Delta_l = 0 and t_l = step (Eq. 4), so its record must be packed
  * (lc_pack_selected) before the next score or optimizer step.  Must follow
  * lc_score_layers(step).  Writes the 0/1 mask (host [n_layers]) and stats
- * when the pointers are non-NULL, which synchronises the stream; with both
- * NULL the call is asynchronous. */
+ * when the pointers are non-NULL, which waits for the select kernel (it
+ * writes its result into pinned host memory, which the call polls; no
+ * stream synchronisation); with both NULL the call is asynchronous. */
 lc_status lc_select(lc_ctx *c, int64_t step, double lr_scale, uint8_t *mask_out,
                     lc_select_stats *stats_out);
 
@@ -224,9 +225,9 @@ lc_status lc_select(lc_ctx *c, int64_t step, double lr_scale, uint8_t *mask_out,
  * bytes.  Records are concatenated without gaps.  SNAPSHOT mode also sets
  * S <- W for the packed layers in the same pass.  Returns LC_ERR_CAPACITY if
  * the record at first_rank alone exceeds `capacity`, LC_ERR_INVALID_ARG if
- * `staging` is not device memory with room for the bytes to be written.  Synchronises the stream
- * only when the selection mask is not yet on the host; the copy itself is
- * asynchronous. */
+ * `staging` is not device memory with room for the bytes to be written.  Waits for the
+ * select kernel's result (polled in pinned host memory) when the mask is not
+ * yet on the host; the copy itself is asynchronous. */
 lc_status lc_pack_selected(lc_ctx *c, void *staging, uint64_t capacity, uint32_t first_rank,
                            lc_pack_result *out);
 
