@@ -7,7 +7,9 @@
  * the test compares with the oracle.  Every version is also appended to a
  * persistence store with the overlapped append (a reuse event, the stream
  * never waits), and the composite rebuilt from the store must equal the one
- * rebuilt from the device versions byte for byte.
+ * rebuilt from the device versions byte for byte.  At every step the
+ * allocation-free score (lc_score_layers_static) of the same arrays must
+ * equal the context's u bit for bit.
  *
  *   lc_c_client <input file> <output file> <store directory>
  *
@@ -227,14 +229,22 @@ int main(int argc, char **argv) {
   LC(lc_store_append_async(store, t_base, mask, versions[0].payload, versions[0].bytes, stream, reuse));
 
   double *u = (double *)xmalloc(8 * N), *delta = (double *)xmalloc(8 * N);
+  double *u_static = (double *)xmalloc(8 * N), *d_u_static = NULL;
+  HIP(hipMalloc((void **)&d_u_static, 8 * N));
   int64_t *t_last = (int64_t *)xmalloc(8 * N);
   for (uint32_t k = 1; k <= n_steps; ++k) {
     const int64_t t = t_base + k;
     LOAD_STATE();
+    /* the allocation-free score of the same weights and shadow, before the
+     * context's pass (which refreshes the shadow in ACCUM mode): the same u,
+     * bit for bit */
+    LC(lc_score_layers_static(segs, S, N, (int32_t)dtype, eps_w, d_u_static, stream));
+    HIP(hipMemcpy(u_static, d_u_static, 8 * N, hipMemcpyDeviceToHost));
     LC(lc_score_layers(c, t));
     lc_select_stats st;
     LC(lc_select(c, t, lr_scale[k], mask, &st));
     LC(lc_read_state(c, u, delta, t_last));
+    if (memcmp(u, u_static, 8 * N) != 0) die("lc_score_layers_static disagrees with lc_score_layers");
     wr(u, 8 * N);
     wr(delta, 8 * N);
     wr(t_last, 8 * N);
@@ -315,6 +325,8 @@ int main(int argc, char **argv) {
     if (versions[k].payload) HIP(hipFree(versions[k].payload));
     free(versions[k].mask);
   }
+  HIP(hipFree(d_u_static));
+  free(u_static);
   HIP(hipFree(dW));
   HIP(hipFree(dS));
   if (dM) HIP(hipFree(dM));
