@@ -26,7 +26,10 @@
 // The allocation-free path's device memory, one copy per GPU for the life of
 // the process.  Host code never uses this name as an address: it is a
 // host-side stand-in there.  Each device's address comes from
-// hipGetSymbolAddress (scratch_base below).
+// hipGetSymbolAddress (scratch_base below).  Nothing in it has to start at
+// zero: every call uploads or writes every table entry its kernels read
+// (segment table, per-layer counts, chunk table, one partial per chunk)
+// before they read it, whatever an earlier call left there.
 static __device__ __align__(256) uint8_t scratch[LC_NOALLOC_SCRATCH_BYTES];
 
 using namespace lc;
