@@ -242,6 +242,10 @@ def cpu_baseline(state, spec, mode_name, sel_fraction, n_blocks=16):
                       f"{len(os.sched_getaffinity(0))} cores visible"}
 
 
+# Blocks per CU at which the probe times each pattern (0: as many as fit).
+PROBE_BLOCKS_PER_CU = (0, 2, 3, 4, 6)
+
+
 def placement_ceiling(state, staging, mode_name, score_gbs, pack_gbs, sweep=False):
     """The access patterns of the score and pack kernels with no arithmetic
     (the kernels' tile and block mapping, from the probe library) over the
@@ -258,38 +262,49 @@ def placement_ceiling(state, staging, mode_name, score_gbs, pack_gbs, sweep=Fals
         return None
     lib = C.CDLL(PROBE_LIB)
     lib.lc_probe_arrays.restype = C.c_int
-    lib.lc_probe_arrays.argtypes = [C.c_int, C.c_void_p, C.c_void_p, C.c_uint64, C.c_int, C.POINTER(C.c_double)]
+    lib.lc_probe_arrays.argtypes = [C.c_int, C.c_void_p, C.c_void_p, C.c_uint64, C.c_int, C.c_int,
+                                    C.POINTER(C.c_double)]
     torch.cuda.synchronize()
 
-    def rate(pattern, a, b, nbytes):
+    def rate(pattern, a, b, nbytes, blocks_per_cu=0):
         g = C.c_double()
-        if lib.lc_probe_arrays(pattern, a, b, nbytes, 8, C.byref(g)) != 0:
+        if lib.lc_probe_arrays(pattern, a, b, nbytes, 8, blocks_per_cu, C.byref(g)) != 0:
             raise RuntimeError("lc_probe_arrays failed")
         return g.value
 
+    def best(pattern, a, b, nbytes):
+        """The pattern at each number of blocks per CU (0: as many as fit);
+        the ceiling is the best of them."""
+        by_k = {k: round(rate(pattern, a, b, nbytes, k), 1) for k in PROBE_BLOCKS_PER_CU}
+        k = max(by_k, key=by_k.get)
+        return by_k[k], k, by_k
+
     w_bytes = state.weight.numel() * state.weight.element_size()
     score_pattern = 3 if mode_name == "accum" else 1
-    ceil_score = rate(score_pattern, state.weight.data_ptr(), state.shadow.data_ptr(), w_bytes)
+    ceil_score, k_score, score_by_k = best(score_pattern, state.weight.data_ptr(), state.shadow.data_ptr(), w_bytes)
     src = state.master if state.master is not None else state.exp_avg
     n = min(src.numel() * 4, staging.numel())
-    ceil_copy = rate(2, src.data_ptr(), staging.data_ptr(), n)
+    ceil_copy, k_copy, copy_by_k = best(2, src.data_ptr(), staging.data_ptr(), n)
     out = {"score_pattern": "r2w1" if score_pattern == 3 else "read2", "score_gbs": round(ceil_score, 1),
            "score_kernel_frac": round(float(score_gbs) / ceil_score, 4), "copy_gbs": round(ceil_copy, 1),
-           "copy_bytes": n}
+           "copy_bytes": n, "score_gbs_by_blocks_per_cu": score_by_k, "copy_gbs_by_blocks_per_cu": copy_by_k}
     if pack_gbs:
         out["pack_kernel_frac"] = round(float(pack_gbs) / ceil_copy, 4)
     if sweep:
         # the shadow (or both arrays) entered `off` bytes later: tiles then pair
         # W and S at other relative positions of the interleave
+        # (each at the number of blocks per CU that gave the ceiling above)
         offs = (0, 256, 1024, 4096, 8192, 20480, 65536, 1 << 20)
         out["score_vs_shadow_offset"] = {
-            o: round(rate(score_pattern, state.weight.data_ptr(), state.shadow.data_ptr() + o, w_bytes - (1 << 20)), 1)
+            o: round(rate(score_pattern, state.weight.data_ptr(), state.shadow.data_ptr() + o, w_bytes - (1 << 20),
+                          k_score), 1)
             for o in offs}
         out["score_vs_both_offset"] = {
-            o: round(rate(score_pattern, state.weight.data_ptr() + o, state.shadow.data_ptr() + o, w_bytes - (1 << 20)), 1)
+            o: round(rate(score_pattern, state.weight.data_ptr() + o, state.shadow.data_ptr() + o, w_bytes - (1 << 20),
+                          k_score), 1)
             for o in offs}
         out["copy_vs_staging_offset"] = {
-            o: round(rate(2, src.data_ptr(), staging.data_ptr() + o, n - (1 << 20)), 1) for o in offs}
+            o: round(rate(2, src.data_ptr(), staging.data_ptr() + o, n - (1 << 20), k_copy), 1) for o in offs}
         if score_pattern == 3:  # the shifted r2w1 runs wrote W's bytes into S at an offset: S <- W again
             state.shadow.copy_(state.weight)
             torch.cuda.synchronize()

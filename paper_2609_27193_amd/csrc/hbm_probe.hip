@@ -8,8 +8,10 @@
 // vectors per lane, all loads issued before any use, accessed through a
 // buffer resource per tile with the non-temporal, device-scope cache policy,
 // and the XCD-contiguous block mapping of the kernels.  The sweep covers
-// vec in {2, 4, 8} and threads in {256, 512}; the arrays can be placed so the
-// streams sit at chosen offsets of the memory interleave:
+// vec in {2, 4, 8} and threads in {256, 512}, and for the kernels' tile
+// (2 x 256) the number of blocks a CU may hold at once (an LDS reservation
+// the kernel never touches: 2, 3, 4, 6, or as many as fit); the arrays can
+// be placed so the streams sit at chosen offsets of the memory interleave:
 //   skew    the second array starts `skew` bytes further into its allocation
 //   offset  both arrays start `offset` bytes past an allocation boundary, so
 //           tiles straddle the boundaries a caller's layout can put them across
@@ -21,8 +23,8 @@
 //
 // Built a second time as a shared library (without LC_PROBE_MAIN), it
 // exports lc_probe_arrays: the kernels' own tile over arrays the caller
-// already holds, so a kernel's rate can be set against the ceiling of the
-// same placement.
+// already holds, at a chosen number of blocks per CU, so a kernel's rate can
+// be set against the ceiling of the same placement.
 #include <hip/hip_runtime.h>
 
 #include <cstdint>
@@ -62,6 +64,20 @@ __device__ __forceinline__ void st(__amdgpu_buffer_rsrc_t r, int k, u32x4 v) {
 __device__ __forceinline__ size_t tile_of(unsigned x, unsigned G) {
   const unsigned full = G - G % 8u;
   return x < full ? static_cast<size_t>(x % 8u) * (full / 8u) + x / 8u : x;
+}
+
+// Dynamic LDS per block that leaves room for at most k blocks on a CU (0 for
+// k = 0, or when the device's limits leave no such size): more than
+// L / (k + 1) of the CU's L bytes, and at most L / k.
+unsigned lds_for(int k) {
+  if (k <= 0) return 0;
+  int dev = 0, cu = 0, blk = 0;
+  if (hipGetDevice(&dev) != hipSuccess ||
+      hipDeviceGetAttribute(&cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess ||
+      hipDeviceGetAttribute(&blk, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess || cu <= 0)
+    return 0;
+  const long want = (cu / (k + 1) + 2048 + 511) / 512 * 512;
+  return (want > cu / k - 1024 || want > blk) ? 0 : static_cast<unsigned>(want);
 }
 
 // PAT: 0 read1, 1 read2, 2 copy, 3 r2w1.  The xor into `sink` under a
@@ -120,21 +136,23 @@ const char* const kNames[4] = {"read1", "read2", "copy", "r2w1"};
 const int kStreams[4] = {1, 2, 2, 3};
 
 template <int PAT, int VEC, int NT>
-void run(const char* a, char* b, unsigned* sink, size_t bytes, long skew, long offset) {
+void run(const char* a, char* b, unsigned* sink, size_t bytes, long skew, long offset, int blocks_per_cu = 0) {
   constexpr unsigned kTile = NT * VEC * 16;
   const unsigned grid = static_cast<unsigned>(bytes / kTile);
-  const double ms = best_ms([&] { hipLaunchKernelGGL((probe<PAT, VEC, NT>), dim3(grid), dim3(NT), 0, 0, a, b, sink); },
-                            8);
+  const unsigned lds = lds_for(blocks_per_cu);
+  const double ms = best_ms(
+      [&] { hipLaunchKernelGGL((probe<PAT, VEC, NT>), dim3(grid), dim3(NT), lds, 0, a, b, sink); }, 8);
   CK(hipGetLastError());
   std::printf("{\"pattern\": \"%s\", \"vec\": %d, \"threads\": %d, \"tile_bytes\": %u, \"bytes_per_array\": %zu, "
-              "\"skew\": %ld, \"offset\": %ld, \"gbs\": %.1f}\n",
-              kNames[PAT], VEC, NT, kTile, bytes, skew, offset, kStreams[PAT] * static_cast<double>(bytes) / ms / 1e6);
+              "\"skew\": %ld, \"offset\": %ld, \"blocks_per_cu\": %d, \"lds\": %u, \"gbs\": %.1f}\n",
+              kNames[PAT], VEC, NT, kTile, bytes, skew, offset, lds ? blocks_per_cu : 0, lds,
+              kStreams[PAT] * static_cast<double>(bytes) / ms / 1e6);
   std::fflush(stdout);
 }
 
 template <int PAT>
 void sweep(const char* a, char* b, unsigned* sink, size_t bytes, long skew, long offset) {
-  run<PAT, 2, 256>(a, b, sink, bytes, skew, offset);
+  for (int k : {0, 2, 3, 4, 6}) run<PAT, 2, 256>(a, b, sink, bytes, skew, offset, k);
   run<PAT, 4, 256>(a, b, sink, bytes, skew, offset);
   run<PAT, 8, 256>(a, b, sink, bytes, skew, offset);
   run<PAT, 2, 512>(a, b, sink, bytes, skew, offset);
@@ -146,14 +164,18 @@ void sweep(const char* a, char* b, unsigned* sink, size_t bytes, long skew, long
 // Rate in GB/s of `pattern` (0 read1, 1 read2, 2 copy, 3 r2w1) with the
 // kernels' tile (2 vectors x 256 lanes, 8 KiB per stream) over the first
 // bytes - bytes % 8 KiB of `a` and `b` (device memory the caller owns; b is
-// written by copy and r2w1, with a's bytes), on the null stream; the best of
-// two rounds of `reps` launches.  Returns 0, or -1 for bad arguments or a
-// HIP error (nothing is launched for bad arguments).
-extern "C" int lc_probe_arrays(int pattern, const void* a, void* b, uint64_t bytes, int reps, double* gbs_out) {
+// written by copy and r2w1, with a's bytes), on the null stream, with at most
+// `blocks_per_cu` blocks per CU (0: as many as fit); the best of two rounds
+// of `reps` launches.  Returns 0, or -1 for bad arguments or a HIP error
+// (nothing is launched for bad arguments).
+extern "C" int lc_probe_arrays(int pattern, const void* a, void* b, uint64_t bytes, int reps, int blocks_per_cu,
+                               double* gbs_out) {
   constexpr unsigned kTile = 256 * 2 * 16;
   const uint64_t tiles = bytes / kTile;
-  if (!a || !b || !gbs_out || pattern < 0 || pattern > 3 || reps < 1 || tiles == 0 || tiles > 0xFFFFFFFFull / 256)
+  if (!a || !b || !gbs_out || pattern < 0 || pattern > 3 || reps < 1 || tiles == 0 || tiles > 0xFFFFFFFFull / 256 ||
+      blocks_per_cu < 0 || blocks_per_cu > 32)
     return -1;
+  const unsigned lds = lds_for(blocks_per_cu);
   unsigned* sink = nullptr;
   if (hipMalloc(&sink, 256 * sizeof(unsigned)) != hipSuccess) return -1;
   const char* pa = static_cast<const char*>(a);
@@ -163,10 +185,10 @@ extern "C" int lc_probe_arrays(int pattern, const void* a, void* b, uint64_t byt
   if (hipEventCreate(&e0) != hipSuccess || hipEventCreate(&e1) != hipSuccess) return -1;
   auto launch = [&] {
     switch (pattern) {
-      case 0: hipLaunchKernelGGL((probe<0, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
-      case 1: hipLaunchKernelGGL((probe<1, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
-      case 2: hipLaunchKernelGGL((probe<2, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
-      default: hipLaunchKernelGGL((probe<3, 2, 256>), grid, block, 0, 0, pa, pb, sink); break;
+      case 0: hipLaunchKernelGGL((probe<0, 2, 256>), grid, block, lds, 0, pa, pb, sink); break;
+      case 1: hipLaunchKernelGGL((probe<1, 2, 256>), grid, block, lds, 0, pa, pb, sink); break;
+      case 2: hipLaunchKernelGGL((probe<2, 2, 256>), grid, block, lds, 0, pa, pb, sink); break;
+      default: hipLaunchKernelGGL((probe<3, 2, 256>), grid, block, lds, 0, pa, pb, sink); break;
     }
   };
   launch();

@@ -40,6 +40,38 @@ constexpr uint32_t kRecordAlign = 256u;
 constexpr uint32_t kFinalizeThreads = 1024;
 constexpr uint32_t kSelectThreads = 256;
 
+// Resident blocks per CU of the streaming kernels (0: as many as registers
+// and waves allow), held there by a dynamic LDS reservation the kernel never
+// touches.  Fewer streams open at once let HBM turn between reads and writes
+// less often; kernels that only read, and kernels whose per-block table
+// lookups need many blocks to hide their latency, want more.  Measured on
+// MI355X, same arrays, one process (GB/s, unreserved -> reserved):
+//   ACCUM score (two reads, one write), 4 per CU: 8B 6425 -> 6688,
+//     70B shard 6230 -> 6324, 13B 6070 -> 6158, Qwen2.5-14B 6414 -> 6574;
+//     2 per CU loses 14%, 3 ties 4 on the larger states;
+//   SNAPSHOT score (two reads): unreserved is best (4 per CU: -2%);
+//   pack and unpack (copies), 6 per CU: +0.2..1.8% (3 per CU: -12%);
+//   fused AdamW, 2 per CU: 5930 -> 6004; fused SGD: no gain at 2..5.
+#ifndef LC_SCORE_ACCUM_BLOCKS_PER_CU
+#define LC_SCORE_ACCUM_BLOCKS_PER_CU 4
+#endif
+#ifndef LC_SCORE_SNAPSHOT_BLOCKS_PER_CU
+#define LC_SCORE_SNAPSHOT_BLOCKS_PER_CU 0
+#endif
+#ifndef LC_COPY_BLOCKS_PER_CU
+#define LC_COPY_BLOCKS_PER_CU 6
+#endif
+#ifndef LC_ADAMW_BLOCKS_PER_CU
+#define LC_ADAMW_BLOCKS_PER_CU 2
+#endif
+#ifndef LC_SGD_BLOCKS_PER_CU
+#define LC_SGD_BLOCKS_PER_CU 0
+#endif
+// Dynamic LDS bytes per block that leave room for at most `blocks_per_cu`
+// blocks on a CU of the current device (0 when blocks_per_cu is 0 or the
+// device's limits leave no such size).
+uint32_t occupancy_lds(uint32_t blocks_per_cu);
+
 // One segment as the score kernel sees it.
 struct ScoreSeg {
   uint64_t w;            // device address of the weights

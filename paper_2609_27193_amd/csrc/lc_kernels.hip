@@ -12,6 +12,8 @@
 //    the cross-wave combine.
 #include "lc_device.h"
 
+#include <atomic>
+
 namespace lc {
 namespace {
 
@@ -370,9 +372,10 @@ __global__ __launch_bounds__(kCopyThreads) void unpack_kernel(const DeviceTables
 // next range of work items; every block does exactly one item.
 template <int DT, bool ACCUM>
 void launch_score_t(const DeviceTables& t, hipStream_t st) {
+  const uint32_t lds = occupancy_lds(ACCUM ? LC_SCORE_ACCUM_BLOCKS_PER_CU : LC_SCORE_SNAPSHOT_BLOCKS_PER_CU);
   for (uint64_t done = 0; done < t.n_chunks;) {
     const uint32_t g = grid_for(t.n_chunks - done, kScoreThreads);
-    hipLaunchKernelGGL((score_kernel<DT, ACCUM>), dim3(g), dim3(kScoreThreads), 0, st, t,
+    hipLaunchKernelGGL((score_kernel<DT, ACCUM>), dim3(g), dim3(kScoreThreads), lds, st, t,
                        static_cast<uint32_t>(done));
     done += g;
   }
@@ -381,15 +384,45 @@ void launch_score_t(const DeviceTables& t, hipStream_t st) {
 template <bool REFRESH>
 void launch_pack_t(const DeviceTables& t, uint32_t first, uint32_t last, uint64_t piece_base, uint64_t n_pieces,
                    uint64_t rec_base, uint8_t* stg, hipStream_t st) {
+  const uint32_t lds = occupancy_lds(LC_COPY_BLOCKS_PER_CU);
   for (uint64_t done = 0; done < n_pieces;) {
     const uint32_t g = grid_for(n_pieces - done, kCopyThreads);
-    hipLaunchKernelGGL((pack_kernel<REFRESH>), dim3(g), dim3(kCopyThreads), 0, st, t, first, last,
+    hipLaunchKernelGGL((pack_kernel<REFRESH>), dim3(g), dim3(kCopyThreads), lds, st, t, first, last,
                        piece_base + done, rec_base, stg);
     done += g;
   }
 }
 
 }  // namespace
+
+// A CU holds L bytes of LDS; a block that asks for more than L / (k + 1)
+// leaves room for at most k blocks.  The reservation asks for 2 KiB more than
+// that (rounded to 512 B) so the kernel's own few bytes of static LDS cannot
+// push it past L / k.  Queried once per device.
+uint32_t occupancy_lds(uint32_t blocks_per_cu) {
+  if (blocks_per_cu == 0) return 0;
+  constexpr int kMaxDevices = 64;
+  static std::atomic<int64_t> lds_cu[kMaxDevices], lds_block[kMaxDevices];  // 0: not queried yet
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  if (lds_cu[dev].load(std::memory_order_relaxed) == 0) {
+    int cu = 0, blk = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMaxSharedMemoryPerMultiprocessor, dev) != hipSuccess ||
+        hipDeviceGetAttribute(&blk, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) != hipSuccess) {
+      (void)hipGetLastError();
+      return 0;
+    }
+    lds_block[dev].store(blk, std::memory_order_relaxed);
+    lds_cu[dev].store(cu > 0 ? cu : -1, std::memory_order_relaxed);
+  }
+  const int64_t cu = lds_cu[dev].load(std::memory_order_relaxed);
+  const int64_t blk = lds_block[dev].load(std::memory_order_relaxed);
+  if (cu <= 0) return 0;
+  const int64_t k = blocks_per_cu;
+  const int64_t want = (cu / (k + 1) + 2048 + 511) / 512 * 512;
+  if (want > cu / k - 1024 || want > blk) return 0;
+  return static_cast<uint32_t>(want);
+}
 
 hipError_t launch_score(const DeviceTables& t, hipStream_t st) {
   if (t.dtype == 1) {
@@ -424,9 +457,10 @@ hipError_t launch_pack(const DeviceTables& t, uint32_t first_rank, uint32_t last
 }
 
 hipError_t launch_unpack(const DeviceTables& t, uint32_t n_ranks, uint64_t n_pieces, hipStream_t st) {
+  const uint32_t lds = occupancy_lds(LC_COPY_BLOCKS_PER_CU);
   for (uint64_t done = 0; done < n_pieces;) {
     const uint32_t g = grid_for(n_pieces - done, kCopyThreads);
-    hipLaunchKernelGGL(unpack_kernel, dim3(g), dim3(kCopyThreads), 0, st, t, n_ranks, done);
+    hipLaunchKernelGGL(unpack_kernel, dim3(g), dim3(kCopyThreads), lds, st, t, n_ranks, done);
     done += g;
   }
   return hipGetLastError();

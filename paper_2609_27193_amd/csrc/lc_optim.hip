@@ -255,10 +255,11 @@ __global__ __launch_bounds__(kScoreThreads) void optim_kernel(const DeviceTables
 template <int OPT, int WDT, int GDT, bool MASTER, typename SC>
 void launch_optim_t(const DeviceTables& t, const SC& sc, hipStream_t st) {
   const uint32_t g = grid_for(t.n_chunks, kScoreThreads);
+  const uint32_t lds = occupancy_lds(OPT == kAdamW ? LC_ADAMW_BLOCKS_PER_CU : LC_SGD_BLOCKS_PER_CU);
   if (g == t.n_chunks)
-    hipLaunchKernelGGL((optim_kernel<OPT, WDT, GDT, MASTER, false, SC>), dim3(g), dim3(kScoreThreads), 0, st, t, sc);
+    hipLaunchKernelGGL((optim_kernel<OPT, WDT, GDT, MASTER, false, SC>), dim3(g), dim3(kScoreThreads), lds, st, t, sc);
   else
-    hipLaunchKernelGGL((optim_kernel<OPT, WDT, GDT, MASTER, true, SC>), dim3(g), dim3(kScoreThreads), 0, st, t, sc);
+    hipLaunchKernelGGL((optim_kernel<OPT, WDT, GDT, MASTER, true, SC>), dim3(g), dim3(kScoreThreads), lds, st, t, sc);
 }
 
 template <int OPT, typename SC>
