@@ -110,6 +110,27 @@ def measured_traffic(kernel: str, workload: str, mode: str):
     return d.get("hbm_bytes_per_launch")
 
 
+def stream_hold(stream, us: float = 1000.0):
+    """Returns a function that enqueues a spin kernel of about `us` microseconds
+    on `stream` (torch's sleep kernel, its cycle count calibrated here once).
+    Enqueued right before a step's first timing event, it keeps the stream busy
+    while the host issues the step's calls, so the event fires when the GPU
+    reaches the step rather than when the host does: the timed region then
+    holds the step's GPU work and its own host round trips, not the host's
+    latency in issuing the first call."""
+    import torch
+    cycles = 1 << 20
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda._sleep(cycles)  # first launch: compile / load
+    e0.record(stream)
+    torch.cuda._sleep(cycles)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    per_us = cycles / max(e0.elapsed_time(e1) * 1e3, 1e-3)
+    n = max(1, int(per_us * us))
+    return lambda: torch.cuda._sleep(n)
+
+
 def copy_calibration(dev):
     """One plain 4 GiB device-to-device copy, for scaling the HBM byte
     counters of a profiling run."""
@@ -398,12 +419,14 @@ def main():
     if args.copy_calibration:
         copy_calibration(dev)
 
+    hold = stream_hold(stream)
     rows = []
     for i in range(warmup + steps):
         t += 1
         state.step(t)
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        hold()
         h0 = time.perf_counter()
         ev[0].record(stream)
         LC.lc_score_layers(ctx, t)
@@ -853,6 +876,7 @@ def main_optim(args, spec, optimizer):
     opt_b = (4 if spec.has_master else 0) + (8 if adamw else 0)  # fp32 bytes per element in a record
     if args.copy_calibration:
         copy_calibration(dev)
+    hold = stream_hold(stream)
     rows = []
     for i in range(warmup + steps):
         t += 1
@@ -861,6 +885,7 @@ def main_optim(args, spec, optimizer):
         ptrs = grad_ptrs(g)
         torch.cuda.synchronize()
         ev = [torch.cuda.Event(enable_timing=True) for _ in range(4)]
+        hold()
         ev[0].record(stream)
         fused(ctx, t, ptrs)
         ev[1].record(stream)

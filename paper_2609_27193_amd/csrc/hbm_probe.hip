@@ -20,6 +20,13 @@
 //
 //   lc_hbm_probe [GiB per array, default 16] [skew bytes, default 20480] [offset bytes, default 0]
 //   lc_hbm_probe empty     (dispatch cost of blocks that find no work)
+//   lc_hbm_probe pairs     (8 separately allocated pairs of 8 GiB arrays: two
+//                           reads + one write and copy per pair, r2w1 with
+//                           each first array against the next pair's second,
+//                           and r2w1 with the second array entered 64 MiB and
+//                           512 MiB later; three rounds: how much the rate
+//                           depends on the physical pages an allocation
+//                           receives, and whether offsets move it)
 //
 // Built a second time as a shared library (without LC_PROBE_MAIN), it
 // exports lc_probe_arrays: the kernels' own tile over arrays the caller
@@ -225,6 +232,54 @@ int main(int argc, char** argv) {
       std::fflush(stdout);
     }
     CK(hipFree(n_work));
+    CK(hipFree(sink));
+    return 0;
+  }
+  if (argc > 1 && std::string(argv[1]) == "pairs") {
+    // grid = bytes / 8 KiB tiles, every tile inside [0, bytes) of both arrays
+    constexpr int kPairs = 8;
+    const size_t bytes = size_t{8} << 30;
+    char *a[kPairs], *b[kPairs];
+    unsigned* sink = nullptr;
+    for (int i = 0; i < kPairs; ++i) {
+      CK(hipMalloc(&a[i], bytes));
+      CK(hipMalloc(&b[i], bytes));
+      CK(hipMemset(a[i], 1, bytes));
+      CK(hipMemset(b[i], 2, bytes));
+    }
+    CK(hipMalloc(&sink, 512 * sizeof(unsigned)));
+    CK(hipDeviceSynchronize());
+    const unsigned lds = lds_for(3);
+    // the shifted runs cover bytes - 512 MiB, so the second array's tiles stay inside it
+    constexpr size_t kMaxShift = size_t{512} << 20;
+    auto rate = [&](int pat, const char* x, char* y, size_t n) {
+      const unsigned g = static_cast<unsigned>(n / (256 * 2 * 16));
+      const double ms = best_ms(
+          [&] {
+            if (pat == 3) hipLaunchKernelGGL((probe<3, 2, 256>), dim3(g), dim3(256), lds, 0, x, y, sink);
+            else hipLaunchKernelGGL((probe<2, 2, 256>), dim3(g), dim3(256), lds, 0, x, y, sink);
+          },
+          6);
+      CK(hipGetLastError());
+      return kStreams[pat] * static_cast<double>(n) / ms / 1e6;
+    };
+    for (int round = 0; round < 3; ++round)
+      for (int i = 0; i < kPairs; ++i) {
+        const double r = rate(3, a[i], b[i], bytes), c = rate(2, a[i], b[i], bytes),
+                     x = rate(3, a[i], b[(i + 1) % kPairs], bytes),
+                     s0 = rate(3, a[i], b[i], bytes - kMaxShift),
+                     s64 = rate(3, a[i], b[i] + (size_t{64} << 20), bytes - kMaxShift),
+                     s512 = rate(3, a[i], b[i] + kMaxShift, bytes - kMaxShift);
+        std::printf("{\"pattern\": \"pairs\", \"round\": %d, \"pair\": %d, \"blocks_per_cu\": %d, "
+                    "\"r2w1_gbs\": %.1f, \"copy_gbs\": %.1f, \"r2w1_next_pair_gbs\": %.1f, "
+                    "\"r2w1_shift0_gbs\": %.1f, \"r2w1_shift64m_gbs\": %.1f, \"r2w1_shift512m_gbs\": %.1f}\n",
+                    round, i, lds ? 3 : 0, r, c, x, s0, s64, s512);
+        std::fflush(stdout);
+      }
+    for (int i = 0; i < kPairs; ++i) {
+      CK(hipFree(a[i]));
+      CK(hipFree(b[i]));
+    }
     CK(hipFree(sink));
     return 0;
   }
