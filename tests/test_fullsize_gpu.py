@@ -10,9 +10,10 @@ cover the rest:
 
 * the decision steps of the 8B (SNAPSHOT), 13B and Qwen2.5-14B (no master)
   states over one staleness period, including the burst of forced layers;
-* u of sampled layers (a rotating transformer block, the final norm, and the
-  embedding / lm_head on the first step and on the staleness burst) against
-  the oracle's Eq. 1 on host copies, within 1e-5;
+* u of every layer on the first step, and of sampled layers after (a
+  rotating transformer block, the final norm, and the embedding / lm_head on
+  the staleness burst), against the oracle's Eq. 1 on host copies, within
+  1e-5;
 * for every layer, the accumulator arithmetic of Eq. 2 (Delta(t) equals
   Delta(t-1) + u(t) bit for bit), and in ACCUM mode S == W after the pass;
 * the oracle's decision rule fed the GPU accumulators reproduces the mask
@@ -114,17 +115,25 @@ class FullRun:
         orc = O.LayerCheckOracle(segs, 1, self.odt, self.spec.has_master, O.MODE_ACCUM, [0.0], 1)
         return np.frombuffer(orc.layer_record(0), dtype=np.uint8)
 
-    def step(self, t, sampled, lr=1.0):
+    def step(self, t, sampled, lr=1.0, pool=None):
+        """One decision step; u of the sampled layers against the oracle's
+        Eq. 1, or of every layer when a worker pool is given."""
         torch = self.torch
         self.state.step(t)
         torch.cuda.synchronize()
-        host = {l: self.host_layer(l) for l in sampled}
+        if pool is not None:
+            uo_all = oracle_scores_every_layer(self, pool)
+            sampled_u = range(self.N)
+        else:
+            host = {l: self.host_layer(l) for l in sampled}
+            uo_all = {l: O.layer_update_score([x["weight"] for x in host[l]], [x["shadow"] for x in host[l]],
+                                              self.odt, 1e-8)[3] for l in sampled}
+            sampled_u = sampled
         _, d_prev, tl_prev = LC.lc_read_state(self.ctx, self.N)
         LC.lc_score_layers(self.ctx, t)
         u, d, tl = LC.lc_read_state(self.ctx, self.N)
-        for l in sampled:
-            uo = O.layer_update_score([x["weight"] for x in host[l]], [x["shadow"] for x in host[l]],
-                                      self.odt, 1e-8)[3]
+        for l in sampled_u:
+            uo = uo_all[l]
             assert (u[l] == 0) == (uo == 0) and abs(u[l] - uo) <= REL * abs(uo), (t, l, u[l], uo)
         for l in range(self.N):  # Eq. 2 arithmetic on every layer
             expect = d_prev[l] + u[l] if self.mode == LC.LC_MODE_ACCUM else u[l]
@@ -142,7 +151,8 @@ class FullRun:
         assert all(d_post[l] == (0.0 if mask[l] else d[l]) for l in range(self.N))
         self.pack_and_check(mask, [l for l in sampled if mask[l]])
         log(f"  t={t}: selected {st['n_selected']}/{self.N} (forced {st['n_forced']}), "
-            f"payload {st['payload_bytes'] / 1e9:.2f} GB, sampled {sampled}")
+            f"payload {st['payload_bytes'] / 1e9:.2f} GB, "
+            f"{'u of every layer' if pool is not None else f'sampled {sampled}'}")
         return mask, st
 
     def pack_and_check(self, mask, check_layers, dest=None):
@@ -211,7 +221,8 @@ def sample_for(t, N, s_max):
 # The benchmark's calibrated base thresholds, so each state selects about
 # its target fraction of layers (8B ~20%, 13B ~15%, Qwen ~30%, 70B shard ~10%).
 # The benchmarked 8B state and the 70B shard are checked on every layer at
-# every step (test_fullsize_every_layer); the other states on samples.
+# every step (test_fullsize_every_layer); the other states on every layer's
+# u at the first step and on samples after.
 WORKLOADS = [
     ("llama3-8b", LC.LC_MODE_SNAPSHOT, 0.0391),
     ("llama2-13b", LC.LC_MODE_ACCUM, 0.157),
@@ -227,6 +238,7 @@ EVERY_LAYER = [
 @pytest.mark.parametrize("name,mode,k0", WORKLOADS,
                          ids=[w[0] + ("-snapshot" if w[1] == LC.LC_MODE_SNAPSHOT else "") for w in WORKLOADS])
 def test_fullsize_decision_steps(name, mode, k0):
+    from concurrent.futures import ThreadPoolExecutor
     spec = I.WORKLOADS[name]()
     k0s = [k0 * (10.0 if l.name == "embed_tokens" else 1.0) for l in spec.layers]
     run = FullRun(spec, mode, k0s)
@@ -236,7 +248,11 @@ def test_fullsize_decision_steps(name, mode, k0):
         calls = run.pack_and_check(base, [run.N - 2, run.N - 1])
         log(f"  base packed in {calls} call(s)")
         for t in range(1, spec.s_max + 1):
-            run.step(t, sample_for(t, run.N, spec.s_max))
+            if t == 1:  # every layer's Eq. 1 against the oracle once
+                with ThreadPoolExecutor(_oracle_workers()) as pool:
+                    run.step(t, sample_for(t, run.N, spec.s_max), pool=pool)
+            else:
+                run.step(t, sample_for(t, run.N, spec.s_max))
     finally:
         run.close()
 
