@@ -21,6 +21,14 @@
  * before anything is enqueued, leaving the context unchanged.  A message for
  * the last failure on the calling thread is available from lc_last_error().
  *
+ * Tracing: with LAYERCHECK_ROCTX=1 in the environment when the first call is
+ * made, every state-changing entry point (context, score, select, pack,
+ * restore, optimizer steps, store) opens a roctx range named after itself
+ * for the length of the call, so a marker trace (rocprofv3 --marker-trace)
+ * places each call's host span beside its kernels.  The roctx library is
+ * loaded at run time; without the variable, or without that library,
+ * nothing is traced and nothing is loaded.
+ *
  * Layer groups (Section 2.2): embed_tokens, each transformer block, the final
  * norm and lm_head.  A layer may consist of any number of tensors
  * ("segments"); a segment is one contiguous range of one tensor, so a ZeRO-3

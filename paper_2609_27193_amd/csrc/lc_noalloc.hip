@@ -18,6 +18,7 @@
 #include "layercheck.h"
 #include "lc_ctx.h"
 #include "lc_internal.h"
+#include "lc_trace.h"
 
 #ifndef LC_NOALLOC_SCRATCH_BYTES
 #define LC_NOALLOC_SCRATCH_BYTES (16u << 20)
@@ -113,6 +114,7 @@ struct DrainOnExit {
 
 extern "C" lc_status lc_score_layers_static(const lc_segment* segments, uint32_t n_segments, uint32_t n_layers,
                                             int32_t weight_dtype, double eps_w, double* u_out, void* stream) {
+  lc::TraceRange trace_("lc_score_layers_static");
   // ---- arguments and sizes (host only: nothing below touches the GPU) --------
   if (!segments) return fail(LC_ERR_INVALID_ARG, "segments is NULL");
   if (!u_out) return fail(LC_ERR_INVALID_ARG, "u_out is NULL");

@@ -1,6 +1,7 @@
 // Host runtime of the LayerCheck HIP library: validation, layer-aligned
 // tables, the call-order state machine and kernel launches behind the C
 // interface declared in include/layercheck.h.
+#include <dlfcn.h>
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -8,6 +9,7 @@
 #include <cmath>
 #include <cstdarg>
 #include <cstdio>
+#include <cstdlib>
 #include <cstring>
 #include <limits>
 #include <new>
@@ -17,6 +19,7 @@
 #include "layercheck.h"
 #include "lc_ctx.h"
 #include "lc_internal.h"
+#include "lc_trace.h"
 
 using namespace lc;
 
@@ -400,6 +403,41 @@ lc_status restore_finish(lc_ctx* c, int64_t t_fail, const std::vector<int64_t>& 
 
 }  // namespace lc
 
+namespace {
+
+using RoctxPush = int (*)(const char*);
+using RoctxPop = int (*)();
+struct Roctx {
+  RoctxPush push = nullptr;
+  RoctxPop pop = nullptr;
+};
+
+// Resolved once per process (thread-safe static initialisation).
+const Roctx& roctx() {
+  static const Roctx r = [] {
+    Roctx x;
+    const char* on = std::getenv("LAYERCHECK_ROCTX");
+    if (!on || std::strcmp(on, "1") != 0) return x;
+    void* h = dlopen("librocprofiler-sdk-roctx.so.1", RTLD_NOW | RTLD_LOCAL);
+    if (!h) return x;
+    x.push = reinterpret_cast<RoctxPush>(dlsym(h, "roctxRangePushA"));
+    x.pop = reinterpret_cast<RoctxPop>(dlsym(h, "roctxRangePop"));
+    if (!x.push || !x.pop) x = Roctx{};
+    return x;
+  }();
+  return r;
+}
+
+}  // namespace
+
+lc::TraceRange::TraceRange(const char* name) : on_(roctx().push != nullptr) {
+  if (on_) roctx().push(name);
+}
+
+lc::TraceRange::~TraceRange() {
+  if (on_) roctx().pop();
+}
+
 extern "C" {
 
 const char* lc_last_error(void) { return g_error.c_str(); }
@@ -425,6 +463,7 @@ lc_status lc_query_layout(const lc_layout_desc* d, uint64_t* numel_out, uint64_t
 }
 
 lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
+  lc::TraceRange trace_("lc_init_layout");
   if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   lc_ctx* c = new (std::nothrow) lc_ctx();
@@ -580,6 +619,7 @@ lc_status lc_init_layout(const lc_layout_desc* d, lc_ctx** out) {
 }
 
 lc_status lc_score_layers(lc_ctx* c, int64_t step) {
+  lc::TraceRange trace_("lc_score_layers");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (step <= c->last_step)
@@ -603,6 +643,7 @@ lc_status lc_score_layers(lc_ctx* c, int64_t step) {
 }
 
 lc_status lc_select(lc_ctx* c, int64_t step, double lr_scale, uint8_t* mask_out, lc_select_stats* stats_out) {
+  lc::TraceRange trace_("lc_select");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (!c->scored || c->scored_step != step)
@@ -631,6 +672,7 @@ lc_status lc_select(lc_ctx* c, int64_t step, double lr_scale, uint8_t* mask_out,
 
 lc_status lc_pack_selected(lc_ctx* c, void* staging, uint64_t capacity, uint32_t first_rank,
                            lc_pack_result* out) {
+  lc::TraceRange trace_("lc_pack_selected");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
@@ -673,6 +715,7 @@ lc_status lc_pack_selected(lc_ctx* c, void* staging, uint64_t capacity, uint32_t
 
 lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versions, int64_t t_fail,
                                int64_t* chosen_step_out) {
+  lc::TraceRange trace_("lc_restore_composite");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (!v || n_versions == 0) return fail(LC_ERR_INVALID_ARG, "no versions");
@@ -769,6 +812,7 @@ lc_status lc_restore_composite(lc_ctx* c, const lc_version* v, uint32_t n_versio
 }
 
 lc_status lc_rebase(lc_ctx* c, int64_t step) {
+  lc::TraceRange trace_("lc_rebase");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (step < c->last_step)
@@ -854,6 +898,7 @@ extern "C" {
 
 lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
                               const uint8_t* decay_mask, const lc_adamw_params* p) {
+  lc::TraceRange trace_("lc_adamw_step_score");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (!p) return fail(LC_ERR_INVALID_ARG, "params must be non-NULL");
@@ -884,6 +929,7 @@ lc_status lc_adamw_step_score(lc_ctx* c, int64_t step, const void* const* grads,
 
 lc_status lc_sgd_step_score(lc_ctx* c, int64_t step, const void* const* grads, int32_t grad_dtype,
                             const uint8_t* decay_mask, const lc_sgd_params* p) {
+  lc::TraceRange trace_("lc_sgd_step_score");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   if (!p) return fail(LC_ERR_INVALID_ARG, "params must be non-NULL");
@@ -900,6 +946,7 @@ lc_status lc_sgd_step_score(lc_ctx* c, int64_t step, const void* const* grads, i
 }
 
 lc_status lc_read_state(lc_ctx* c, double* u_out, double* delta_out, int64_t* t_last_out) {
+  lc::TraceRange trace_("lc_read_state");
   lc_status st = check_ctx(c);
   if (st != LC_OK) return st;
   const size_t N = c->L.N;
@@ -916,6 +963,7 @@ uint64_t lc_record_bytes(const lc_ctx* c, uint32_t layer) {
 }
 
 lc_status lc_destroy(lc_ctx* c) {
+  lc::TraceRange trace_("lc_destroy");
   if (!c) return LC_OK;
   hipError_t e = hipStreamSynchronize(c->stream);
   free_all(c);

@@ -32,6 +32,7 @@
 #include <vector>
 
 #include "lc_ctx.h"
+#include "lc_trace.h"
 
 using namespace lc;
 
@@ -599,6 +600,7 @@ extern "C" {
 
 lc_status lc_store_open(const char* dir, uint32_t n_layers, const uint64_t* record_bytes, uint64_t buffer_bytes,
                         lc_store** out) {
+  lc::TraceRange trace_("lc_store_open");
   if (!out) return fail(LC_ERR_INVALID_ARG, "out is NULL");
   *out = nullptr;
   if (!dir || !*dir || n_layers == 0 || !record_bytes) return fail(LC_ERR_INVALID_ARG, "bad store arguments");
@@ -827,15 +829,18 @@ extern "C" {
 
 lc_status lc_store_append(lc_store* s, int64_t step, const uint8_t* mask, const void* payload, uint64_t bytes,
                           void* stream) {
+  lc::TraceRange trace_("lc_store_append");
   return append_impl(s, step, mask, payload, bytes, stream, true, nullptr);
 }
 
 lc_status lc_store_append_async(lc_store* s, int64_t step, const uint8_t* mask, const void* payload,
                                 uint64_t bytes, void* stream, void* reuse_event) {
+  lc::TraceRange trace_("lc_store_append_async");
   return append_impl(s, step, mask, payload, bytes, stream, false, reuse_event);
 }
 
 lc_status lc_store_sync(lc_store* s) {
+  lc::TraceRange trace_("lc_store_sync");
   if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
   return wait_idle(s);
 }
@@ -871,6 +876,7 @@ lc_status lc_store_plan(lc_store* s, int64_t t_fail, int64_t* chosen_step_out) {
 }
 
 lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chosen_step_out) {
+  lc::TraceRange trace_("lc_store_restore");
   if (!s || !c) return fail(LC_ERR_INVALID_ARG, "store and context must be non-NULL");
   if (c->poisoned) return fail(LC_ERR_BAD_STATE, "context is poisoned by an earlier HIP error");
   if (c->L.N != s->N || c->L.rec_bytes != s->R)
@@ -912,6 +918,7 @@ lc_status lc_store_restore(lc_store* s, lc_ctx* c, int64_t t_fail, int64_t* chos
 }
 
 lc_status lc_store_compact(lc_store* s, int64_t t_keep, uint32_t* removed_out) {
+  lc::TraceRange trace_("lc_store_compact");
   if (removed_out) *removed_out = 0;
   if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
   lc_status st = wait_idle(s);
@@ -937,6 +944,7 @@ lc_status lc_store_compact(lc_store* s, int64_t t_keep, uint32_t* removed_out) {
 }
 
 lc_status lc_store_discard_after(lc_store* s, int64_t step, uint32_t* removed_out) {
+  lc::TraceRange trace_("lc_store_discard_after");
   if (removed_out) *removed_out = 0;
   if (!s) return fail(LC_ERR_INVALID_ARG, "store is NULL");
   lc_status st = wait_idle(s);
@@ -947,6 +955,7 @@ lc_status lc_store_discard_after(lc_store* s, int64_t step, uint32_t* removed_ou
 }
 
 lc_status lc_store_close(lc_store* s) {
+  lc::TraceRange trace_("lc_store_close");
   if (!s) return LC_OK;
   lc_status st = wait_idle(s);
   {
