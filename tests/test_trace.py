@@ -69,3 +69,30 @@ def test_ranges_opened_and_closed_when_on(built):
         pytest.skip("no roctx library in this ROCm")
     out = run_child("1")
     assert "mapped 1" in out and "depth 0" in out, out
+
+
+GPU_CHILD = r"""
+import sys
+sys.path.insert(0, sys.argv[1])
+import __graft_entry__ as g
+g.smoke()
+print("roctx mapped", int(any(sys.argv[2] in line for line in open("/proc/self/maps"))), flush=True)
+"""
+
+
+@pytest.mark.gpu
+def test_traced_decision_steps_match_the_oracle():
+    """Decision steps and a composite restore on cuda:0 with the ranges on
+    (the smoke run: scores within 1e-5, masks, payloads, shadow and restore
+    bit-exact against the oracle), in a process of its own."""
+    from tests.conftest import gpu_available
+    if not gpu_available():
+        pytest.skip("needs an MI355X")
+    if not os.path.exists(f"/opt/rocm/lib/{ROCTX}.1"):
+        pytest.skip("no roctx library in this ROCm")
+    env = dict(os.environ, LAYERCHECK_ROCTX="1")
+    r = subprocess.run([sys.executable, "-u", "-c", GPU_CHILD, ROOT, ROCTX], capture_output=True, text=True,
+                       env=env, timeout=240)
+    print(r.stdout[-1500:], flush=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    assert "smoke OK" in r.stdout and "roctx mapped 1" in r.stdout
