@@ -155,6 +155,45 @@ def test_restore_composite_then_continue(where):
 
 
 @pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_long_horizon_lr_schedule(mode):
+    """120 decision steps, about 15 staleness periods (S_max = 8), with a
+    cosine learning-rate schedule from lr_0 to 0.1 lr_0 driving the
+    threshold K(t) = K0 s(lr(t)) (Eq. 3).  At every step both sides agree
+    (u and Delta within 1e-5, masks, stats, payloads and shadow exact), so the
+    accumulators stay in step over many persist cycles; the staleness bound
+    holds at every step (Section 3.3); both rules fire; as K falls, more
+    layers are persisted by drift in the last stretch than in the first.  A
+    composite restore from the whole history at a mid-schedule t_fail then
+    matches the oracle (mixed timestamps, all within the staleness bound),
+    and the run resumes from it."""
+    import math
+    spec = reduced_8b()
+    T = 120
+    p = Pair(spec, mode, k0_for(spec, 0.01))
+    lr = lambda t: 0.1 + 0.9 * 0.5 * (1.0 + math.cos(math.pi * t / T))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        stats = []
+        run_steps(p, range(1, T + 1), lr=lr, stats=stats)
+        assert all(st["max_age"] <= spec.s_max - 1 for st in stats)
+        assert_both_rules_fired(stats)
+        by_drift = [st["n_selected"] - st["n_forced"] for st in stats]
+        assert sum(by_drift[-30:]) > sum(by_drift[:30]), by_drift
+        log(f"  {T} steps: drift-selected layer-steps {sum(by_drift)}, forced "
+            f"{sum(st['n_forced'] for st in stats)}; near-threshold excluded {p.near_excluded}, "
+            f"resyncs {p.resyncs}")
+        t_fail = T // 2 + 3  # mid-schedule; later, K is so low that nearly every layer persists each step
+        chosen = _restore_and_compare(p, t_fail, "device")
+        log(f"  restored at t_fail={t_fail} from steps {sorted(set(chosen.tolist()))}")
+        assert len(set(chosen.tolist())) >= 2
+        assert min(chosen.tolist()) >= t_fail - spec.s_max + 1  # every layer within the staleness bound
+        p.adopt_restored()
+        run_steps(p, range(t_fail + 1, t_fail + 4), lr=lr)
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
 def test_rebase_mid_run_then_restore(mode):
     """A full base checkpoint in the middle of a run (Section 3.4's base,
     taken again after an unscored stretch): Delta and t_l reset, the shadow
