@@ -194,6 +194,37 @@ def test_long_horizon_lr_schedule(mode):
 
 
 @pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
+def test_decisions_at_irregular_steps(mode):
+    """The weights move every iteration, decisions come only at steps 1, 2,
+    5, 6, 7, 19, 20 and 35 (S_max = 8).  A score after skipped iterations
+    measures the change since the previous scored step (ACCUM) or since the
+    last persist (SNAPSHOT), on both sides alike; a gap of S_max or more
+    forces every layer that drift did not select (Section 3.3), leaving
+    every layer's age 0 after the decision."""
+    spec = reduced_8b()
+    assert spec.s_max == 8
+    decisions = {1, 2, 5, 6, 7, 19, 20, 35}
+    p = Pair(spec, mode, k0_for(spec, 0.01))
+    try:
+        p.pack(0, np.ones(p.N, np.uint8))
+        stats = {}
+        for t in range(1, max(decisions) + 1):
+            if t in decisions:
+                mask, st = p.step(t)
+                stats[t] = st
+                log(f"  step {t}: selected {st['n_selected']}/{p.N} forced {st['n_forced']} "
+                    f"max_age {st['max_age']}")
+            else:
+                p.advance(t)  # an iteration with no decision
+        for t in (19, 35):  # 12 and 15 iterations since the previous decision
+            assert stats[t]["n_selected"] == p.N and stats[t]["max_age"] == 0, (t, stats[t])
+        assert any(st["n_forced"] > 0 for st in stats.values())
+        p.check_arrays()
+    finally:
+        p.close()
+
+
+@pytest.mark.parametrize("mode", [LC.LC_MODE_ACCUM, LC.LC_MODE_SNAPSHOT], ids=["accum", "snapshot"])
 def test_rebase_mid_run_then_restore(mode):
     """A full base checkpoint in the middle of a run (Section 3.4's base,
     taken again after an unscored stretch): Delta and t_l reset, the shadow
