@@ -119,6 +119,9 @@ def stream_hold(stream, us: float = 1000.0):
     holds the step's GPU work and its own host round trips, not the host's
     latency in issuing the first call."""
     import torch
+    if not hasattr(torch.cuda, "_sleep"):
+        log("[bench] this torch has no sleep kernel: steps are timed without holding the stream")
+        return lambda: None
     cycles = 1 << 20
     e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     torch.cuda._sleep(cycles)  # first launch: compile / load
