@@ -198,6 +198,66 @@ def check_staleness_period(cls, mode=O.MODE_ACCUM):
                 orc.pack(0, 1 << 30)
 
 
+def check_irregular_steps(cls, mode=O.MODE_ACCUM):
+    # Decisions need not come every iteration.  (a) zero drift, S_max = 4,
+    # decisions at 1, 2, 3, 9, 10, 12, 13: nothing is due until the gap from
+    # t_base reaches S_max (step 9, age 9), then every layer is forced and its
+    # age is 0; the next forcing is exactly S_max after that (step 13).
+    segs = _const_layout(3)
+    orc = cls(segs, 3, O.DT_F32, True, mode, [1e-3] * 3, s_max=4)
+    orc.pack(0, 1 << 30)
+    last = 0
+    for t in (1, 2, 3, 9, 10, 12, 13):
+        orc.score(t)
+        mask, st = orc.select(t, 1.0)
+        due = int(t - last >= 4)
+        assert list(mask) == [due] * 3, (t, mask)
+        assert st["n_forced"] == 3 * due
+        assert st["max_age"] == (0 if due else t - last), (t, st)
+        last = t if due else last
+        orc.pack(0, 1 << 30)
+    # (b) Eq. 1 sees only the weights at decision steps.  Layer 0 holds four
+    # elements at 1/2; each unscored iteration moves the first two up and the
+    # last two down by d = 2^-9, which keeps mean|W| at 1/2.  Layer 1 never
+    # moves.  K0 = 2^-6, S_max far away, eps_w = 0.
+    d = 2.0 ** -9
+    segs = _const_layout(2)
+    orc = cls(segs, 2, O.DT_F32, True, mode, [2.0 ** -6] * 2, s_max=100, eps_w=0.0)
+    orc.pack(0, 1 << 30)
+
+    def move(k):
+        w = segs[0].weight
+        w[:2] += k * d
+        w[2:] -= k * d
+
+    def decide_at(t):
+        orc.score(t)
+        u = list(orc.u)
+        mask, _ = orc.select(t, 1.0)
+        orc.pack(0, 1 << 30)
+        return u, list(mask)
+
+    u, mask = decide_at(1)
+    assert u == [0.0, 0.0] and mask == [0, 0]
+    move(1)
+    move(1)  # iterations 2 and 3, decision at 3: |W - W(1)| = 2d per element
+    u, mask = decide_at(3)
+    assert u == [2.0 ** -7, 0.0] and mask == [0, 0], (u, mask)
+    move(-1)
+    move(-1)  # back to 1/2 by step 6
+    u, mask = decide_at(6)
+    if mode == O.MODE_ACCUM:
+        # reference W(3): the path length adds up, Delta = 2^-7 + 2^-7 = K0
+        assert u == [2.0 ** -7, 0.0] and mask == [1, 0], (u, mask)
+    else:
+        # reference: the base persist; the net displacement is zero
+        assert u == [0.0, 0.0] and mask == [0, 0], (u, mask)
+    for k in (1, 1, -1, -1):
+        move(k)  # a round trip between two decisions is invisible to Eq. 1
+    u, mask = decide_at(11)
+    assert u == [0.0, 0.0] and mask == [0, 0], (u, mask)
+
+
 def check_k0_extremes(cls):
     lay = HostLayout([[5, 3], [4], [7]], seed=4)
     # K0 = 0: every layer persists by drift every step.  With S_max = 1 every

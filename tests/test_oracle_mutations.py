@@ -130,6 +130,7 @@ def all_checks(M):
         yield lambda c=c: c(cls)
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
         yield lambda mode=mode: P.check_staleness_period(cls, mode)
+        yield lambda mode=mode: P.check_irregular_steps(cls, mode)
         yield lambda mode=mode: P.check_stats_invariants(cls, mode)
         yield lambda mode=mode: P.check_restore_roundtrip(cls, mode)
         yield lambda mode=mode: P.check_rebase(cls, mode)

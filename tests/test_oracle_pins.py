@@ -30,6 +30,11 @@ def test_staleness_period(mode):
 
 
 @pytest.mark.parametrize("mode", [O.MODE_ACCUM, O.MODE_SNAPSHOT])
+def test_irregular_steps(mode):
+    P.check_irregular_steps(O.LayerCheckOracle, mode)
+
+
+@pytest.mark.parametrize("mode", [O.MODE_ACCUM, O.MODE_SNAPSHOT])
 def test_zero_layer(mode):
     P.check_zero_layer(O.LayerCheckOracle, mode)
 
