@@ -27,6 +27,18 @@
 //                           512 MiB later; three rounds: how much the rate
 //                           depends on the physical pages an allocation
 //                           receives, and whether offsets move it)
+//   lc_hbm_probe tail      (two 16 GiB arrays, read2 and r2w1 with the kernels'
+//                           tile at 2, 3, 4, 6 blocks per CU or as many as fit:
+//                           bare; with the score kernel's two dependent table
+//                           lookups per block; with those lookups and its
+//                           end-of-block reduction to one fp64 pair; with the
+//                           lookups and one fp64 pair per wave instead (no LDS,
+//                           no barrier): what a block's own latency costs)
+//   lc_hbm_probe persist   (two 16 GiB arrays, read2, r2w1 and copy: one tile
+//                           per block against k resident blocks per CU that
+//                           each walk tiles of their XCD's eighth, loading the
+//                           next tile before consuming the current one, in
+//                           grid-stride order or in contiguous runs)
 //
 // Built a second time as a shared library (without LC_PROBE_MAIN), it
 // exports lc_probe_arrays: the kernels' own tile over arrays the caller
@@ -38,6 +50,9 @@
 #include <cstdio>
 #include <cstdlib>
 #include <string>
+#include <vector>
+
+#include "lc_device.h"
 
 namespace {
 
@@ -115,6 +130,134 @@ __global__ __launch_bounds__(NT) void probe(const char* a, char* b, unsigned* si
 // worst case whose work is decided on the device).
 __global__ __launch_bounds__(256) void empty_blocks(const unsigned* n_work, unsigned* sink) {
   if (blockIdx.x < *n_work) sink[threadIdx.x] = blockIdx.x;
+}
+
+// ---- tail: the cost of a block's own latency at few blocks per CU ------------
+// Tiles are grouped into segments of kTailSegTiles; LOOKUP 1 finds a tile's
+// addresses through tile -> segment -> (a, b, first tile), two dependent
+// loads like the score kernel's chunk -> segment tables.  REDUCE 1 forms the
+// score kernel's terms (|w - s| and |s| of bf16 pairs, fp32 per vector, fp64
+// per lane) and reduces them to one fp64 pair per block (wave sums, LDS
+// combine, thread 0 stores); REDUCE 2 stores one pair per wave instead.
+constexpr unsigned kTailSegTiles = 4096;
+struct TailSeg {
+  uint64_t a, b, first;
+};
+struct TailArgs {
+  const char* a;
+  char* b;
+  const uint32_t* tile_seg;
+  const TailSeg* segs;
+  double2* partials;  // [tiles * 4]
+  unsigned* sink;
+};
+
+template <int PAT, int LOOKUP, int REDUCE>
+__global__ __launch_bounds__(256) void tail_probe(const TailArgs g) {
+  constexpr unsigned kTile = 256 * 2 * 16;
+  const size_t t = tile_of(blockIdx.x, gridDim.x);
+  const char* pa;
+  char* pb;
+  if constexpr (LOOKUP == 0) {
+    pa = g.a + t * kTile;
+    pb = g.b + t * kTile;
+  } else {
+    const TailSeg sg = g.segs[g.tile_seg[t]];
+    pa = reinterpret_cast<const char*>(sg.a) + (t - sg.first) * kTile;
+    pb = reinterpret_cast<char*>(sg.b) + (t - sg.first) * kTile;
+  }
+  const auto ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(pa), 0, static_cast<int>(kTile), 0x00020000);
+  const auto rb = __builtin_amdgcn_make_buffer_rsrc(pb, 0, static_cast<int>(kTile), 0x00020000);
+  u32x4 v[2], w[2];
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    v[k] = ld<256>(ra, k);
+    w[k] = ld<256>(rb, k);
+  }
+  if constexpr (REDUCE == 0) {
+    unsigned acc = 0;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      if constexpr (PAT == 3) st<256>(rb, k, v[k]);
+      acc ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
+      acc += w[k].x + w[k].y + w[k].z + w[k].w;
+    }
+    if (acc == 0x9e3779b9u) g.sink[threadIdx.x] = acc;
+  } else {
+    double a = 0.0, b = 0.0;
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      float d[8], e[8];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float w0 = lc::bf_lo(v[k][q]), w1 = lc::bf_hi(v[k][q]);
+        const float s0 = lc::bf_lo(w[k][q]), s1 = lc::bf_hi(w[k][q]);
+        d[2 * q] = fabsf(w0 - s0);
+        d[2 * q + 1] = fabsf(w1 - s1);
+        e[2 * q] = fabsf(s0);
+        e[2 * q + 1] = fabsf(s1);
+      }
+      a += static_cast<double>(((d[0] + d[1]) + (d[2] + d[3])) + ((d[4] + d[5]) + (d[6] + d[7])));
+      b += static_cast<double>(((e[0] + e[1]) + (e[2] + e[3])) + ((e[4] + e[5]) + (e[6] + e[7])));
+      if constexpr (PAT == 3) st<256>(rb, k, v[k]);
+    }
+    if constexpr (REDUCE == 1) {
+      lc::block_sum2<256>(a, b);
+      if (threadIdx.x == 0) g.partials[t] = make_double2(a, b);
+    } else {
+      lc::wave_sum2(a, b);
+      if ((threadIdx.x & 63) == 0) g.partials[t * 4 + (threadIdx.x >> 6)] = make_double2(a, b);
+    }
+  }
+}
+
+// ---- persist: resident blocks walking tiles against one tile per block --------
+// G blocks (a multiple of 8; block x runs on XCD x mod 8) each walk `per`
+// tiles of their XCD's eighth: ORDER 0 grid-stride (tile base + j + i G/8),
+// ORDER 1 contiguous runs (tile base + j per + i).  The next tile's loads are
+// issued before the current tile is consumed, into a second register set (no
+// copies between the sets, so each wait is for the older tile only); past the
+// last tile the descriptors cover zero bytes and the loads touch no memory.
+template <int PAT, int ORDER>
+__global__ __launch_bounds__(256) void persist_probe(const char* a, char* b, unsigned* sink, unsigned tiles) {
+  constexpr unsigned kTile = 256 * 2 * 16;
+  const unsigned B = gridDim.x / 8u, xcd = blockIdx.x % 8u, j = blockIdx.x / 8u;
+  const unsigned per = tiles / 8u / B;
+  const size_t base = static_cast<size_t>(xcd) * (tiles / 8u);
+  auto tile_at = [&](unsigned i) -> size_t {
+    return ORDER == 0 ? base + j + static_cast<size_t>(i) * B : base + static_cast<size_t>(j) * per + i;
+  };
+  u32x4 va[2], wa[2], vb[2], wb[2];
+  auto issue = [&](unsigned i, u32x4* v, u32x4* w) {
+    const bool ok = i < per;
+    const size_t t = ok ? tile_at(i) : 0;
+    const int n = ok ? static_cast<int>(kTile) : 0;
+    const auto ra = __builtin_amdgcn_make_buffer_rsrc(const_cast<char*>(a) + t * kTile, 0, n, 0x00020000);
+    const auto rb = __builtin_amdgcn_make_buffer_rsrc(b + t * kTile, 0, n, 0x00020000);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      v[k] = ld<256>(ra, k);
+      if constexpr (PAT != 2) w[k] = ld<256>(rb, k);
+    }
+  };
+  unsigned acc = 0;
+  auto consume = [&](unsigned i, const u32x4* v, const u32x4* w) {
+    const auto rb = tile(b, tile_at(i), kTile);
+#pragma unroll
+    for (int k = 0; k < 2; ++k) {
+      if constexpr (PAT >= 2) st<256>(rb, k, v[k]);
+      acc ^= v[k].x ^ v[k].y ^ v[k].z ^ v[k].w;
+      if constexpr (PAT != 2) acc += w[k].x + w[k].y + w[k].z + w[k].w;
+    }
+  };
+  issue(0, va, wa);
+  for (unsigned i = 0; i < per; i += 2) {  // per is even (host check)
+    issue(i + 1, vb, wb);
+    consume(i, va, wa);
+    issue(i + 2, va, wa);
+    consume(i + 1, vb, wb);
+  }
+  if (acc == 0x9e3779b9u) sink[threadIdx.x] = acc;
 }
 
 template <typename F>
@@ -280,6 +423,122 @@ int main(int argc, char** argv) {
       CK(hipFree(a[i]));
       CK(hipFree(b[i]));
     }
+    CK(hipFree(sink));
+    return 0;
+  }
+  if (argc > 1 && (std::string(argv[1]) == "tail" || std::string(argv[1]) == "persist")) {
+    // two 16 GiB arrays; every block's tiles lie inside [0, bytes) of both
+    const size_t bytes = size_t{16} << 30;
+    constexpr unsigned kTile = 256 * 2 * 16;
+    const unsigned tiles = static_cast<unsigned>(bytes / kTile);  // 2 M, a multiple of kTailSegTiles and of 8
+    char *a = nullptr, *b = nullptr;
+    unsigned* sink = nullptr;
+    CK(hipMalloc(&a, bytes));
+    CK(hipMalloc(&b, bytes));
+    CK(hipMalloc(&sink, 256 * sizeof(unsigned)));
+    CK(hipMemset(a, 1, bytes));
+    CK(hipMemset(b, 2, bytes));
+    if (std::string(argv[1]) == "tail") {
+      const unsigned nseg = tiles / kTailSegTiles;
+      std::vector<uint32_t> tile_seg(tiles);
+      std::vector<TailSeg> segs(nseg);
+      for (unsigned i = 0; i < nseg; ++i)
+        segs[i] = TailSeg{reinterpret_cast<uint64_t>(a + static_cast<size_t>(i) * kTailSegTiles * kTile),
+                          reinterpret_cast<uint64_t>(b + static_cast<size_t>(i) * kTailSegTiles * kTile),
+                          static_cast<uint64_t>(i) * kTailSegTiles};
+      for (unsigned i = 0; i < tiles; ++i) tile_seg[i] = i / kTailSegTiles;
+      TailArgs g{a, b, nullptr, nullptr, nullptr, sink};
+      uint32_t* d_ts = nullptr;
+      TailSeg* d_segs = nullptr;
+      double2* parts = nullptr;
+      CK(hipMalloc(&d_ts, tiles * sizeof(uint32_t)));
+      CK(hipMalloc(&d_segs, nseg * sizeof(TailSeg)));
+      CK(hipMalloc(&parts, static_cast<size_t>(tiles) * 4 * sizeof(double2)));
+      CK(hipMemcpy(d_ts, tile_seg.data(), tiles * sizeof(uint32_t), hipMemcpyHostToDevice));
+      CK(hipMemcpy(d_segs, segs.data(), nseg * sizeof(TailSeg), hipMemcpyHostToDevice));
+      CK(hipDeviceSynchronize());
+      g.tile_seg = d_ts;
+      g.segs = d_segs;
+      g.partials = parts;
+      const char* vname[4] = {"bare", "lookups", "lookups+block_reduce", "lookups+wave_partials"};
+      auto one = [&](int pat, int variant, int k) {
+        const unsigned lds = lds_for(k);
+        if (k > 0 && lds == 0) return;
+        auto launch = [&] {
+          const dim3 grid(tiles), block(256);
+          if (pat == 1) {
+            if (variant == 0) hipLaunchKernelGGL((tail_probe<1, 0, 0>), grid, block, lds, 0, g);
+            else if (variant == 1) hipLaunchKernelGGL((tail_probe<1, 1, 0>), grid, block, lds, 0, g);
+            else if (variant == 2) hipLaunchKernelGGL((tail_probe<1, 1, 1>), grid, block, lds, 0, g);
+            else hipLaunchKernelGGL((tail_probe<1, 1, 2>), grid, block, lds, 0, g);
+          } else {
+            if (variant == 0) hipLaunchKernelGGL((tail_probe<3, 0, 0>), grid, block, lds, 0, g);
+            else if (variant == 1) hipLaunchKernelGGL((tail_probe<3, 1, 0>), grid, block, lds, 0, g);
+            else if (variant == 2) hipLaunchKernelGGL((tail_probe<3, 1, 1>), grid, block, lds, 0, g);
+            else hipLaunchKernelGGL((tail_probe<3, 1, 2>), grid, block, lds, 0, g);
+          }
+        };
+        const double ms = best_ms(launch, 5);
+        CK(hipGetLastError());
+        std::printf("{\"pattern\": \"%s\", \"variant\": \"%s\", \"blocks_per_cu\": %d, \"gbs\": %.1f}\n",
+                    kNames[pat], vname[variant], k, kStreams[pat] * static_cast<double>(bytes) / ms / 1e6);
+        std::fflush(stdout);
+      };
+      for (int pat : {1, 3})
+        for (int k : {2, 3, 4, 6, 0})
+          for (int variant = 0; variant < 4; ++variant) one(pat, variant, k);
+      CK(hipFree(d_ts));
+      CK(hipFree(d_segs));
+      CK(hipFree(parts));
+    } else {
+      int dev = 0, cus = 0;
+      CK(hipGetDevice(&dev));
+      CK(hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev));
+      CK(hipDeviceSynchronize());
+      for (int pat : {1, 3, 2})
+        for (int k : {1, 2, 4}) {
+          const unsigned lds = lds_for(k);
+          if (lds == 0) continue;
+          const double ms1 = best_ms(
+              [&] {
+                if (pat == 1) hipLaunchKernelGGL((probe<1, 2, 256>), dim3(tiles), dim3(256), lds, 0, a, b, sink);
+                else if (pat == 3) hipLaunchKernelGGL((probe<3, 2, 256>), dim3(tiles), dim3(256), lds, 0, a, b, sink);
+                else hipLaunchKernelGGL((probe<2, 2, 256>), dim3(tiles), dim3(256), lds, 0, a, b, sink);
+              },
+              5);
+          CK(hipGetLastError());
+          // G blocks per launch, all resident at once (k per CU); each walks
+          // per = tiles / G tiles, an even count
+          const unsigned G = static_cast<unsigned>(k * cus);
+          const bool fits = G > 0 && G % 8 == 0 && (tiles / 8) % (G / 8) == 0 && (tiles / G) % 2 == 0;
+          double ms_stride = 0.0, ms_runs = 0.0;
+          if (fits) {
+            ms_stride = best_ms(
+                [&] {
+                  if (pat == 1) hipLaunchKernelGGL((persist_probe<1, 0>), dim3(G), dim3(256), lds, 0, a, b, sink, tiles);
+                  else if (pat == 3) hipLaunchKernelGGL((persist_probe<3, 0>), dim3(G), dim3(256), lds, 0, a, b, sink, tiles);
+                  else hipLaunchKernelGGL((persist_probe<2, 0>), dim3(G), dim3(256), lds, 0, a, b, sink, tiles);
+                },
+                5);
+            CK(hipGetLastError());
+            ms_runs = best_ms(
+                [&] {
+                  if (pat == 1) hipLaunchKernelGGL((persist_probe<1, 1>), dim3(G), dim3(256), lds, 0, a, b, sink, tiles);
+                  else if (pat == 3) hipLaunchKernelGGL((persist_probe<3, 1>), dim3(G), dim3(256), lds, 0, a, b, sink, tiles);
+                  else hipLaunchKernelGGL((persist_probe<2, 1>), dim3(G), dim3(256), lds, 0, a, b, sink, tiles);
+                },
+                5);
+            CK(hipGetLastError());
+          }
+          const double rate = kStreams[pat] * static_cast<double>(bytes) / 1e6;
+          std::printf("{\"pattern\": \"%s\", \"blocks_per_cu\": %d, \"one_tile_per_block_gbs\": %.1f, "
+                      "\"persistent_grid_stride_gbs\": %.1f, \"persistent_runs_gbs\": %.1f}\n",
+                      kNames[pat], k, rate / ms1, fits ? rate / ms_stride : 0.0, fits ? rate / ms_runs : 0.0);
+          std::fflush(stdout);
+        }
+    }
+    CK(hipFree(a));
+    CK(hipFree(b));
     CK(hipFree(sink));
     return 0;
   }

@@ -43,20 +43,22 @@ constexpr uint32_t kSelectThreads = 256;
 // Resident blocks per CU of the streaming kernels (0: as many as registers
 // and waves allow), held there by a dynamic LDS reservation the kernel never
 // touches.  Fewer streams open at once let HBM turn between reads and writes
-// less often; kernels that only read, and kernels whose per-block table
-// lookups need many blocks to hide their latency, want more.  Measured on
+// less often; kernels that only read, and kernels that end each block with a
+// reduction (its tail leaves the block's slot without loads in flight), want
+// more.  Measured on
 // MI355X, same arrays, one process (GB/s, unreserved -> reserved):
 //   ACCUM score (two reads, one write), 4 per CU: 8B 6425 -> 6688,
 //     70B shard 6230 -> 6324, 13B 6070 -> 6158, Qwen2.5-14B 6414 -> 6574;
 //     2 per CU loses 14%, 3 ties 4 on the larger states;
-//   SNAPSHOT score (two reads): unreserved is best (4 per CU: -2%);
+//   SNAPSHOT score (two reads), 5 per CU: 8B 6960 -> 7224, 13B 7069 -> 7232,
+//     Qwen2.5-14B 6590 -> 6733, 70B shard 6990 -> 7219 (3 and 4 per CU lose);
 //   pack and unpack (copies), 6 per CU: +0.2..1.8% (3 per CU: -12%);
-//   fused AdamW, 2 per CU: 5930 -> 6004; fused SGD: no gain at 2..5.
+//   fused AdamW, 2 per CU: 5930 -> 6004; fused SGD: no gain at 2..6.
 #ifndef LC_SCORE_ACCUM_BLOCKS_PER_CU
 #define LC_SCORE_ACCUM_BLOCKS_PER_CU 4
 #endif
 #ifndef LC_SCORE_SNAPSHOT_BLOCKS_PER_CU
-#define LC_SCORE_SNAPSHOT_BLOCKS_PER_CU 0
+#define LC_SCORE_SNAPSHOT_BLOCKS_PER_CU 5
 #endif
 #ifndef LC_COPY_BLOCKS_PER_CU
 #define LC_COPY_BLOCKS_PER_CU 6
