@@ -16,6 +16,10 @@ SRC = open(O.__file__).read()
 
 MUTANTS = {
     "denominator_uses_current": ("B += float(np.sum(np.abs(y)))", "B += float(np.sum(np.abs(x)))"),
+    "widen_bf16_as_fp16": ("return (values.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)",
+                           "return values.view(np.float16).astype(np.float64)"),
+    "widen_drops_low_byte": ("return (values.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)",
+                             "return ((values.astype(np.uint32) & np.uint32(0xFF00)) << np.uint32(16)).view(np.float32).astype(np.float64)"),
     "signed_difference": ("A += float(np.sum(np.abs(x - y)))", "A += float(np.sum(x - y))"),
     "eps_dropped": ("np.float64(B / n + eps_w)", "np.float64(B / n)"),
     "eps_outside_mean": ("np.float64(B / n + eps_w)", "np.float64((B + eps_w) / n)"),
