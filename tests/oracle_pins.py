@@ -373,7 +373,12 @@ def check_stats_invariants(cls, mode=O.MODE_ACCUM):
             # weighted staleness: an explicit sum over layers
             assert abs(st["weighted_age"] - sum(a * b for a, b in zip(n, ages)) / sum(n)) <= 1e-12 * max(1, st["max_age"])
             assert st["n_selected"] == int(mask.sum())
-            orc.pack(0, 1 << 40)
+            # payload: the selected layers' records, each block (bf16 W, fp32
+            # master, m, v of every tensor) padded to 256 B, written out here
+            rec = [sum(-(-x * 2 // 256) * 256 + 3 * (-(-x * 4 // 256) * 256) for x in sizes[l]) for l in range(N)]
+            assert st["payload_bytes"] == sum(rec[l] for l in range(N) if mask[l]), (st, rec, list(mask))
+            payload, res = orc.pack(0, 1 << 40)
+            assert res["bytes_written"] == len(payload) == st["payload_bytes"]
 
 
 # ---------------------------------------------------------------- records ---

@@ -63,6 +63,10 @@ MUTANTS = {
                                   'off = sum(self.R[j] for j in range(l))'),
     "restore_keeps_old_shadow": ("            for s in self.by_layer[l]:\n                s.shadow[...] = s.weight\n            self.delta[l] = 0.0",
                                  "            self.delta[l] = 0.0"),
+    "stats_ages_before_reset": ("ages = [step - self.t_last[l] for l in range(self.N)]",
+                                "ages = [step - self._pre_t_last[l] for l in range(self.N)]"),
+    "payload_counts_every_layer": ('"payload_bytes": sum(self.R[l] for l in range(self.N) if mask[l]),',
+                                   '"payload_bytes": sum(self.R),'),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
