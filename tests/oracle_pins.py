@@ -502,6 +502,36 @@ def check_restore_errors(cls):
     assert orc.restore([base, part], 3).tolist() == [3, 0]
 
 
+def check_call_order_errors(cls):
+    # The interface's call rules, which the oracle mirrors so that refusals
+    # compare between the two sides: decision steps strictly increase; select
+    # takes a positive, finite s(lr); a pack starts at a rank inside the
+    # selection; a restore at t_fail resumes the run at t_fail + 1, also below
+    # the last step before the failure; a base may not precede the last step.
+    lay = HostLayout([[5], [3, 2]], seed=12)
+    orc = cls(lay.segs, 2, O.DT_BF16, True, O.MODE_ACCUM, [1e-3] * 2, s_max=4)
+    payload, _ = orc.pack(0, 1 << 30)
+    base = {"step": 0, "mask": np.ones(2, np.uint8), "payload": payload}
+    for t in (1, 2, 3):
+        lay.step([1.0, 1.0])
+        orc.score(t)
+        expect_error(lambda: orc.score(t), O.LC_ERR_BAD_STATE)
+        for bad in (0.0, -1.0, float("nan"), float("inf")):
+            expect_error(lambda: orc.select(t, bad), O.LC_ERR_INVALID_ARG)
+        mask, st = orc.select(t, 1.0)
+        expect_error(lambda: orc.pack(st["n_selected"] + 1, 1 << 30), O.LC_ERR_INVALID_ARG)
+        orc.pack(0, 1 << 30)
+    expect_error(lambda: orc.score(2), O.LC_ERR_BAD_STATE)
+    expect_error(lambda: orc.rebase(2), O.LC_ERR_BAD_STATE)
+    assert orc.restore([base], 1).tolist() == [0, 0]
+    expect_error(lambda: orc.score(1), O.LC_ERR_BAD_STATE)
+    lay.step([1.0, 1.0])
+    orc.score(2)  # below the step reached before the failure: the resumed run
+    orc.select(2, 1.0)
+    orc.pack(0, 1 << 30)
+    orc.rebase(2)  # a base at the last step is allowed
+
+
 def check_accum_equals_snapshot_first_step(cls):
     la = HostLayout([[30, 2], [50]], seed=10)
     lb = HostLayout([[30, 2], [50]], seed=10)

@@ -67,6 +67,12 @@ MUTANTS = {
                                 "ages = [step - self._pre_t_last[l] for l in range(self.N)]"),
     "payload_counts_every_layer": ('"payload_bytes": sum(self.R[l] for l in range(self.N) if mask[l]),',
                                    '"payload_bytes": sum(self.R),'),
+    "score_allows_repeat_step": ("    def score(self, step: int) -> None:\n        if step <= self.last_step:",
+                                 "    def score(self, step: int) -> None:\n        if step < self.last_step:"),
+    "restore_keeps_last_step": ("        self.last_step = t_fail\n        self.scored_step = None\n        self.mask = None",
+                                "        self.scored_step = None\n        self.mask = None"),
+    "select_accepts_bad_lr_scale": ('        if not (lr_scale > 0.0) or lr_scale == float("inf"):', "        if False:"),
+    "pack_first_rank_unchecked": ('        if first_rank < 0 or first_rank > len(sel):\n            raise OracleError(LC_ERR_INVALID_ARG, "first_rank out of range")\n', ""),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
@@ -134,6 +140,7 @@ def all_checks(M):
     yield lambda: P.check_bf16_round(M.bf16_round)
     for c in (P.check_ge_threshold, P.check_k0_extremes, P.check_record_format, P.check_capacity,
               P.check_restore_errors, P.check_accum_equals_snapshot_first_step, P.check_resync,
+              P.check_call_order_errors,
               P.check_unpacked_selection_blocks):
         yield lambda c=c: c(cls)
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):

@@ -148,6 +148,9 @@ def test_restore_composite_then_continue(where):
         chosen = _restore_and_compare(p, t_fail, where)
         log(f"  restored from steps {sorted(set(chosen.tolist()))}")
         assert len(set(chosen.tolist())) >= 2
+        with pytest.raises(LC.LCError) as e:  # the resumed run starts after t_fail
+            LC.lc_score_layers(p.ctx, t_fail)
+        assert e.value.code == LC.LC_ERR_BAD_STATE
         p.adopt_restored()  # resume from the composite state
         run_steps(p, range(t_fail + 1, t_fail + 4))
     finally:
@@ -344,8 +347,8 @@ def test_state_machine_errors():
         p.pack(0, np.ones(p.N, np.uint8))
         p.advance(1)
         p.score(1)
-        expect(I_, lambda: LC.lc_select(p.ctx, 1, 0.0, p.N))
-        expect(I_, lambda: LC.lc_select(p.ctx, 1, float("inf"), p.N))
+        for bad in (0.0, -1.0, float("nan"), float("inf")):
+            expect(I_, lambda: LC.lc_select(p.ctx, 1, bad, p.N))
         expect(B, lambda: LC.lc_select(p.ctx, 2, 1.0, p.N))
         expect(B, lambda: LC.lc_score_layers(p.ctx, 1))        # not increasing
         d, tl = LC.lc_read_state(p.ctx, p.N)[1:]
@@ -359,6 +362,7 @@ def test_state_machine_errors():
         expect(I_, lambda: LC.lc_restore_composite(p.ctx, [v0, dict(v0)], 3, p.N))
         expect(I_, lambda: LC.lc_restore_composite(p.ctx, [dict(v0, payload_bytes=sum(p.R) - 256)], 3, p.N))
         expect(I_, lambda: LC.lc_restore_composite(p.ctx, [], 3, p.N))
+        expect(B, lambda: LC.lc_rebase(p.ctx, 0))              # a base before the last step
         p.check_arrays()  # failed calls changed nothing
     finally:
         p.close()
