@@ -406,12 +406,70 @@ def check_record_format(cls):
     assert bytes(payload[off + 1280:off + 1792]) == s2.exp_avg_sq.tobytes()
 
 
+def check_record_format_weights_only(cls):
+    # Section 4.7 (SGD): a layout without Adam moments persists the weights
+    # (and the fp32 master) only: bf16 W blocks, then master blocks, each
+    # padded to 256 B -- 6 B per parameter when nothing is padded.
+    rng = np.random.default_rng(13)
+    segs = []
+    for l, n in ((0, 128), (0, 3), (1, 256)):
+        base = (rng.standard_normal(n) * 0.02).astype(np.float32)
+        segs.append(O.OSegment(l, f32_to_bf16_bits(base), np.zeros(n, np.uint16), base.copy(), None, None))
+    orc = cls(segs, 2, O.DT_BF16, True, O.MODE_ACCUM, [1e-3, 1e-3], s_max=4)
+    assert orc.R == [256 + 256 + 512 + 256, 512 + 1024], orc.R
+    payload, res = orc.pack(0, 1 << 30)
+    assert res["bytes_written"] == len(payload) == 1280 + 1536
+    s0, s1, s2 = segs
+    assert bytes(payload[0:256]) == s0.weight.tobytes()
+    assert bytes(payload[256:262]) == s1.weight.tobytes() and not payload[262:512].any()
+    assert bytes(payload[512:1024]) == s0.master.tobytes()
+    assert bytes(payload[1024:1036]) == s1.master.tobytes() and not payload[1036:1280].any()
+    assert bytes(payload[1280:1792]) == s2.weight.tobytes()
+    assert bytes(payload[1792:2816]) == s2.master.tobytes()
+
+
+def check_fused_step_rules(cls):
+    # The fused optimizer step replaces the score of its step: select follows
+    # it at the same step; it accumulates (Eq. 2), so SNAPSHOT mode refuses
+    # it; AdamW needs the moment arrays.
+    lay = HostLayout([[40], [24, 8]], seed=14)
+    grads = [np.full(s.numel, 0.5, np.float32) for s in lay.segs]
+    orc = cls(lay.segs, 2, O.DT_BF16, True, O.MODE_ACCUM, [1e9, 1e9], s_max=2)
+    orc.pack(0, 1 << 30)
+    orc.adamw_step_score(1, grads, 1e-3, 0.9, 0.95, 1e-8, 0.0, 1)
+    u1 = list(orc.u)
+    mask, st = orc.select(1, 1.0)
+    assert list(mask) == [0, 0] and st["max_age"] == 1
+    orc.pack(0, 1 << 30)
+    orc.sgd_step_score(2, grads, 1e-3, 0.0)
+    mask, st = orc.select(2, 1.0)  # age 2 = S_max: both forced, Delta reset
+    assert list(mask) == [1, 1] and st["n_forced"] == 2 and orc.delta == [0.0, 0.0]
+    assert all(x > 0 for x in u1)
+    lay2 = HostLayout([[40]], seed=15)
+    snap = cls(lay2.segs, 1, O.DT_BF16, True, O.MODE_SNAPSHOT, [1e9], s_max=2)
+    snap.pack(0, 1 << 30)
+    g2 = [np.full(s.numel, 0.5, np.float32) for s in lay2.segs]
+    expect_error(lambda: snap.adamw_step_score(1, g2, 1e-3, 0.9, 0.95, 1e-8, 0.0, 1), O.LC_ERR_BAD_STATE)
+    expect_error(lambda: snap.sgd_step_score(1, g2, 1e-3, 0.0), O.LC_ERR_BAD_STATE)
+    n = 16
+    base = np.full(n, 0.25, np.float32)
+    bare = cls([O.OSegment(0, f32_to_bf16_bits(base), np.zeros(n, np.uint16), base.copy(), None, None)], 1,
+               O.DT_BF16, True, O.MODE_ACCUM, [1e9], s_max=2)
+    expect_error(lambda: bare.adamw_step_score(1, [np.ones(n, np.float32)], 1e-3, 0.9, 0.95, 1e-8, 0.0, 1),
+                 O.LC_ERR_BAD_STATE)
+    bare.sgd_step_score(1, [np.ones(n, np.float32)], 2.0 ** -4, 0.0)  # SGD needs none
+    assert bare.by_layer[0][0].master[0] == np.float32(0.25 - 2.0 ** -4)
+
+
 def check_fourteen_bytes_per_param():
     # pad-free blocks (every tensor a multiple of 128 elements): 2 + 4 + 4 + 4 bytes
     assert O.record_bytes([128 * 7, 4096], 2, True) == 14 * (128 * 7 + 4096)
     assert O.record_bytes([128 * 7, 4096], 2, False) == 10 * (128 * 7 + 4096)
     assert O.record_bytes([64 * 3], 4, False) == 12 * 64 * 3
     assert O.record_bytes([1], 2, True) == 4 * 256
+    # without Adam moments (Section 4.7): weights and master only
+    assert O.record_bytes([128 * 5], 2, True, False) == 6 * 128 * 5
+    assert O.record_bytes([128 * 5], 2, False, False) == 2 * 128 * 5
 
 
 def check_capacity(cls):

@@ -73,6 +73,13 @@ MUTANTS = {
                                 "        self.scored_step = None\n        self.mask = None"),
     "select_accepts_bad_lr_scale": ('        if not (lr_scale > 0.0) or lr_scale == float("inf"):', "        if False:"),
     "pack_first_rank_unchecked": ('        if first_rank < 0 or first_rank > len(sel):\n            raise OracleError(LC_ERR_INVALID_ARG, "first_rank out of range")\n', ""),
+    "record_moments_when_absent": ('            + (["exp_avg", "exp_avg_sq"] if has_moments else []))',
+                                   '            + ["exp_avg", "exp_avg_sq"])'),
+    "fused_step_in_snapshot": ('        if self.mode != MODE_ACCUM:\n            raise OracleError(LC_ERR_BAD_STATE, "the fused optimizer step accumulates (ACCUM mode)")\n', ''),
+    "fused_step_not_selectable": ('        self.last_step = step\n        self.scored_step = step\n        self.unpacked = set()\n        self.mask = None\n\n    def adamw_step_score',
+                                  '        self.last_step = step\n        self.unpacked = set()\n        self.mask = None\n\n    def adamw_step_score'),
+    "sgd_decay_scales_the_step": ('    return (p1 - (sc["lr"] * g.astype(f)).astype(f)).astype(f)',
+                                  '    return (p1 - (sc["lr"] * sc["decay"] * g.astype(f)).astype(f)).astype(f)'),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
@@ -140,7 +147,7 @@ def all_checks(M):
     yield lambda: P.check_bf16_round(M.bf16_round)
     for c in (P.check_ge_threshold, P.check_k0_extremes, P.check_record_format, P.check_capacity,
               P.check_restore_errors, P.check_accum_equals_snapshot_first_step, P.check_resync,
-              P.check_call_order_errors,
+              P.check_call_order_errors, P.check_record_format_weights_only, P.check_fused_step_rules,
               P.check_unpacked_selection_blocks):
         yield lambda c=c: c(cls)
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
@@ -154,7 +161,8 @@ def all_checks(M):
         yield lambda mode=mode: run_bruteforce(M, mode, O.DT_BF16, 0, steps=12)
     for chk in (A.test_first_step_is_lr_times_sign, A.test_decoupled_weight_decay_on_zero_gradient,
                 A.test_matches_torch_adamw_over_steps, A.test_fused_step_drift_is_eq1_on_the_parameters,
-                G.test_closed_form_exact, G.test_decoupled_weight_decay, G.test_matches_torch_sgd,
+                G.test_closed_form_exact, G.test_decay_and_gradient_together, G.test_decoupled_weight_decay,
+                G.test_matches_torch_sgd,
                 G.test_drift_is_eq1_on_the_parameters):
         yield lambda chk=chk: chk(M)
 

@@ -22,6 +22,18 @@ def test_closed_form_exact(O=O_real):
     assert O.sgd_update(p, g, sc, True)[3] == -0.5
 
 
+def test_decay_and_gradient_together(O=O_real):
+    # lr = 2^-4, wd = 2^-2: decay = 1 - 2^-6 exactly; p (1 - lr wd) - lr g with
+    # every operation exact, so the decay multiplies p alone, not the step
+    sc = O.sgd_scalars(2.0 ** -4, 2.0 ** -2)
+    assert sc["decay"] == np.float32(1.0 - 2.0 ** -6)
+    p = np.array([1.0, 0.5, -2.0], np.float32)
+    g = np.array([1.0, -2.0, 4.0], np.float32)
+    exp = np.array([1.0 - 2.0 ** -6 - 2.0 ** -4, 0.5 - 2.0 ** -7 + 2.0 ** -3, -2.0 + 2.0 ** -5 - 2.0 ** -2], np.float32)
+    assert np.array_equal(O.sgd_update(p, g, sc, True), exp)
+    assert np.array_equal(O.sgd_update(p, g, sc, False), p - np.float32(2.0 ** -4) * g)
+
+
 def test_decoupled_weight_decay(O=O_real):
     sc = O.sgd_scalars(1e-2, 0.1)
     p = np.array([1.0, -2.0, 0.375], np.float32)
