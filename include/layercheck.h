@@ -102,7 +102,7 @@ typedef struct {
   const double *k0;           /* host [n_layers]: base thresholds K0_l >= 0
                                  (Section 3.4 uses 1e-3, 1e-2 for embeddings) */
   int64_t s_max;              /* staleness bound S_max >= 1 (Eq. 5)            */
-  double eps_w;               /* Eq. 1 stabiliser, >= 0 (e.g. 1e-8)            */
+  double eps_w;               /* Eq. 1 stabiliser, finite and >= 0 (e.g. 1e-8) */
   int64_t t_base;             /* step of the base full checkpoint (Sec. 3.4)   */
   void *stream;               /* hipStream_t, borrowed; NULL = null stream     */
 } lc_layout_desc;

@@ -254,8 +254,10 @@ class LayerCheckOracle:
             raise OracleError(LC_ERR_INVALID_ARG, "empty layout")
         if weight_dtype not in (DT_BF16, DT_F32) or mode not in (MODE_ACCUM, MODE_SNAPSHOT):
             raise OracleError(LC_ERR_INVALID_ARG, "bad dtype or mode")
-        if len(k0) != n_layers or s_max < 1 or not (eps_w >= 0.0):
+        if len(k0) != n_layers or s_max < 1 or not (eps_w >= 0.0) or eps_w == float("inf"):
             raise OracleError(LC_ERR_INVALID_ARG, "bad thresholds")
+        if not all(k >= 0.0 for k in k0):  # refuses NaN too
+            raise OracleError(LC_ERR_INVALID_ARG, "K0 must be >= 0")
         self.by_layer: List[List[OSegment]] = [[] for _ in range(n_layers)]
         self.has_moments = segments[0].exp_avg is not None
         last = -1

@@ -486,6 +486,62 @@ def check_capacity(cls):
     assert bytes(np.concatenate([p0, p1])) == bytes(full)
 
 
+def check_snapshot_partial_pack_refresh(cls):
+    # SNAPSHOT mode refreshes the shadow of the layers a pack call writes, and
+    # only those: after a capacity-limited first call the other selected
+    # layers still hold their last persisted weights in the shadow.
+    lay = HostLayout([[100], [300], [50]], seed=16)
+    orc = cls(lay.segs, 3, O.DT_BF16, True, O.MODE_SNAPSHOT, [0.0] * 3, s_max=4)
+    orc.pack(0, 1 << 30)
+    old = [s.weight.copy() for s in lay.segs]
+    lay.step([1.0, 1.0, 1.0])
+    orc.score(1)
+    mask, _ = orc.select(1, 1.0)
+    assert list(mask) == [1, 1, 1]
+    _, r = orc.pack(0, orc.R[0])
+    assert r["n_packed"] == 1
+    segs = lay.segs
+    assert np.array_equal(segs[0].shadow, segs[0].weight)
+    for i in (1, 2):
+        assert np.array_equal(segs[i].shadow, old[i]) and not np.array_equal(segs[i].shadow, segs[i].weight)
+    orc.pack(1, 1 << 30)
+    assert all(np.array_equal(s_.shadow, s_.weight) for s_ in segs)
+
+
+def check_layout_validation(cls):
+    # Layouts the interface refuses (LC_ERR_INVALID_ARG), mirrored by the oracle.
+    def segs(layers, master=(True,), moments=(True,)):
+        out = []
+        for i, l in enumerate(layers):
+            n = 4
+            base = np.full(n, 0.5, np.float32)
+            ma = master[i % len(master)]
+            mo = moments[i % len(moments)]
+            out.append(O.OSegment(l, f32_to_bf16_bits(base), np.zeros(n, np.uint16), base.copy() if ma else None,
+                                  np.zeros(n, np.float32) if mo else None, np.zeros(n, np.float32) if mo else None))
+        return out
+
+    def refused(fn):
+        expect_error(fn, O.LC_ERR_INVALID_ARG)
+
+    ok = dict(weight_dtype=O.DT_BF16, has_master=True, mode=O.MODE_ACCUM, k0=[1e-3, 1e-3], s_max=4)
+    cls(segs([0, 1]), 2, **ok)  # the accepted form
+    refused(lambda: cls(segs([1, 0]), 2, **ok))                       # layers not grouped in order
+    refused(lambda: cls(segs([0, 0]), 2, **ok))                       # layer 1 has no tensor
+    refused(lambda: cls(segs([0, 2]), 2, **ok))                       # layer out of range
+    refused(lambda: cls([], 2, **ok))                                 # empty layout
+    refused(lambda: cls(segs([0, 1], master=(True, False)), 2, **ok))  # master on some tensors only
+    refused(lambda: cls(segs([0, 1], moments=(True, False)), 2, **ok))  # moments on some tensors only
+    refused(lambda: cls(segs([0, 1]), 2, **dict(ok, s_max=0)))        # S_max < 1
+    refused(lambda: cls(segs([0, 1]), 2, **dict(ok, k0=[1e-3])))      # one K0 per layer
+    refused(lambda: cls(segs([0, 1]), 2, **dict(ok, mode=7)))         # unknown mode
+    refused(lambda: cls(segs([0, 1]), 2, **dict(ok, weight_dtype=9)))  # unknown weight type
+    for eps in (-1e-8, float("nan"), float("inf")):
+        refused(lambda: cls(segs([0, 1]), 2, eps_w=eps, **ok))         # eps_w finite, >= 0
+    for k in (-1e-3, float("nan")):
+        refused(lambda: cls(segs([0, 1]), 2, **dict(ok, k0=[1e-3, k])))  # K0 >= 0
+
+
 # ---------------------------------------------------------------- recovery --
 
 def check_restore_roundtrip(cls, mode=O.MODE_ACCUM):

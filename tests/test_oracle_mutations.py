@@ -80,6 +80,17 @@ MUTANTS = {
                                   '        self.last_step = step\n        self.unpacked = set()\n        self.mask = None\n\n    def adamw_step_score'),
     "sgd_decay_scales_the_step": ('    return (p1 - (sc["lr"] * g.astype(f)).astype(f)).astype(f)',
                                   '    return (p1 - (sc["lr"] * sc["decay"] * g.astype(f)).astype(f)).astype(f)'),
+    "init_accepts_unordered_layers": ("if not (0 <= s.layer < n_layers) or s.layer < last or s.numel == 0:",
+                                      "if not (0 <= s.layer < n_layers) or s.numel == 0:"),
+    "init_accepts_master_mismatch": ('            if (s.master is None) == has_master:\n                raise OracleError(LC_ERR_INVALID_ARG, "master presence mismatch")\n', ""),
+    "init_accepts_smax_zero": ("if len(k0) != n_layers or s_max < 1 or not (eps_w >= 0.0)",
+                               "if len(k0) != n_layers or s_max < 0 or not (eps_w >= 0.0)"),
+    "init_accepts_negative_eps": ("or not (eps_w >= 0.0) or eps_w", "or eps_w"),
+    "init_accepts_infinite_eps": ('or not (eps_w >= 0.0) or eps_w == float("inf"):', "or not (eps_w >= 0.0):"),
+    "init_accepts_missing_layer": ('        if any(len(g) == 0 for g in self.by_layer):\n            raise OracleError(LC_ERR_INVALID_ARG, "layer without tensors")\n', ""),
+    "snapshot_pack_refreshes_unpacked": ("            for l in sel[first_rank:last]:\n                for s in self.by_layer[l]:\n                    s.shadow[...] = s.weight",
+                                         "            for l in sel:\n                for s in self.by_layer[l]:\n                    s.shadow[...] = s.weight"),
+    "init_accepts_negative_k0": ("        if not all(k >= 0.0 for k in k0):  # refuses NaN too", "        if False:"),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
@@ -148,6 +159,7 @@ def all_checks(M):
     for c in (P.check_ge_threshold, P.check_k0_extremes, P.check_record_format, P.check_capacity,
               P.check_restore_errors, P.check_accum_equals_snapshot_first_step, P.check_resync,
               P.check_call_order_errors, P.check_record_format_weights_only, P.check_fused_step_rules,
+              P.check_snapshot_partial_pack_refresh, P.check_layout_validation,
               P.check_unpacked_selection_blocks):
         yield lambda c=c: c(cls)
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):

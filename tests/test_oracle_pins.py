@@ -19,6 +19,7 @@ def test_score_pins(check):
                                    P.check_capacity, P.check_restore_errors,
                                    P.check_accum_equals_snapshot_first_step, P.check_resync, P.check_call_order_errors,
                                    P.check_record_format_weights_only, P.check_fused_step_rules,
+                                   P.check_snapshot_partial_pack_refresh, P.check_layout_validation,
                                    P.check_unpacked_selection_blocks],
                          ids=lambda f: f.__name__)
 def test_state_pins(check):
