@@ -175,6 +175,9 @@ class Pair:
             self.torch.cuda.synchronize()
             got = torch_bytes(staging[:res["bytes_written"]]) if res["bytes_written"] else np.zeros(0, np.uint8)
             assert np.array_equal(got, pay_o), f"step {t}: payload differs at rank {rank}"
+            # SNAPSHOT refreshes the shadow of the layers each call writes, and only
+            # those: compare after every call, not only after the last
+            self.check_shadow()
             parts_g.append(got)
             parts_o.append(pay_o)
             if res["done"]:
@@ -187,7 +190,6 @@ class Pair:
             dev = self.torch.from_numpy(np.concatenate(parts_g)).to("cuda") if total else None
             self.versions_dev.append((t, mask.copy(), dev))
             self.versions_host.append((t, mask.copy(), payload))
-        self.check_shadow()
         return payload
 
     def check_shadow(self):
