@@ -609,7 +609,9 @@ def check_restore_errors(cls):
             ([part], 3, O.LC_ERR_NO_VERSION),
             ([base, part], -1, O.LC_ERR_NO_VERSION),
             ([base, dict(base)], 2, O.LC_ERR_INVALID_ARG),
-            ([base, {"step": 3, "mask": np.array([1, 0], np.uint8), "payload": payload}], 5, O.LC_ERR_INVALID_ARG)):
+            ([base, {"step": 3, "mask": np.array([1, 0], np.uint8), "payload": payload}], 5, O.LC_ERR_INVALID_ARG),
+            ([base, {"step": 3, "mask": np.array([1, 0, 0], np.uint8), "payload": payload[:orc.R[0]]}], 5,
+             O.LC_ERR_INVALID_ARG)):
         expect_error(lambda: orc.restore(versions, t_fail), code)
     # a version newer than t_fail is ignored
     assert orc.restore([base, part], 2).tolist() == [0, 0]
@@ -630,15 +632,18 @@ def check_call_order_errors(cls):
         lay.step([1.0, 1.0])
         orc.score(t)
         expect_error(lambda: orc.score(t), O.LC_ERR_BAD_STATE)
+        expect_error(lambda: orc.pack(0, 1 << 30), O.LC_ERR_BAD_STATE)  # nothing selected yet
         for bad in (0.0, -1.0, float("nan"), float("inf")):
             expect_error(lambda: orc.select(t, bad), O.LC_ERR_INVALID_ARG)
         mask, st = orc.select(t, 1.0)
+        expect_error(lambda: orc.select(t, 1.0), O.LC_ERR_BAD_STATE)  # one select per score
         expect_error(lambda: orc.pack(st["n_selected"] + 1, 1 << 30), O.LC_ERR_INVALID_ARG)
         orc.pack(0, 1 << 30)
     expect_error(lambda: orc.score(2), O.LC_ERR_BAD_STATE)
     expect_error(lambda: orc.rebase(2), O.LC_ERR_BAD_STATE)
     assert orc.restore([base], 1).tolist() == [0, 0]
     expect_error(lambda: orc.score(1), O.LC_ERR_BAD_STATE)
+    expect_error(lambda: orc.select(1, 1.0), O.LC_ERR_BAD_STATE)  # a restore is no score
     lay.step([1.0, 1.0])
     orc.score(2)  # below the step reached before the failure: the resumed run
     orc.select(2, 1.0)

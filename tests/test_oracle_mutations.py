@@ -91,6 +91,10 @@ MUTANTS = {
     "snapshot_pack_refreshes_unpacked": ("            for l in sel[first_rank:last]:\n                for s in self.by_layer[l]:\n                    s.shadow[...] = s.weight",
                                          "            for l in sel:\n                for s in self.by_layer[l]:\n                    s.shadow[...] = s.weight"),
     "init_accepts_negative_k0": ("        if not all(k >= 0.0 for k in k0):  # refuses NaN too", "        if False:"),
+    "plan_skips_mask_length": ('            if m.shape != (self.N,):\n                raise OracleError(LC_ERR_INVALID_ARG, "mask length")\n', ''),
+    "pack_without_selection": ('        if self.mask is None:\n            raise OracleError(LC_ERR_BAD_STATE, "nothing selected")\n', ''),
+    "restore_leaves_a_score": ("        self.last_step = t_fail\n        self.scored_step = None", "        self.last_step = t_fail\n        self.scored_step = t_fail"),
+    "select_twice_per_score": ("        self.scored_step = None\n        self.mask = mask\n        self.mask_step = step", "        self.mask = mask\n        self.mask_step = step"),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",

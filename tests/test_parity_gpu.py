@@ -347,12 +347,14 @@ def test_state_machine_errors():
         p.pack(0, np.ones(p.N, np.uint8))
         p.advance(1)
         p.score(1)
+        expect(B, lambda: LC.lc_pack_selected(p.ctx, st.data_ptr(), max(p.R), 0))  # nothing selected yet
         for bad in (0.0, -1.0, float("nan"), float("inf")):
             expect(I_, lambda: LC.lc_select(p.ctx, 1, bad, p.N))
         expect(B, lambda: LC.lc_select(p.ctx, 2, 1.0, p.N))
         expect(B, lambda: LC.lc_score_layers(p.ctx, 1))        # not increasing
         d, tl = LC.lc_read_state(p.ctx, p.N)[1:]
         mask, _ = p.select(1, 1.0, d, tl)
+        expect(B, lambda: LC.lc_select(p.ctx, 1, 1.0, p.N))   # one select per score
         p.pack(1, mask)
         # restore errors
         full = np.ones(p.N, np.uint8)
