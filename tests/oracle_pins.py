@@ -181,6 +181,29 @@ def check_ge_threshold(cls):
     assert list(mask) == [1, 1], mask
 
 
+def check_delta_in_fp64(cls):
+    # Reading #14: Delta accumulates in fp64.  One fp32 layer of 1024 elements
+    # at 1.0: step 1 doubles every element (u = 1 exactly), step 2 moves one
+    # element by one ulp of 2.0 (u = 2^-22 / 1024 / 2 = 2^-33 exactly).  With
+    # K0 = 1 + 2^-34 only an fp64 accumulator (1 + 2^-33) crosses; an fp32
+    # one stays at 1.0.
+    n = 1024
+    w = np.ones(n, np.float32)
+    segs = [O.OSegment(0, w, np.zeros(n, np.float32), w.copy(), np.zeros(n, np.float32), np.zeros(n, np.float32))]
+    orc = cls(segs, 1, O.DT_F32, True, O.MODE_ACCUM, [1.0 + 2.0 ** -34], s_max=100, eps_w=0.0)
+    orc.pack(0, 1 << 30)
+    w[...] = 2.0
+    orc.score(1)
+    assert orc.u == [1.0]
+    mask, _ = orc.select(1, 1.0)
+    assert list(mask) == [0]
+    w[0] = np.float32(2.0 + 2.0 ** -22)
+    orc.score(2)
+    assert orc.u == [2.0 ** -33] and orc.delta == [1.0 + 2.0 ** -33]
+    mask, _ = orc.select(2, 1.0)
+    assert list(mask) == [1]
+
+
 def check_staleness_period(cls, mode=O.MODE_ACCUM):
     # zero drift: each layer persists exactly at t_base + k*S_max
     for s_max in (1, 3, 4):

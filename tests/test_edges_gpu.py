@@ -178,6 +178,42 @@ def test_segment_larger_than_4gib_closed_form():
         LC.lc_destroy(ctx)
 
 
+def test_delta_accumulates_in_fp64():
+    """Eq. 2 in fp64 on the device: one fp32 layer of 1024 elements at 1.0,
+    doubled at step 1 (u = 1 exactly), then one element moved by one ulp of
+    2.0 at step 2 (u = 2^-33 exactly).  K0 = 1 + 2^-34 is crossed only by an
+    fp64 accumulator; the same construction pins the oracle."""
+    import torch
+    n = 1024
+    dev = torch.device("cuda")
+    W = torch.ones(n, dtype=torch.float32, device=dev)
+    S = torch.empty_like(W)
+    m = torch.zeros_like(W)
+    v = torch.zeros_like(W)
+    seg = LC.Segment(0, n, W.data_ptr(), S.data_ptr(), None, m.data_ptr(), v.data_ptr())
+    lay = LC.LayoutDesc([seg], 1, LC.LC_DT_F32, False, LC.LC_MODE_ACCUM, [1.0 + 2.0 ** -34], s_max=100, eps_w=0.0,
+                        stream=torch.cuda.current_stream().cuda_stream)
+    ctx = LC.lc_init_layout(lay)
+    try:
+        R = LC.lc_record_bytes(ctx, 0)
+        staging = torch.empty(R, dtype=torch.uint8, device=dev)
+        assert LC.lc_pack_selected(ctx, staging.data_ptr(), R, 0)["done"] == 1  # the base
+        W.fill_(2.0)
+        LC.lc_score_layers(ctx, 1)
+        mask, _ = LC.lc_select(ctx, 1, 1.0, 1)
+        u, d, _ = LC.lc_read_state(ctx, 1)
+        assert u[0] == 1.0 and mask.tolist() == [0]
+        W[0] = 2.0 + 2.0 ** -22
+        LC.lc_score_layers(ctx, 2)
+        u, d, _ = LC.lc_read_state(ctx, 1)
+        assert u[0] == 2.0 ** -33 and d[0] == 1.0 + 2.0 ** -33, (u[0], d[0])
+        mask, st = LC.lc_select(ctx, 2, 1.0, 1)
+        assert mask.tolist() == [1] and st["n_forced"] == 0
+        assert LC.lc_pack_selected(ctx, staging.data_ptr(), R, 0)["done"] == 1
+    finally:
+        LC.lc_destroy(ctx)
+
+
 def many_layer_spec(n_layers=1500, seed=11):
     """Many tiny layers of 1-3 tensors (1..300 elements each): the select
     kernel's per-layer loops and prefix tables, and packs of hundreds of

@@ -95,6 +95,8 @@ MUTANTS = {
     "pack_without_selection": ('        if self.mask is None:\n            raise OracleError(LC_ERR_BAD_STATE, "nothing selected")\n', ''),
     "restore_leaves_a_score": ("        self.last_step = t_fail\n        self.scored_step = None", "        self.last_step = t_fail\n        self.scored_step = t_fail"),
     "select_twice_per_score": ("        self.scored_step = None\n        self.mask = mask\n        self.mask_step = step", "        self.mask = mask\n        self.mask_step = step"),
+    "delta_accumulated_in_fp32": ("            if self.mode == MODE_ACCUM:\n                self.delta[l] = self.delta[l] + u",
+                                  "            if self.mode == MODE_ACCUM:\n                self.delta[l] = float(np.float32(self.delta[l] + u))"),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
@@ -160,7 +162,8 @@ def all_checks(M):
         P.check_exact_rational)]
     cls = M.LayerCheckOracle
     yield lambda: P.check_bf16_round(M.bf16_round)
-    for c in (P.check_ge_threshold, P.check_k0_extremes, P.check_record_format, P.check_capacity,
+    for c in (P.check_ge_threshold, P.check_delta_in_fp64, P.check_k0_extremes, P.check_record_format,
+              P.check_capacity,
               P.check_restore_errors, P.check_accum_equals_snapshot_first_step, P.check_resync,
               P.check_call_order_errors, P.check_record_format_weights_only, P.check_fused_step_rules,
               P.check_snapshot_partial_pack_refresh, P.check_layout_validation,

@@ -15,7 +15,8 @@ def test_score_pins(check):
     check(O.layer_update_score)
 
 
-@pytest.mark.parametrize("check", [P.check_ge_threshold, P.check_k0_extremes, P.check_record_format,
+@pytest.mark.parametrize("check", [P.check_ge_threshold, P.check_delta_in_fp64, P.check_k0_extremes,
+                                   P.check_record_format,
                                    P.check_capacity, P.check_restore_errors,
                                    P.check_accum_equals_snapshot_first_step, P.check_resync, P.check_call_order_errors,
                                    P.check_record_format_weights_only, P.check_fused_step_rules,
