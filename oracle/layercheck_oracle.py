@@ -30,8 +30,8 @@ What it computes, in the paper's notation:
   with step <= t_fail; the base full checkpoint is simply a version holding
   every layer.
 
-Readings where the paper is silent (each is listed with its reason in the
-design notes): eps_w is added to the *mean* exactly as Eq. 1 is typeset; the
+Readings where the paper is silent: eps_w is added to the *mean* exactly as
+Eq. 1 is typeset; the
 comparison operators are ">=" for both rules; the payload format (records of
 selected layers in ascending layer id, each record [W | master | m | v],
 every (array, tensor) block zero-padded to a multiple of 256 bytes) is this
@@ -51,7 +51,9 @@ Parity status: every function here is pinned by the ``-m "not gpu"`` tests
 (closed forms, exact-rational brute force, invariants, the paper's Table 1
 record-size and layer-count figures; ``bf16_round`` against hand-worked bit
 patterns and torch's independent conversion; ``resync`` against taking the
-same decision directly); no function is "parity unpinned".
+same decision directly; the call and layout rules against the interface's
+refusals), and the pins are themselves checked to fail on planted mistakes;
+no function is "parity unpinned".
 """
 from __future__ import annotations
 
