@@ -339,7 +339,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(json.dumps({"error": "the benchmark measures one GPU only; --gpus must be 1 "
-                                   "(the decision step is per-rank, see the design notes on sharding)"}))
+                                   "(the decision step is per-rank: each rank would run it on its own shard)"}))
         sys.exit(2)
     if args.ceilings:
         # a child process of its own: this process has not touched the GPU yet
