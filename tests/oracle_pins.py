@@ -664,7 +664,10 @@ def check_call_order_errors(cls):
         orc.pack(0, 1 << 30)
     expect_error(lambda: orc.score(2), O.LC_ERR_BAD_STATE)
     expect_error(lambda: orc.rebase(2), O.LC_ERR_BAD_STATE)
-    assert orc.restore([base], 1).tolist() == [0, 0]
+    lay.step([1.0, 1.0])
+    orc.score(4)
+    orc.select(4, 1.0)  # a selection left unpacked ...
+    assert orc.restore([base], 1).tolist() == [0, 0]  # ... is replaced by the restore
     expect_error(lambda: orc.score(1), O.LC_ERR_BAD_STATE)
     expect_error(lambda: orc.select(1, 1.0), O.LC_ERR_BAD_STATE)  # a restore is no score
     lay.step([1.0, 1.0])

@@ -5,7 +5,8 @@ update (Sections 3.4 and 4.1) without restating the optimizer, so the
 oracle follows the published AdamW definition.  Pins: the closed form of the
 first step (bias correction makes the update lr * sign(g)), decoupled weight
 decay on a zero gradient (p * (1 - lr wd), and nothing on a non-decayed
-group), agreement with torch.optim.AdamW (an independent implementation,
+group), eps added beside the root of v_hat (a gradient as small as eps),
+agreement with torch.optim.AdamW (an independent implementation,
 different rounding order) over several steps, and Eq. 1 on the optimizer's
 parameters for the drift.
 """
@@ -23,6 +24,17 @@ def test_first_step_is_lr_times_sign(O=O_real):
     ulp = np.spacing(np.float32(0.5))
     assert np.all(np.abs(p_new - (0.5 - 1e-3 * np.sign(g))) <= 2 * ulp), p_new
     assert np.allclose(m, 0.1 * g, rtol=2e-7) and np.allclose(v, 0.001 * g * g, rtol=4e-7)
+
+
+def test_eps_beside_the_root(O=O_real):
+    # A gradient as small as eps: on the first step m_hat = g and
+    # sqrt(v_hat) = |g|, so the step is lr * g / (|g| + eps) = lr / 2 * sign(g)
+    # when |g| = eps (eps inside the root, or squared, gives about lr instead)
+    sc = O.adamw_scalars(1.0, 0.9, 0.999, 1e-8, 0.0, 1)
+    g = np.array([1e-8, -1e-8], np.float32)
+    p = np.zeros(2, np.float32)
+    p_new, _, _ = O.adamw_update(p, np.zeros(2, np.float32), np.zeros(2, np.float32), g, sc, True)
+    assert np.allclose(p_new, [-0.5, 0.5], rtol=1e-5), p_new
 
 
 def test_decoupled_weight_decay_on_zero_gradient(O=O_real):

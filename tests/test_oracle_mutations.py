@@ -97,6 +97,10 @@ MUTANTS = {
     "select_twice_per_score": ("        self.scored_step = None\n        self.mask = mask\n        self.mask_step = step", "        self.mask = mask\n        self.mask_step = step"),
     "delta_accumulated_in_fp32": ("            if self.mode == MODE_ACCUM:\n                self.delta[l] = self.delta[l] + u",
                                   "            if self.mode == MODE_ACCUM:\n                self.delta[l] = float(np.float32(self.delta[l] + u))"),
+    "restore_keeps_pending_selection": ("        self.mask = None\n        self.unpacked = set()\n        return chosen",
+                                        "        self.mask = None\n        return chosen"),
+    "adamw_eps_squared": ('    denom = (np.sqrt(v_hat).astype(f) + sc["eps"]).astype(f)',
+                          '    denom = (np.sqrt(v_hat).astype(f) + sc["eps"] * sc["eps"]).astype(f)'),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
@@ -179,7 +183,7 @@ def all_checks(M):
     for mode in (O.MODE_ACCUM, O.MODE_SNAPSHOT):
         yield lambda mode=mode: run_bruteforce(M, mode, O.DT_BF16, 0, steps=12)
     for chk in (A.test_first_step_is_lr_times_sign, A.test_decoupled_weight_decay_on_zero_gradient,
-                A.test_matches_torch_adamw_over_steps, A.test_fused_step_drift_is_eq1_on_the_parameters,
+                A.test_matches_torch_adamw_over_steps, A.test_eps_beside_the_root, A.test_fused_step_drift_is_eq1_on_the_parameters,
                 G.test_closed_form_exact, G.test_decay_and_gradient_together, G.test_decoupled_weight_decay,
                 G.test_matches_torch_sgd,
                 G.test_drift_is_eq1_on_the_parameters):
