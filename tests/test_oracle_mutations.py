@@ -101,6 +101,38 @@ MUTANTS = {
                                         "        self.mask = None\n        return chosen"),
     "adamw_eps_squared": ('    denom = (np.sqrt(v_hat).astype(f) + sc["eps"]).astype(f)',
                           '    denom = (np.sqrt(v_hat).astype(f) + sc["eps"] * sc["eps"]).astype(f)'),
+    "age_off_by_one": ("age = step - t_last[l]", "age = step - t_last[l] - 1"),
+    "plan_allows_duplicate_steps": ('        if dup:\n            raise OracleError(LC_ERR_INVALID_ARG, f"layer {l}: two versions at step {best_step}")\n', ""),
+    "plan_falls_back_silently": ('        if best is None:\n            raise OracleError(LC_ERR_NO_VERSION, f"layer {l}: no persisted version <= {t_fail}")\n',
+                                 "        if best is None:\n            best = 0\n"),
+    "capacity_error_dropped": ('        if last == first_rank and first_rank < len(sel):\n            raise OracleError(LC_ERR_CAPACITY, "record does not fit")\n', ""),
+    "record_segments_reversed": ("            for s in g:\n                raw = getattr(s, arr).tobytes()",
+                                 "            for s in reversed(g):\n                raw = getattr(s, arr).tobytes()"),
+    "restore_segments_reversed": ("                for s in self.by_layer[l]:\n                    dst = getattr(s, arr)",
+                                  "                for s in reversed(self.by_layer[l]):\n                    dst = getattr(s, arr)"),
+    "plan_skips_payload_check": ('            if len(v["payload"]) != need:\n                raise OracleError(LC_ERR_INVALID_ARG, "payload size does not match mask")\n', ""),
+    "restore_reads_unpadded": ("                    pos += padded(nb)", "                    pos += nb"),
+    "adamw_bias_step_off_by_one": ('"c1": f(1.0 / (1.0 - beta1 ** t)), "c2": f(1.0 / (1.0 - beta2 ** t)),',
+                                   '"c1": f(1.0 / (1.0 - beta1 ** (t + 1))), "c2": f(1.0 / (1.0 - beta2 ** (t + 1))),'),
+    "adamw_decay_after_update": ('    p1 = (p * sc["decay"]).astype(f) if decayed else p.astype(f)\n    p_new = (p1 - (sc["lr"] * upd).astype(f)).astype(f)',
+                                 '    p_new = (p - (sc["lr"] * upd).astype(f)).astype(f)\n    p_new = (p_new * sc["decay"]).astype(f) if decayed else p_new'),
+    "adamw_m_hat_from_old_m": ('    m_hat = (m_new * sc["c1"]).astype(f)', '    m_hat = (m * sc["c1"]).astype(f)'),
+    "adamw_c2_uses_beta1": ('"c2": f(1.0 / (1.0 - beta2 ** t)),', '"c2": f(1.0 / (1.0 - beta1 ** t)),'),
+    "optim_reads_weights_not_master": ("            if s.master is not None:\n                p_old = s.master.copy()",
+                                       "            if False:\n                p_old = s.master.copy()"),
+    "optim_master_not_written": ("            if s.master is not None:\n                s.master[...] = p_new",
+                                 "            if False:\n                s.master[...] = p_new"),
+    "optim_drift_without_eps": ("_, _, _, u = layer_update_score([s._p_new for s in g], [s._p_old for s in g], DT_F32, self.eps_w)",
+                                "_, _, _, u = layer_update_score([s._p_new for s in g], [s._p_old for s in g], DT_F32, 0.0)"),
+    "optim_drift_on_stored_weights": ("_, _, _, u = layer_update_score([s._p_new for s in g], [s._p_old for s in g], DT_F32, self.eps_w)",
+                                      "_, _, _, u = layer_update_score([s.weight for s in g], [s.shadow for s in g], self.dtype, self.eps_w)"),
+    "eps_in_numerator_too": ("np.float64(A / n) / np.float64(B / n + eps_w)", "np.float64(A / n + eps_w) / np.float64(B / n + eps_w)"),
+    "restore_strict_t_fail": ('if v["step"] <= t_fail and v["mask"][l]:', 'if v["step"] < t_fail and v["mask"][l]:'),
+    "select_resets_every_timestamp": ("            if mask[l]:  # Eq. 4: reset on persist\n                self.delta[l] = 0.0\n                self.t_last[l] = step",
+                                      "            if mask[l]:  # Eq. 4: reset on persist\n                self.delta[l] = 0.0\n            self.t_last[l] = step"),
+    "weighted_age_over_layer_count": ('            "weighted_age": float(num) / float(den),', '            "weighted_age": float(num) / float(self.N),'),
+    "stats_max_age_is_min": ('            "max_age": max(ages),', '            "max_age": min(ages),'),
+    "pack_reports_done_early": ('"next_rank": last, "done": int(last == len(sel))}', '"next_rank": last, "done": 1}'),
     "weighted_by_count_not_size": ("num = sum(self.n[l] * ages[l] for l in range(self.N))",
                                    "num = sum(ages[l] for l in range(self.N)) * sum(self.n) // self.N"),
     "rebase_keeps_delta": ("            self.delta[l] = 0.0\n            self.t_last[l] = step\n            for s in g:",
